@@ -1,0 +1,211 @@
+"""Pins for the oracle's linearizer (CPU only).
+
+The definitional linearizer is checked against things fixed outside it:
+closed forms of perfect trees, caterpillars and grid DAGs; the paper's own DFS
+linearizer (Sec. 4.2) on post-order-numbered forests; the barrier invariant of
+Appendix A.4 (no node of a batch is a child of another node of that batch);
+the contiguity of batches (Appendix B); and brute force over every small shape.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import cortex_oracle as O
+from paper_2011_01383_amd import inputs as I
+
+
+def level_sizes(lin):
+    off = lin["level_offsets"]
+    return [int(off[i + 1] - off[i]) for i in range(int(lin["num_levels"]))]
+
+
+def check_invariants(children, K, lin):
+    N = children.size // K
+    L = int(lin["num_levels"])
+    off = lin["level_offsets"]
+    h = lin["height"]
+    assert off[0] == 0 and off[L] == N
+    assert all(off[i + 1] > off[i] for i in range(L)), "every level is non-empty"
+    # rows are a permutation, node_row is its inverse
+    assert sorted(lin["level_nodes"].tolist()) == list(range(N))
+    assert (lin["node_row"][lin["level_nodes"]] == np.arange(N)).all()
+    for lvl in range(L):
+        rows = range(off[lvl], off[lvl + 1])
+        ids = [int(lin["level_nodes"][r]) for r in rows]
+        assert all(h[v] == lvl for v in ids)
+        assert ids == sorted(ids), "stable: ascending id inside a level"
+        ids_set = set(ids)
+        for r in rows:
+            for s in range(K):
+                cr = int(lin["child_rows"][r * K + s])
+                c = int(children[int(lin["level_nodes"][r]) * K + s])
+                assert (cr < 0) == (c < 0)
+                if cr >= 0:
+                    assert int(lin["level_nodes"][cr]) == c
+                    # barrier invariant: children live in strictly lower levels
+                    assert cr < off[lvl] and c not in ids_set
+        if lvl > 0:
+            # height definition: some child sits exactly one level below
+            for r in rows:
+                kids = [int(lin["child_rows"][r * K + s]) for s in range(K)]
+                assert max(h[int(lin["level_nodes"][k])] for k in kids if k >= 0) == lvl - 1
+
+
+@pytest.mark.parametrize("height", [0, 1, 2, 3, 5, 7])
+def test_perfect_tree_closed_form(height):
+    children, _ = I.forest_to_children([I.perfect_tree(height)], 2)
+    lin = O.linearize(children, 2)
+    assert level_sizes(lin) == [2 ** (height - l) for l in range(height + 1)]
+    check_invariants(children, 2, lin)
+
+
+@pytest.mark.parametrize("n_leaves,left", [(1, True), (2, True), (9, True), (9, False), (40, False)])
+def test_caterpillar_closed_form(n_leaves, left):
+    children, _ = I.forest_to_children([I.caterpillar(n_leaves, left)], 2)
+    lin = O.linearize(children, 2)
+    assert level_sizes(lin) == [n_leaves] + [1] * (n_leaves - 1)
+    check_invariants(children, 2, lin)
+
+
+@pytest.mark.parametrize("g,R,C", [(1, 1, 1), (1, 2, 3), (3, 4, 4), (2, 5, 3)])
+def test_grid_dag_closed_form(g, R, C):
+    children = I.grid_children(g, R, C)
+    lin = O.linearize(children, 2)
+    h = lin["height"]
+    for gi in range(g):
+        for i in range(R):
+            for j in range(C):
+                assert h[gi * R * C + i * C + j] == i + j
+    sizes = level_sizes(lin)
+    assert sizes == [g * sum(1 for i in range(R) if 0 <= l - i < C) for l in range(R + C - 1)]
+    # rows of level l: grid-major, then i ascending (the ids are increasing)
+    for l in range(R + C - 1):
+        rows = lin["level_nodes"][lin["level_offsets"][l]:lin["level_offsets"][l + 1]]
+        expect = [gi * R * C + i * C + (l - i) for gi in range(g) for i in range(R) if 0 <= l - i < C]
+        assert rows.tolist() == expect
+    check_invariants(children, 2, lin)
+
+
+def test_full_grid_workload_closed_form():
+    wl = I.make_workload(4)
+    lin = O.linearize(wl.children, 2)
+    assert int(lin["num_levels"]) == 63
+    assert level_sizes(lin) == [64 * min(l + 1, 63 - l) for l in range(63)]
+
+
+def _paper_rows(children, K):
+    leaf_batch, internal = O.paper_linearize_trees(children, K)
+    return leaf_batch + [v for b in internal for v in b], [len(leaf_batch)] + [len(b) for b in internal]
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 3])
+@pytest.mark.parametrize("j", [0, 1, 2])
+def test_matches_paper_linearizer_on_workloads(k, j):
+    wl = I.make_workload(k, j)
+    lin = O.linearize(wl.children, wl.K)
+    rows, sizes = _paper_rows(wl.children, wl.K)
+    assert lin["level_nodes"].tolist() == rows
+    assert level_sizes(lin) == sizes
+    check_invariants(wl.children, wl.K, lin)
+
+
+def _all_binary_shapes(n):
+    if n == 1:
+        return [[]]
+    out = []
+    for k in range(1, n):
+        for l in _all_binary_shapes(k):
+            for r in _all_binary_shapes(n - k):
+                out.append([l, r])
+    return out
+
+
+def _all_ordered_trees(n, max_arity):
+    """Every ordered tree with exactly n nodes and arity <= max_arity."""
+    if n == 1:
+        return [[]]
+    out = []
+
+    def forests(m, slots):
+        if m == 0:
+            yield []
+            return
+        if slots == 0:
+            return
+        for first in range(1, m + 1):
+            for t in _all_ordered_trees(first, max_arity):
+                for rest in forests(m - first, slots - 1):
+                    yield [t] + rest
+
+    for f in forests(n - 1, max_arity):
+        out.append(f)
+    return out
+
+
+def test_catalan_counts():
+    # brute-force enumerators are themselves pinned by their counting sequences
+    assert [len(_all_binary_shapes(n)) for n in range(1, 8)] == [1, 1, 2, 5, 14, 42, 132]
+    assert [len(_all_ordered_trees(n, 4)) for n in range(1, 7)] == [1, 1, 2, 5, 14, 41]
+
+
+def test_brute_force_small_trees_vs_paper_linearizer():
+    rng = np.random.default_rng(5)
+    shapes = [s for n in range(1, 8) for s in _all_binary_shapes(n)]
+    for shape in shapes:
+        children, _ = I.forest_to_children([shape], 2)
+        lin = O.linearize(children, 2)
+        rows, sizes = _paper_rows(children, 2)
+        assert lin["level_nodes"].tolist() == rows and level_sizes(lin) == sizes
+        check_invariants(children, 2, lin)
+        # relabeling: the level of each node is unchanged, rows re-sort by the new ids
+        N = children.size // 2
+        perm = rng.permutation(N).astype(np.int32)
+        ch2 = I.relabel(children, 2, perm)
+        lin2 = O.linearize(ch2, 2)
+        assert (lin2["height"][perm] == lin["height"]).all()
+        check_invariants(ch2, 2, lin2)
+    for n in range(1, 8):
+        for t in _all_ordered_trees(n, 4):
+            children, _ = I.forest_to_children([t], 4)
+            lin = O.linearize(children, 4)
+            rows, sizes = _paper_rows(children, 4)
+            assert lin["level_nodes"].tolist() == rows and level_sizes(lin) == sizes
+
+
+def test_forest_of_mixed_heights_shares_levels():
+    trees = [I.perfect_tree(2), [], I.caterpillar(4)]
+    children, _ = I.forest_to_children(trees, 2)
+    lin = O.linearize(children, 2)
+    # heights 2, 0, 3 -> L = 4; level 0 = 4 + 1 + 4 leaves
+    assert int(lin["num_levels"]) == 4
+    assert level_sizes(lin) == [9, 3, 2, 1]
+    check_invariants(children, 2, lin)
+
+
+def test_dag_with_shared_children_and_duplicates():
+    # node 3 -> (1, 2), node 4 -> (3, 3) duplicate, node 2 -> (1, -1), node 5 -> (0, 4)
+    children = np.array([-1, -1, -1, -1, 1, -1, 1, 2, 3, 3, 0, 4], dtype=np.int32)
+    lin = O.linearize(children, 2)
+    assert lin["height"].tolist() == [0, 0, 1, 2, 3, 4]
+    check_invariants(children, 2, lin)
+
+
+def test_random_dags_invariants():
+    rng = np.random.default_rng(11)
+    for trial in range(30):
+        N = int(rng.integers(1, 60))
+        K = int(rng.integers(1, 5))
+        ch = I.random_dag(rng, N, K)
+        check_invariants(ch, K, O.linearize(ch, K))
+
+
+def test_errors():
+    with pytest.raises(O.ChildRangeError):
+        O.linearize(np.array([1, -1, 2, -1], dtype=np.int32), 2)   # child 2 >= N
+    with pytest.raises(O.ChildRangeError):
+        O.linearize(np.array([-2, -1], dtype=np.int32), 2)
+    with pytest.raises(O.CycleError):
+        O.linearize(np.array([1, -1, 0, -1], dtype=np.int32), 2)   # 0 -> 1 -> 0
+    with pytest.raises(O.CycleError):
+        O.linearize(np.array([0], dtype=np.int32), 1)              # self loop
