@@ -1,0 +1,221 @@
+"""Benchmark of the level-synchronous recursive-inference hot path on one GPU.
+
+One step = one pass of the whole path over one batch: cortex_linearize (node
+heights, level lists, child rows) followed by the fused persistent forward
+kernel, both enqueued on one stream with the inputs already resident in HBM.
+
+Default workload: binary N-ary TreeLSTM, hidden 256, a batch of 10 random
+binary trees with 10-40 leaves each (seeded synthetic stand-in for the SST
+trees of the paper's TreeLSTM evaluation).
+
+Prints ONE JSON line with the contract fields plus:
+  roofline      the forward kernel's achieved algorithmic FLOP/s (or GB/s) from
+                its own HIP-event-timed launches, against the MI355X peak
+  cpu_baseline  the fp64 oracle timed on this host's cores over a bounded sample
+  breakdown     latency percentiles and the linearize / forward split
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "batch inference latency (ms) + nodes/sec; fraction of HBM/FLOP roofline"
+PEAK_FP32_TFLOPS = 157.3        # MI355X dense fp32 (MFMA and vector)
+PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
+
+
+def algorithmic_work(wl):
+    """(flops, bytes) the method must do for one batch.
+
+    Flops: 2 per multiply-add of the contractions actually needed (present
+    child slots only, leaves of TreeRNN / N-ary / MV-RNN are copies) plus one
+    per bias add.  Bytes: weights read once, inputs gathered once, every
+    output state written once, the int32 structure read once.
+    """
+    H, K, N = wl.H, wl.K, wl.N
+    ch = wl.children.reshape(N, K)
+    present = ch >= 0
+    E = int(present.sum())
+    n_int = int(present.any(1).sum())
+    n_leaf = N - n_int
+    f4 = 4
+    struct_bytes = N * K * 4 + N * 4
+    if wl.cell == "tree_rnn":
+        flops = E * 2 * H * H + n_int * H
+        byts = (2 * H * H + H) * f4 + n_leaf * H * f4 + N * H * f4 + struct_bytes
+    elif wl.cell == "nary_treelstm":
+        flops = E * 2 * H * 5 * H + n_int * 5 * H
+        byts = (2 * 5 * H * H + 5 * H) * f4 + n_leaf * H * f4 + 2 * N * H * f4 + struct_bytes
+    elif wl.cell == "childsum_treelstm":
+        flops = N * (2 * H * 4 * H + 4 * H) + n_int * 2 * H * 3 * H + E * 2 * H * H
+        byts = (8 * H * H + 4 * H) * f4 + N * H * f4 + 2 * N * H * f4 + struct_bytes
+    elif wl.cell == "mvrnn":
+        flops = n_int * (2 * H * 2 * H * H + 2 * 2 * H * H + 2 * H * 2 * H)
+        byts = (2 * H * 2 * H) * f4 + n_leaf * (H * H + H) * f4 + N * (H * H + H) * f4 + struct_bytes
+    else:  # dagrnn
+        flops = N * (2 * H * H + H) + E * 2 * H * H
+        byts = (3 * H * H + H) * f4 + N * H * f4 + N * H * f4 + struct_bytes
+    return float(flops), float(byts)
+
+
+def bound_of(flops, byts):
+    """The roofline that bounds the algorithm: the larger ideal time wins."""
+    t_f = flops / (PEAK_FP32_TFLOPS * 1e12)
+    t_b = byts / (PEAK_HBM_GBS * 1e9)
+    return "mfma" if t_f >= t_b else "hbm"
+
+
+def cpu_baseline(wl, seconds):
+    """The fp64 oracle (linearize + recursive forward) on a bounded sample."""
+    from oracle import cortex_oracle as O
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=1)
+    except Exception:          # threadpoolctl missing: BLAS may use more threads
+        limiter = None
+    runs = 0
+    t0 = time.perf_counter()
+    while True:
+        O.linearize(wl.children, wl.K)
+        O.forward_workload(wl)
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    if limiter is not None:
+        limiter.unregister()
+    return {"value": wl.N * runs / el, "unit": "nodes/s", "cores": 1, "kind": "oracle",
+            "sample": "%d full passes of the %d-node batch (linearize + forward, fp64, 1 thread) in %.1f s"
+                      % (runs, wl.N, el)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=1, help="0..4: tree_rnn, nary, childsum, mvrnn, dag")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--node-groups", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the path shards by whole trees/grids with no "
+              "exchange, and runs on more than one GPU are not part of this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2011_01383_amd import cortex as C
+    from paper_2011_01383_amd import inputs as I
+    from paper_2011_01383_amd.runner import DeviceWorkload
+
+    if not os.path.exists(C.LIB_PATH):
+        from paper_2011_01383_amd import build
+        build.build()
+    torch.cuda.set_device(0)
+    wl = I.make_workload(args.workload)
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, args.node_groups)
+    dw = DeviceWorkload(wl)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        dw.step()
+    torch.cuda.synchronize()
+    assert dw.status_code() == 0, "device status %d" % dw.status_code()
+
+    # ---- timed region: exactly K steps ----
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g0 = torch.cuda.Event(enable_timing=True)
+    g1 = torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        dw.step()
+        ev[i][1].record(stream)
+    g1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = g0.elapsed_time(g1)
+    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    assert dw.status_code() == 0
+    ms_per_step = total_ms / args.steps
+
+    # ---- per-kernel timing (HIP events on the launch stream) ----
+    def time_calls(fn, n):
+        es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for a, b in es:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in es])
+
+    n_k = max(20, min(args.steps, 200))
+    lin_ms = time_calls(dw.linearize, n_k)
+    fwd_ms = time_calls(dw.forward, n_k)
+    assert dw.status_code() == 0
+
+    flops, byts = algorithmic_work(wl)
+    bound = bound_of(flops, byts)
+    fwd_avg_s = float(fwd_ms.mean()) / 1e3
+    if bound == "mfma":
+        achieved = flops / fwd_avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None}
+    else:
+        achieved = byts / fwd_avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+    roof["kernel"] = "forward (%s)" % wl.cell
+    roof["kernel_avg_ms"] = float(fwd_ms.mean())
+    roof["algorithmic_flops"] = flops
+    roof["algorithmic_bytes"] = byts
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, args.cpu_seconds)
+
+    lin_host = dw.lin_host()
+    out = {
+        "metric": METRIC,
+        "value": wl.N / (ms_per_step / 1e3),
+        "unit": "nodes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded)",
+        "config": {"workload": wl.name, "cell": wl.cell, "hidden": wl.H, "nodes": wl.N,
+                   "levels": int(lin_host["num_levels"]), "max_arity": wl.K,
+                   "grid_linearize": C.cortex_last_grid(0), "grid_forward": C.cortex_last_grid(1)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "breakdown": {
+            "latency_ms_p10": float(np.percentile(step_ms, 10)),
+            "latency_ms_p50": float(np.percentile(step_ms, 50)),
+            "latency_ms_p90": float(np.percentile(step_ms, 90)),
+            "linearize_ms_p50": float(np.median(lin_ms)),
+            "forward_ms_p50": float(np.median(fwd_ms)),
+            "host_wall_s": wall,
+        },
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

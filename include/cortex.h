@@ -1,0 +1,201 @@
+/*
+ * cortex.h - C ABI of the MI355X (gfx950) level-synchronous recursive
+ * inference library.
+ *
+ * The library evaluates recursive models (tree RNNs, tree LSTMs, MV-RNN and
+ * grid DAG-RNNs) over a batch of trees or DAGs in two steps:
+ *
+ *   1. cortex_linearize   - data-structure linearization (Sec. 4.2 "Data
+ *                           Structure Linearization", numbering scheme of
+ *                           Appendix B): node heights, per-level node lists
+ *                           (dynamic batching, Sec. 3.1) and child rows.
+ *   2. cortex_tree_forward / cortex_dag_forward
+ *                         - the lowered loop nest of Sec. 4.1 ("RA Lowering":
+ *                           a leaf loop, then a loop over batches of nodes with
+ *                           one barrier per batch, Appendix A.4), run as ONE
+ *                           persistent kernel with the cell weights resident
+ *                           on chip (kernel fusion and model persistence,
+ *                           Sec. 7.2 and 7.3).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers named d_* are DEVICE memory owned by the caller.  The library
+ *   never allocates or frees memory.  Scratch space comes from the caller's
+ *   workspace (d_ws, ws_bytes); it must be zero-filled ONCE before its first
+ *   use and then passed back unchanged: the kernels leave it ready for the
+ *   next call.  Calls that overlap in time must use distinct workspaces.
+ * - stream is a hipStream_t (NULL = the default stream).  Every call only
+ *   enqueues work on it and returns; nothing is synchronised.
+ * - The return value reports host-detectable errors (CORTEX_E_*).  When a
+ *   call returns an error it has enqueued nothing.
+ * - Data-dependent errors are written by the kernels to *d_status (an int32
+ *   in device memory, CORTEX_ST_*; the caller sets it to 0 before the first
+ *   call and reads it after synchronising).  A kernel that finds *d_status
+ *   non-zero on entry writes no outputs, so a failed linearization makes the
+ *   following forward a no-op.
+ * - Results are deterministic: the same inputs give bitwise identical outputs
+ *   on the same GPU.
+ *
+ * Structure format (Sec. 3: a batch of trees or DAGs whose maximum number of
+ * children K is declared up front):
+ *   d_children[v*K + s] is the node id in child slot s of node v, or -1 when
+ *   the slot is empty.  Node ids are 0..N-1.  Any numbering is accepted.  A
+ *   node may be the child of several nodes (DAG), a slot may repeat a child.
+ */
+#ifndef CORTEX_H
+#define CORTEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- host return codes ------------------------------------------------ */
+#define CORTEX_OK 0
+#define CORTEX_E_INVAL (-1)       /* a NULL pointer, a negative size, K or H out of range */
+#define CORTEX_E_HIP (-2)         /* a HIP runtime call failed */
+#define CORTEX_E_TOO_LARGE (-3)   /* the launch cannot be made co-resident on the GPU */
+#define CORTEX_E_WORKSPACE (-4)   /* ws_bytes is smaller than the *_workspace_bytes figure */
+
+/* ---- device status codes (written to *d_status) -------------------------- */
+#define CORTEX_ST_OK 0
+#define CORTEX_ST_CHILD_RANGE 1      /* a child index outside [-1, N) */
+#define CORTEX_ST_CYCLE 2            /* the structure has a cycle (not a DAG) */
+#define CORTEX_ST_BARRIER_TIMEOUT 3  /* a device-wide barrier waited past its limit */
+#define CORTEX_ST_BAD_LINEARIZATION 4 /* forward was handed an inconsistent linearization */
+#define CORTEX_ST_INPUT_RANGE 5      /* an input index outside [-1, rows of the input table) */
+
+/* Cells (Sec. 7.1, Table "Models and datasets"). */
+#define CORTEX_TREE_RNN 0            /* h = tanh(W [h_l; h_r] + b); leaf h = x */
+#define CORTEX_NARY_TREELSTM 1       /* binary N-ary TreeLSTM; leaf (h, c) = (x, 0) */
+#define CORTEX_CHILDSUM_TREELSTM 2   /* child-sum TreeLSTM; input x at every node */
+#define CORTEX_MVRNN 3               /* MV-RNN; leaf (p, P) = (a, A) */
+
+/*
+ * Linearization (Sec. 4.2, Appendix B).  Every pointer is device memory
+ * allocated by the caller with the capacity shown; cortex_linearize fills it.
+ *
+ * height(v) = 0 for a node without children, else 1 + max height of its
+ * children.  Rows are the nodes sorted by (height, node id): level l (the l-th
+ * "batch" of dynamic batching) is the contiguous row range
+ * [level_offsets[l], level_offsets[l+1]), level 0 holds the leaves, and no row
+ * of a level is a child of another row of the same level.  This numbers the
+ * leaves first, the reverse of the paper's Appendix B scheme, with the same
+ * contiguity and the same one-compare leaf test (row < level_offsets[1]).
+ */
+typedef struct {
+  int32_t num_nodes;       /* N (input) */
+  int32_t max_arity;       /* K (input), 1..4 */
+  int32_t *num_levels;     /* [1]     L = 1 + max height (0 when N == 0) */
+  int32_t *height;         /* [N]     by node id */
+  int32_t *level_offsets;  /* [N+1]   capacity; the first L+1 entries are written */
+  int32_t *level_nodes;    /* [N]     row -> node id */
+  int32_t *node_row;       /* [N]     node id -> row */
+  int32_t *child_rows;     /* [N*K]   row r, slot s -> row of that child, or -1 */
+} cortex_lin_t;
+
+/* Cell weights, float32, row-major [out, in] (y = W x means y_o = sum_i W[o,i] x_i).
+ * Unused members are NULL.
+ *   TREE_RNN           W [H, 2H] (columns 0..H-1 act on slot 0, H..2H-1 on slot 1), b [H]
+ *   NARY_TREELSTM      U [2, 5, H, H] = (U_l, U_r), gates (i, f_l, f_r, o, u); b [5, H]
+ *   CHILDSUM_TREELSTM  W [4, H, H], U [4, H, H], gates (i, f, o, u); b [4, H]
+ *   MVRNN              W [H, 2H], W_M [H, 2H]
+ */
+typedef struct {
+  const float *W;
+  const float *U;
+  const float *b;
+  const float *W_M;
+} cortex_weights_t;
+
+/* ---- linearization -------------------------------------------------------- */
+
+/* Workspace bytes cortex_linearize needs for N nodes of arity K (0 if invalid). */
+size_t cortex_linearize_workspace_bytes(int32_t N, int32_t K);
+
+/*
+ * Linearize N nodes of maximum arity K (Sec. 4.2).
+ *   d_children  [N*K] int32, -1 = empty slot (not modified)
+ *   lin         output arrays (see cortex_lin_t); lin->num_nodes must equal N
+ *               and lin->max_arity must equal K
+ * Kernel-detected errors: CORTEX_ST_CHILD_RANGE, CORTEX_ST_CYCLE,
+ * CORTEX_ST_BARRIER_TIMEOUT (outputs are then undefined).
+ * N == 0 is an empty batch: it writes num_levels = 0.
+ */
+int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin,
+                     int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream);
+
+/* ---- forward ------------------------------------------------------------- */
+
+/* Workspace bytes the forward entry points need for a cell (or -1 for the
+ * DAG cell) with N nodes and hidden size H (0 if invalid). */
+size_t cortex_forward_workspace_bytes(int32_t cell, int32_t N, int32_t H);
+
+/*
+ * Forward pass of a tree cell over a linearized batch (the loop nest of
+ * Sec. 4.1: a specialized leaf loop, then one fused step per level).
+ *   cell        CORTEX_TREE_RNN / NARY_TREELSTM / CHILDSUM_TREELSTM / MVRNN
+ *   H           hidden size: 64 or 256 for TREE_RNN, NARY and CHILDSUM; 64 for MVRNN
+ *   lin         the output of cortex_linearize (K must be 2, or 1..4 for CHILDSUM)
+ *   d_x_table   [x_rows, H] float32: leaf vectors or an embedding table
+ *   d_x_index   [N] int32 by NODE ID: the input row of each node, -1 = none
+ *               (zero input).  TREE_RNN, NARY and MVRNN read it at leaves only;
+ *               CHILDSUM reads it at every node.
+ *   d_leaf_mat  MVRNN only: [x_rows, H, H] leaf matrices (row-major)
+ *   w           weights (layouts above)
+ *   d_h         [N, H] output, in ROW order (row r = node lin->level_nodes[r])
+ *   d_c_or_P    NARY/CHILDSUM: [N, H] memory cells; MVRNN: [N, H, H] matrices;
+ *               TREE_RNN: unused (may be NULL).  Row order.
+ * An absent child slot contributes a zero state (Sec. 4.3).
+ */
+int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,
+                        int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
+                        const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status,
+                        void *d_ws, size_t ws_bytes, void *stream);
+
+/*
+ * Forward pass of the DAG-RNN cell (recursive part of DAG-RNN, Sec. 7.1):
+ *   h(v) = tanh(W x(v) + U_0 h(slot 0) + U_1 h(slot 1) + b)
+ * (for image grids slot 0 is the node above, slot 1 the node to the left).
+ *   H      256 (or 64)
+ *   lin    the output of cortex_linearize with K == 2
+ *   d_x    [N, H] float32 input by NODE ID
+ *   d_W    [H, H];  d_U [2, H, H] (slot 0 then slot 1);  d_b [H]
+ *   d_h    [N, H] output in ROW order
+ * Every node, sources included, runs the cell; an empty slot contributes 0.
+ */
+int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, const float *d_W,
+                       const float *d_U, const float *d_b, float *d_h, int32_t *d_status,
+                       void *d_ws, size_t ws_bytes, void *stream);
+
+/* ---- tuning and diagnostics ---------------------------------------------- */
+
+/*
+ * Launch knobs, process-wide, read at each launch.  They change the schedule,
+ * never the results.
+ *   CORTEX_KNOB_LIN_BLOCKS          workgroups of the linearizer (0 = chosen from N)
+ *   CORTEX_KNOB_FWD_NODE_GROUPS     node groups of the forward; workgroups =
+ *                                   hidden slices x node groups (0 = fill the GPU)
+ *   CORTEX_KNOB_BARRIER_TIMEOUT_US  spin limit of one device-wide barrier wait in
+ *                                   microseconds (default 5,000,000; 0 makes every
+ *                                   wait time out at once, for tests of that path)
+ * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value.
+ */
+#define CORTEX_KNOB_LIN_BLOCKS 0
+#define CORTEX_KNOB_FWD_NODE_GROUPS 1
+#define CORTEX_KNOB_BARRIER_TIMEOUT_US 2
+int cortex_set_knob(int32_t knob, int64_t value);
+int64_t cortex_get_knob(int32_t knob);
+
+/* Workgroups the last launch of each kind used (for reports; host-side). */
+int32_t cortex_last_grid(int32_t which /* 0 = linearize, 1 = forward */);
+
+/* Library version string. */
+const char *cortex_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CORTEX_H */

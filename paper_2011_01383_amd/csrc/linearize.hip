@@ -1,0 +1,326 @@
+// Data-structure linearization on the GPU (Sec. 4.2, numbering of Appendix B).
+//
+// One persistent cooperative kernel computes, for N nodes of arity K:
+//   1. heights: height(v) = 0 without children, else 1 + max over children.
+//      Each workgroup owns a contiguous chunk of node ids held in LDS and
+//      relaxes it to a local fixed point (children outside the chunk are read
+//      from HBM); global rounds repeat until no workgroup changes a height.
+//      Values only grow and never exceed the true height, so the fixed point
+//      is the height; a value >= N proves a cycle.
+//   2. rows: a stable least-significant-digit counting sort of the node ids
+//      on height (8-bit digits, one pass while L <= 256).  Each pass builds
+//      per-tile digit histograms, scans them in (digit, tile) order and
+//      scatters every tile with wave-ballot ranking, which keeps equal keys
+//      in id order.  The result is the dynamic-batching order: level by level,
+//      ascending id inside a level.
+//   3. level offsets from the height steps along the sorted rows, and the
+//      child rows through node_row.
+#include "cortex_device.hpp"
+#include "cortex_host.hpp"
+
+namespace cortex {
+
+constexpr int kLinThreads = 256;
+constexpr int kLinWaves = kLinThreads / 64;
+constexpr int kTile = 1024;                  // radix tile
+constexpr int kSubs = kTile / 64;            // 64-item sub-chunks per tile
+constexpr int kSubsPerWave = kSubs / kLinWaves;
+constexpr int kMaxChunk = 8192;              // heights per workgroup held in LDS
+constexpr int kTargetChunk = 1024;           // default chunk when the grid is free
+
+// kernel-specific sync words
+constexpr int kWordFlag0 = 0;                // 3 rotating "changed" flags: words 0..2
+constexpr int kWordMaxH = 3;
+constexpr int kLinWords = 4;
+
+struct LinArgs {
+  const int32_t *children;
+  int32_t N, K;
+  int32_t *num_levels, *height, *level_offsets, *level_nodes, *node_row, *child_rows;
+  int32_t *status;
+  unsigned int *sync;
+  int32_t *tile_hist;          // [256 * tiles]
+  int32_t *perm_a, *perm_b;    // [N] ping-pong between sort passes
+  int32_t chunk, tiles;
+  uint64_t timeout;
+};
+
+__device__ __forceinline__ int lds_load(const int *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_store(int *p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
+  __shared__ int hs[kMaxChunk];
+  __shared__ int cnt[kSubs][256];
+  __shared__ int hist[256];
+  __shared__ int scan_tmp[kLinThreads];
+
+  const SyncWords sw{a.sync};
+  const int tid = threadIdx.x;
+  const int G = gridDim.x;
+  const int N = a.N, K = a.K;
+  const int lo = blockIdx.x * a.chunk;
+  const int hi = min(N, lo + a.chunk);
+  const int n = max(0, hi - lo);
+  bool ok = load_status(a.status) == 0;
+
+  // ---------------- 1. heights ----------------
+  for (int i = tid; i < n; i += kLinThreads) hs[i] = 0;
+  __syncthreads();
+  int round = 0;
+  while (ok) {
+    if (G > 1 && blockIdx.x == 0 && tid == 0)
+      __hip_atomic_store(sw.word(kWordFlag0 + (round + 1) % 3), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int block_changed = (round == 0);
+    int local_max = 0;
+    for (;;) {
+      int changed = 0, cyc = 0;
+      for (int i = tid; i < n; i += kLinThreads) {
+        const int v = lo + i;
+        int m = -1;
+        for (int s = 0; s < K; ++s) {
+          int c = a.children[(size_t)v * K + s];
+          if (c < -1 || c >= N) {
+            if (round == 0) raise_status(a.status, CORTEX_ST_CHILD_RANGE);
+            continue;
+          }
+          if (c < 0) continue;
+          int hc;
+          if (c >= lo && c < hi) hc = lds_load(&hs[c - lo]);
+          else if (round == 0) hc = 0;    // global heights not written yet: 0 is a lower bound
+          else hc = __hip_atomic_load(&a.height[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          m = max(m, hc);
+        }
+        const int nh = m + 1;
+        if (nh > lds_load(&hs[i])) {
+          lds_store(&hs[i], nh);
+          changed = 1;
+          if (nh >= N) {
+            raise_status(a.status, CORTEX_ST_CYCLE);
+            cyc = 1;
+          }
+        }
+      }
+      // uniform exit decision for the whole workgroup
+      const int any = __syncthreads_or(changed);
+      const int stop = __syncthreads_or(cyc);
+      block_changed |= any;
+      if (!any || stop) break;
+    }
+    for (int i = tid; i < n; i += kLinThreads) {
+      const int hv = hs[i];
+      a.height[lo + i] = hv;
+      local_max = max(local_max, hv);
+    }
+    // block-wide max of the chunk, folded into the global maximum
+    for (int off = 32; off > 0; off >>= 1) local_max = max(local_max, __shfl_xor(local_max, off));
+    if ((tid & 63) == 0) scan_tmp[tid >> 6] = local_max;
+    __syncthreads();
+    if (tid == 0) {
+      int mx = 0;
+      for (int w = 0; w < kLinWaves; ++w) mx = max(mx, scan_tmp[w]);
+      if (G == 1) {
+        *sw.word(kWordMaxH) = (unsigned)mx;
+      } else {
+        __hip_atomic_fetch_max(sw.word(kWordMaxH), (unsigned)mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (block_changed)
+          __hip_atomic_fetch_or(sw.word(kWordFlag0 + round % 3), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    ok = grid_sync(sw, a.status, a.timeout);
+    if (!ok) break;
+    if (G == 1) break;                                  // one chunk: local fixed point is global
+    const unsigned f = __hip_atomic_load(sw.word(kWordFlag0 + round % 3), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    ++round;
+    if (f == 0) break;
+  }
+
+  int L = 0;
+  if (ok) L = 1 + (int)__hip_atomic_load(sw.word(kWordMaxH), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // ---------------- 2. stable counting sort on height ----------------
+  int passes = 1;
+  for (int v = (L - 1) >> 8; v > 0; v >>= 8) ++passes;
+  const int T = a.tiles;
+  const int wave = tid >> 6, lane = tid & 63;
+  const unsigned long long lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+
+  for (int p = 0; ok && p < passes; ++p) {
+    const int shift = 8 * p;
+    const int32_t *in = (p == 0) ? nullptr : ((p & 1) ? a.perm_a : a.perm_b);
+    const bool last = (p == passes - 1);
+    int32_t *out = last ? a.level_nodes : ((p & 1) ? a.perm_b : a.perm_a);
+
+    // (a) per-tile digit histograms, stored digit-major
+    for (int t = blockIdx.x; t < T; t += G) {
+      hist[tid] = 0;
+      __syncthreads();
+      for (int i = tid; i < kTile; i += kLinThreads) {
+        const int idx = t * kTile + i;
+        if (idx < N) {
+          const int item = in ? in[idx] : idx;
+          atomicAdd(&hist[(a.height[item] >> shift) & 255], 1);
+        }
+      }
+      __syncthreads();
+      a.tile_hist[(size_t)tid * T + t] = hist[tid];
+      __syncthreads();
+    }
+    ok = grid_sync(sw, a.status, a.timeout);
+    if (!ok) break;
+
+    // (b) exclusive scan of the 256*T counts, by workgroup 0
+    if (blockIdx.x == 0) {
+      const int M = 256 * T;
+      const int seg = (M + kLinThreads - 1) / kLinThreads;
+      const int b0 = min(M, tid * seg), b1 = min(M, b0 + seg);
+      int sum = 0;
+      for (int i = b0; i < b1; ++i) sum += a.tile_hist[i];
+      scan_tmp[tid] = sum;
+      __syncthreads();
+      if (tid == 0) {
+        int run = 0;
+        for (int w = 0; w < kLinThreads; ++w) { int x = scan_tmp[w]; scan_tmp[w] = run; run += x; }
+      }
+      __syncthreads();
+      int run = scan_tmp[tid];
+      for (int i = b0; i < b1; ++i) { int x = a.tile_hist[i]; a.tile_hist[i] = run; run += x; }
+    }
+    ok = grid_sync(sw, a.status, a.timeout);
+    if (!ok) break;
+
+    // (c) stable scatter: rank = (digit base of this tile) + (equal digits
+    //     earlier in the tile).  Sub-chunk q of 64 items goes to wave q/4.
+    for (int t = blockIdx.x; t < T; t += G) {
+      for (int i = tid; i < kSubs * 256; i += kLinThreads) (&cnt[0][0])[i] = 0;
+      __syncthreads();
+      int item[kSubsPerWave], dig[kSubsPerWave], rank[kSubsPerWave];
+      bool valid[kSubsPerWave];
+#pragma unroll
+      for (int qq = 0; qq < kSubsPerWave; ++qq) {
+        const int q = wave * kSubsPerWave + qq;
+        const int idx = t * kTile + q * 64 + lane;
+        valid[qq] = idx < N;
+        item[qq] = valid[qq] ? (in ? in[idx] : idx) : 0;
+        dig[qq] = valid[qq] ? ((a.height[item[qq]] >> shift) & 255) : 0;
+        unsigned long long peers = __ballot(valid[qq]);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const bool bit = (dig[qq] >> b) & 1;
+          const unsigned long long m = __ballot(bit);
+          peers &= bit ? m : ~m;
+        }
+        rank[qq] = __popcll(peers & lt_mask);
+        if (valid[qq] && rank[qq] == 0) cnt[q][dig[qq]] = __popcll(peers);
+      }
+      __syncthreads();
+      {   // exclusive scan over sub-chunks, one digit per thread
+        int run = 0;
+        for (int q = 0; q < kSubs; ++q) { int x = cnt[q][tid]; cnt[q][tid] = run; run += x; }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int qq = 0; qq < kSubsPerWave; ++qq) {
+        if (!valid[qq]) continue;
+        const int q = wave * kSubsPerWave + qq;
+        const int pos = a.tile_hist[(size_t)dig[qq] * T + t] + cnt[q][dig[qq]] + rank[qq];
+        if (pos < 0 || pos >= N) {              // cannot happen for consistent counts
+          raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+          continue;
+        }
+        out[pos] = item[qq];
+        if (last) a.node_row[item[qq]] = pos;
+      }
+      __syncthreads();
+    }
+    ok = grid_sync(sw, a.status, a.timeout);
+  }
+
+  // ---------------- 3. level offsets and child rows ----------------
+  if (ok) {
+    const int gtid = blockIdx.x * kLinThreads + tid;
+    const int gstride = G * kLinThreads;
+    for (int r = gtid; r < N; r += gstride) {
+      const int h = a.height[a.level_nodes[r]];
+      const int hp = r > 0 ? a.height[a.level_nodes[r - 1]] : -1;
+      for (int l = hp + 1; l <= h; ++l) a.level_offsets[l] = r;
+      const int v = a.level_nodes[r];
+      for (int s = 0; s < K; ++s) {
+        const int c = a.children[(size_t)v * K + s];
+        a.child_rows[(size_t)r * K + s] = c < 0 ? -1 : a.node_row[c];
+      }
+    }
+    if (blockIdx.x == 0 && tid == 0) {
+      a.level_offsets[L] = N;
+      *a.num_levels = L;
+    }
+  }
+  grid_exit(sw, kLinWords);
+}
+
+static size_t lin_tiles(int32_t N) { return (size_t)(N + kTile - 1) / kTile; }
+
+}  // namespace cortex
+
+using namespace cortex;
+
+extern "C" size_t cortex_linearize_workspace_bytes(int32_t N, int32_t K) {
+  if (N < 0 || K < 1 || K > 4) return 0;
+  size_t b = kSyncBytes;
+  b += align_up(256 * lin_tiles(N) * sizeof(int32_t), 256);
+  b += 2 * align_up((size_t)N * sizeof(int32_t), 256);
+  return b;
+}
+
+extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin,
+                                int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream) {
+  if (!lin || !d_status || N < 0 || K < 1 || K > 4) return CORTEX_E_INVAL;
+  if (lin->num_nodes != N || lin->max_arity != K || !lin->num_levels) return CORTEX_E_INVAL;
+  if (N == 0) {
+    return hipMemsetAsync(lin->num_levels, 0, sizeof(int32_t), (hipStream_t)stream) == hipSuccess
+               ? CORTEX_OK : CORTEX_E_HIP;
+  }
+  if (!d_children || !lin->height || !lin->level_offsets || !lin->level_nodes || !lin->node_row ||
+      !lin->child_rows || !d_ws)
+    return CORTEX_E_INVAL;
+  if (ws_bytes < cortex_linearize_workspace_bytes(N, K)) return CORTEX_E_WORKSPACE;
+
+  const int cap = max_coresident(linearize_kernel, kLinThreads, 0);
+  if (cap <= 0) return CORTEX_E_HIP;
+  int64_t g = knob(CORTEX_KNOB_LIN_BLOCKS);
+  if (g <= 0) g = (N + kTargetChunk - 1) / kTargetChunk;
+  const int64_t g_min = (N + kMaxChunk - 1) / kMaxChunk;
+  if (g < g_min) g = g_min;
+  if (g > N) g = N;
+  if (g > cap) {
+    if (g_min > cap) return CORTEX_E_TOO_LARGE;
+    g = cap;
+  }
+  LinArgs a;
+  a.children = d_children;
+  a.N = N;
+  a.K = K;
+  a.num_levels = lin->num_levels;
+  a.height = lin->height;
+  a.level_offsets = lin->level_offsets;
+  a.level_nodes = lin->level_nodes;
+  a.node_row = lin->node_row;
+  a.child_rows = lin->child_rows;
+  a.status = d_status;
+  char *ws = (char *)d_ws;
+  a.sync = (unsigned int *)ws;
+  ws += kSyncBytes;
+  a.tiles = (int32_t)lin_tiles(N);
+  a.tile_hist = (int32_t *)ws;
+  ws += align_up(256 * (size_t)a.tiles * sizeof(int32_t), 256);
+  a.perm_a = (int32_t *)ws;
+  ws += align_up((size_t)N * sizeof(int32_t), 256);
+  a.perm_b = (int32_t *)ws;
+  a.chunk = (int32_t)((N + g - 1) / g);
+  a.timeout = barrier_timeout_ticks();
+  set_last_grid(0, (int32_t)g);
+  return launch_coop(linearize_kernel, (int)g, kLinThreads, 0, a, stream);
+}

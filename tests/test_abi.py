@@ -1,0 +1,78 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+declared in include/cortex.h, and rejects bad arguments on the host before
+enqueuing anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2011_01383_amd import cortex as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cortex.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(cortex_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(C.LIB_PATH):
+        from paper_2011_01383_amd import build
+        build.build()
+    return C.load()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("cortex_linearize", "cortex_tree_forward", "cortex_dag_forward",
+                     "cortex_linearize_workspace_bytes", "cortex_forward_workspace_bytes"):
+        assert required in names
+    assert sorted(C.EXPORTED) == names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version(lib):
+    assert "gfx950" in C.cortex_version()
+
+
+def test_workspace_sizes(lib):
+    assert C.cortex_linearize_workspace_bytes(10, 5) == 0          # K out of range
+    assert C.cortex_linearize_workspace_bytes(-1, 2) == 0
+    small = C.cortex_linearize_workspace_bytes(100, 2)
+    big = C.cortex_linearize_workspace_bytes(100000, 2)
+    assert 0 < small < big
+    assert big >= 2 * 100000 * 4                                  # two permutation buffers
+    assert C.cortex_forward_workspace_bytes(1, 368, 256) > 0
+    assert C.cortex_forward_workspace_bytes(9, 368, 256) == 0
+
+
+def test_host_validation_returns_before_any_device_work(lib):
+    lin = C.cortex_lin_t(10, 2, None, None, None, None, None, None)
+    # K out of range, N mismatch, NULL status: all rejected on the host
+    assert lib.cortex_linearize(None, 10, 5, ctypes.byref(lin), None, None, 0, None) == C.CORTEX_E_INVAL
+    assert lib.cortex_linearize(None, 11, 2, ctypes.byref(lin), ctypes.c_void_p(8), None, 0, None) == C.CORTEX_E_INVAL
+    assert lib.cortex_linearize(None, 10, 2, None, ctypes.c_void_p(8), None, 0, None) == C.CORTEX_E_INVAL
+    w = C.cortex_weights_t(None, None, None, None)
+    assert lib.cortex_tree_forward(7, 256, ctypes.byref(lin), None, 0, None, None, ctypes.byref(w),
+                                   None, None, ctypes.c_void_p(8), None, 0, None) == C.CORTEX_E_INVAL
+    assert lib.cortex_dag_forward(256, None, None, None, None, None, None, None, None, 0, None) == C.CORTEX_E_INVAL
+
+
+def test_knobs(lib):
+    old = C.cortex_get_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS)
+    assert C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, 3) == C.CORTEX_OK
+    assert C.cortex_get_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS) == 3
+    assert C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, old) == C.CORTEX_OK
+    assert C.cortex_set_knob(99, 1) == C.CORTEX_E_INVAL
+    assert C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, -1) == C.CORTEX_E_INVAL
+    assert C.cortex_get_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US) > 0

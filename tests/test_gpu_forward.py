@@ -1,0 +1,165 @@
+"""GPU forward parity: every cell against the fp64 oracle, element by element,
+within 1e-4 max-abs and 1e-5 mean-abs, at the five full workloads (several
+seeds) and at small ragged sizes; plus schedule variants, determinism and the
+error paths."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cortex_oracle as O
+from paper_2011_01383_amd import cortex as C
+from paper_2011_01383_amd import inputs as I
+from paper_2011_01383_amd.runner import DeviceWorkload
+from tests.gpu_helpers import (announce, cached_oracle, cached_oracle_lin, cached_workload, compare_lin,
+                               compare_states, need_gpu)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    need_gpu()
+    yield
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, 0)
+    C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, 0)
+
+
+def run(wl, groups=0):
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, groups)
+    dw = DeviceWorkload(wl)
+    dw.h.fill_(float("nan"))
+    if dw.c is not None:
+        dw.c.fill_(float("nan"))
+    dw.step()
+    st = dw.status_code()
+    assert st == 0, "device status %d" % st
+    return dw
+
+
+@pytest.mark.parametrize("k", range(5))
+@pytest.mark.parametrize("j", range(3))
+def test_workload_parity(k, j):
+    wl = cached_workload(k, j)
+    announce("forward workload %d seed %d (%s N=%d)" % (k, j, wl.name, wl.N))
+    dw = run(wl)
+    compare_lin(dw.lin_host(), cached_oracle_lin(k, j), wl.K)
+    compare_states(dw.states_by_node(), cached_oracle(k, j), wl.name)
+
+
+SMALL = {
+    "tree_rnn_h64": lambda s: I.tree_rnn_workload(s, n_leaves=int(np.random.default_rng(s).integers(1, 80)), H=64),
+    "tree_rnn_h256": lambda s: I.tree_rnn_workload(s, n_leaves=37, H=256),
+    "nary_h64": lambda s: I.nary_treelstm_workload(s, batch=4, H=64, vocab=50, leaf_lo=1, leaf_hi=30),
+    "nary_h256": lambda s: I.nary_treelstm_workload(s, batch=3, H=256, vocab=50, leaf_lo=1, leaf_hi=25),
+    "childsum_h64": lambda s: I.childsum_treelstm_workload(s, batch=4, H=64, vocab=50, node_lo=1, node_hi=60),
+    "childsum_h256": lambda s: I.childsum_treelstm_workload(s, batch=3, H=256, vocab=50, node_lo=1, node_hi=40),
+    "mvrnn": lambda s: I.mvrnn_workload(s, batch=4, d=64, leaf_lo=1, leaf_hi=30),
+    "mvrnn_gain1": lambda s: I.mvrnn_workload(s, batch=3, d=64, leaf_lo=10, leaf_hi=40, wm_scale=0.153),
+    "dag_h64": lambda s: I.dagrnn_workload(s, n_grids=3, rows=7, cols=5, H=64),
+    "dag_h256": lambda s: I.dagrnn_workload(s, n_grids=2, rows=9, cols=11, H=256),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+@pytest.mark.parametrize("seed", [1, 2])
+@pytest.mark.parametrize("groups", [0, 1, 3])
+def test_small_ragged(name, seed, groups):
+    wl = SMALL[name](500 + seed)
+    announce("small %s seed %d groups %d N=%d" % (name, seed, groups, wl.N))
+    dw = run(wl, groups)
+    compare_states(dw.states_by_node(), O.forward_workload(wl), name)
+
+
+def test_single_leaf_trees():
+    for maker in (lambda: I.tree_rnn_workload(3, n_leaves=1, H=64),
+                  lambda: I.nary_treelstm_workload(3, batch=1, H=256, leaf_lo=1, leaf_hi=1),
+                  lambda: I.childsum_treelstm_workload(3, batch=1, H=256, node_lo=1, node_hi=1),
+                  lambda: I.mvrnn_workload(3, batch=1, leaf_lo=1, leaf_hi=1),
+                  lambda: I.dagrnn_workload(3, n_grids=1, rows=1, cols=1, H=256)):
+        wl = maker()
+        announce("single node %s" % wl.cell)
+        dw = run(wl)
+        compare_states(dw.states_by_node(), O.forward_workload(wl), wl.cell)
+
+
+def test_caterpillar_deep_levels():
+    """A 300-leaf caterpillar: 299 barrier-separated levels of one node."""
+    children, is_leaf = I.forest_to_children([I.caterpillar(300, True)], 2)
+    wl = I.nary_treelstm_workload(9, batch=1, H=256)
+    rng = np.random.default_rng(9)
+    wl.children = children
+    wl.x_index = np.where(is_leaf, rng.integers(0, 1000, is_leaf.size), -1).astype(np.int32)
+    announce("caterpillar 300")
+    dw = run(wl)
+    compare_states(dw.states_by_node(), O.forward_workload(wl), "caterpillar")
+
+
+def test_dag_input_with_shared_children():
+    """Tree cells accept DAGs: a node may be the child of several nodes."""
+    rng = np.random.default_rng(3)
+    ch = I.random_dag(rng, 400, 2, p_absent=0.2)
+    wl = I.tree_rnn_workload(4, n_leaves=2, H=64)
+    wl.children = ch
+    ch2 = ch.reshape(-1, 2)
+    leaf = (ch2 < 0).all(1)
+    wl.x_table = rng.standard_normal((int(leaf.sum()), 64)).astype(np.float32)
+    wl.x_index = np.where(leaf, np.cumsum(leaf) - 1, -1).astype(np.int32)
+    announce("tree_rnn over random DAG")
+    dw = run(wl)
+    compare_states(dw.states_by_node(), O.forward_workload(wl), "dag-tree_rnn")
+
+
+@pytest.mark.parametrize("k", range(5))
+def test_deterministic(k):
+    wl = cached_workload(k, 0)
+    announce("determinism workload %d" % k)
+    dw = run(wl)
+    first = dw.states_by_node()
+    for _ in range(5):
+        dw.step()
+        assert dw.status_code() == 0
+        again = dw.states_by_node()
+        for key in first:
+            np.testing.assert_array_equal(again[key], first[key])
+
+
+def test_failed_linearization_makes_forward_a_noop():
+    wl = I.nary_treelstm_workload(5, batch=2, H=256)
+    wl.children = wl.children.copy()
+    wl.children[-1] = wl.N - 1            # root becomes its own child: a cycle
+    announce("cycle -> forward no-op")
+    dw = DeviceWorkload(wl)
+    dw.h.fill_(float("nan"))
+    dw.step()
+    assert dw.status_code() == C.CORTEX_ST_CYCLE
+    assert torch.isnan(dw.h).all()
+
+
+def test_input_index_out_of_range():
+    wl = I.nary_treelstm_workload(6, batch=2, H=256)
+    leaf = np.where(wl.x_index >= 0)[0][0]
+    wl.x_index = wl.x_index.copy()
+    wl.x_index[leaf] = 5000                # beyond the 1000-row table
+    announce("x_index out of range")
+    dw = DeviceWorkload(wl)
+    dw.step()
+    assert dw.status_code() == C.CORTEX_ST_INPUT_RANGE
+
+
+def test_host_errors_enqueue_nothing():
+    wl = cached_workload(1, 0)
+    dw = DeviceWorkload(wl)
+    # unsupported hidden size
+    rc = C.cortex_tree_forward(C.CORTEX_NARY_TREELSTM, 100, dw.lin, dw.x_table, dw.x_rows, dw.x_index, None,
+                               U=dw.U, b=dw.b, h=dw.h, c_or_P=dw.c, status=dw.status, ws=dw.ws_fwd)
+    assert rc == C.CORTEX_E_INVAL
+    # workspace too small
+    small = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    rc = C.cortex_tree_forward(C.CORTEX_NARY_TREELSTM, 256, dw.lin, dw.x_table, dw.x_rows, dw.x_index, None,
+                               U=dw.U, b=dw.b, h=dw.h, c_or_P=dw.c, status=dw.status, ws=small)
+    assert rc == C.CORTEX_E_WORKSPACE
+    # more node groups than can be co-resident
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, 100000)
+    rc = C.cortex_tree_forward(C.CORTEX_NARY_TREELSTM, 256, dw.lin, dw.x_table, dw.x_rows, dw.x_index, None,
+                               U=dw.U, b=dw.b, h=dw.h, c_or_P=dw.c, status=dw.status, ws=dw.ws_fwd)
+    assert rc == C.CORTEX_E_TOO_LARGE

@@ -1,0 +1,196 @@
+"""GPU linearizer parity: bit-exact against the oracle's definitional
+linearization (Sec. 4.2) on the five workloads, closed forms, multi-pass
+sorts, random DAGs and error paths."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cortex_oracle as O
+from paper_2011_01383_amd import cortex as C
+from paper_2011_01383_amd import inputs as I
+from tests.gpu_helpers import announce, cached_oracle_lin, cached_workload, compare_lin, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    need_gpu()
+    yield
+    C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, 0)
+    C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 5000000)
+
+
+def gpu_linearize(children, K, blocks=0):
+    children = np.ascontiguousarray(children, dtype=np.int32)
+    N = children.size // K
+    C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, blocks)
+    d_children = torch.from_numpy(children).cuda() if N > 0 else torch.zeros(1, dtype=torch.int32, device="cuda")
+    lin = C.Linearization.alloc(N, K)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = C.workspace(C.cortex_linearize_workspace_bytes(N, K))
+    C.check(C.cortex_linearize(d_children, N, K, lin, status, ws), "cortex_linearize")
+    torch.cuda.synchronize()
+    st = int(status.item())
+    L = int(lin.num_levels.item())
+    out = None
+    if st == 0:
+        out = {"num_levels": np.int32(L), "height": lin.height[:N].cpu().numpy(),
+               "level_offsets": lin.level_offsets[:L + 1].cpu().numpy(),
+               "level_nodes": lin.level_nodes[:N].cpu().numpy(),
+               "node_row": lin.node_row[:N].cpu().numpy(),
+               "child_rows": lin.child_rows[:N * K].cpu().numpy()}
+    return st, out, (lin, status, ws, d_children)
+
+
+@pytest.mark.parametrize("k", range(5))
+@pytest.mark.parametrize("j", range(4))
+def test_workloads_bit_exact(k, j):
+    wl = cached_workload(k, j)
+    announce("linearize workload %d seed %d N=%d" % (k, j, wl.N))
+    st, got, _ = gpu_linearize(wl.children, wl.K)
+    assert st == 0
+    compare_lin(got, cached_oracle_lin(k, j), wl.K)
+
+
+@pytest.mark.parametrize("blocks", [1, 2, 5, 16, 64])
+def test_grid_dag_any_block_count(blocks):
+    wl = cached_workload(4, 0)
+    announce("linearize grid blocks=%d" % blocks)
+    st, got, _ = gpu_linearize(wl.children, 2, blocks)
+    assert st == 0
+    compare_lin(got, cached_oracle_lin(4, 0), 2)
+
+
+@pytest.mark.parametrize("height", [0, 1, 4, 9])
+def test_perfect_trees(height):
+    children, _ = I.forest_to_children([I.perfect_tree(height)], 2)
+    announce("perfect tree h=%d" % height)
+    st, got, _ = gpu_linearize(children, 2)
+    assert st == 0
+    compare_lin(got, O.linearize(children, 2), 2)
+
+
+@pytest.mark.parametrize("N,blocks", [(300, 0), (300, 3), (5000, 0), (100000, 0), (100000, 200)])
+def test_long_chain_multi_pass_closed_form(N, blocks):
+    """A chain of N nodes has L = N levels of one node each; L > 256 needs
+    two or three digit passes.  Node v has child v-1 (closed form, no oracle:
+    height(v) = v, every level holds one node, child row = row - 1)."""
+    children = np.full(N, -1, dtype=np.int32)
+    children[1:] = np.arange(N - 1, dtype=np.int32)
+    announce("chain N=%d blocks=%d" % (N, blocks))
+    st, got, _ = gpu_linearize(children, 1, blocks)
+    assert st == 0
+    ar = np.arange(N, dtype=np.int32)
+    assert int(got["num_levels"]) == N
+    np.testing.assert_array_equal(got["height"], ar)
+    np.testing.assert_array_equal(got["level_offsets"], np.arange(N + 1, dtype=np.int32))
+    np.testing.assert_array_equal(got["level_nodes"], ar)
+    np.testing.assert_array_equal(got["node_row"], ar)
+    np.testing.assert_array_equal(got["child_rows"], ar - 1)
+
+
+def test_reversed_chain_relabeled():
+    """Chain with ids descending (child has the higher id): exercises global
+    rounds that cross every chunk boundary."""
+    N = 3000
+    children = np.full(N, -1, dtype=np.int32)
+    children[:-1] = np.arange(1, N, dtype=np.int32)
+    announce("reversed chain N=%d" % N)
+    st, got, _ = gpu_linearize(children, 1, 6)
+    assert st == 0
+    np.testing.assert_array_equal(got["height"], (N - 1 - np.arange(N)).astype(np.int32))
+    np.testing.assert_array_equal(got["level_nodes"], (N - 1 - np.arange(N)).astype(np.int32))
+
+
+def test_random_dags_fuzz():
+    rng = np.random.default_rng(2024)
+    for trial in range(120):
+        N = int(rng.integers(1, 3000)) if trial % 4 else int(rng.integers(1, 12))
+        K = int(rng.integers(1, 5))
+        ch = I.random_dag(rng, N, K, p_absent=float(rng.uniform(0.0, 0.9)))
+        blocks = int(rng.choice([0, 1, 2, 3, 7]))
+        announce("fuzz trial %d N=%d K=%d blocks=%d" % (trial, N, K, blocks))
+        st, got, _ = gpu_linearize(ch, K, blocks)
+        assert st == 0, trial
+        compare_lin(got, O.linearize(ch, K), K)
+
+
+def test_relabeled_workloads():
+    rng = np.random.default_rng(7)
+    for k in range(4):
+        wl = cached_workload(k, 0)
+        perm = rng.permutation(wl.N).astype(np.int32)
+        ch = I.relabel(wl.children, wl.K, perm)
+        announce("relabeled workload %d" % k)
+        st, got, _ = gpu_linearize(ch, wl.K, 0)
+        assert st == 0
+        compare_lin(got, O.linearize(ch, wl.K), wl.K)
+
+
+def test_single_node_and_empty():
+    announce("N=1")
+    st, got, _ = gpu_linearize(np.array([-1, -1], np.int32), 2)
+    assert st == 0 and int(got["num_levels"]) == 1
+    np.testing.assert_array_equal(got["level_offsets"], [0, 1])
+    announce("N=0")
+    st, got, _ = gpu_linearize(np.zeros(0, np.int32), 2)
+    assert st == 0 and int(got["num_levels"]) == 0
+
+
+@pytest.mark.parametrize("blocks", [1, 4])
+def test_child_out_of_range(blocks):
+    ch = np.array([-1, -1, 0, 7, 1, 2], dtype=np.int32)     # child 7 >= N = 3
+    announce("range error blocks=%d" % blocks)
+    st, _, _ = gpu_linearize(ch, 2, blocks)
+    assert st == C.CORTEX_ST_CHILD_RANGE
+    ch = np.array([-1, -1, -5, 0], dtype=np.int32)
+    st, _, _ = gpu_linearize(ch, 2, blocks)
+    assert st == C.CORTEX_ST_CHILD_RANGE
+
+
+@pytest.mark.parametrize("blocks", [1, 3])
+def test_cycles(blocks):
+    announce("cycles blocks=%d" % blocks)
+    st, _, _ = gpu_linearize(np.array([0], np.int32), 1, 1)            # self loop
+    assert st == C.CORTEX_ST_CYCLE
+    N = 600                                                             # long cycle across chunks
+    ch = np.roll(np.arange(N, dtype=np.int32), 1)
+    st, _, _ = gpu_linearize(ch, 1, blocks)
+    assert st == C.CORTEX_ST_CYCLE
+    # a cycle hanging under a valid tree
+    ch = np.array([-1, -1, 0, 2, 3, -1, 1, -1], dtype=np.int32)   # 1 -> 2 -> 3 -> 1
+    st, _, _ = gpu_linearize(ch, 2, blocks)
+    assert st == C.CORTEX_ST_CYCLE
+
+
+def test_forced_barrier_timeout_then_recovery():
+    """A zero spin limit makes every barrier wait time out; the kernel must
+    report it and leave the workspace reusable."""
+    wl = cached_workload(4, 0)
+    announce("forced barrier timeout")
+    C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 0)
+    seen = set()
+    for _ in range(3):
+        st, _, keep = gpu_linearize(wl.children, 2, 64)
+        seen.add(st)
+    assert seen <= {0, C.CORTEX_ST_BARRIER_TIMEOUT}
+    assert C.CORTEX_ST_BARRIER_TIMEOUT in seen
+    C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 5000000)
+    # reuse the same workspace after the timeouts
+    lin, status, ws, d_children = keep
+    status.zero_()
+    C.check(C.cortex_linearize(d_children, wl.N, 2, lin, status, ws), "cortex_linearize")
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert int(lin.num_levels.item()) == 63
+
+
+def test_deterministic_repeats():
+    wl = cached_workload(1, 0)
+    announce("determinism")
+    st, first, _ = gpu_linearize(wl.children, 2)
+    for _ in range(20):
+        st2, again, _ = gpu_linearize(wl.children, 2)
+        assert st2 == 0
+        compare_lin(again, first, 2)
