@@ -21,9 +21,16 @@
  * ---------------------------------------
  * - Pointers named d_* are DEVICE memory owned by the caller.  The library
  *   never allocates or frees memory.  Scratch space comes from the caller's
- *   workspace (d_ws, ws_bytes); it must be zero-filled ONCE before its first
- *   use and then passed back unchanged: the kernels leave it ready for the
- *   next call.  Calls that overlap in time must use distinct workspaces.
+ *   workspace (d_ws, ws_bytes); it must be zero-filled before its first use
+ *   and then passed back unchanged: a call that ends with *d_status == 0
+ *   leaves it ready for the next call.  After a call that ends with a
+ *   non-zero status, zero the workspace again before reusing it.  Calls that
+ *   overlap in time must use distinct workspaces.
+ * - The kernels are persistent: every workgroup of a launch must be resident
+ *   at once.  A grid of at most one workgroup per compute unit is launched
+ *   with a plain launch (it is resident at once on a GPU not shared with
+ *   other persistent work); larger grids use the cooperative launch.  A
+ *   device-wide barrier never waits past its spin limit.
  * - stream is a hipStream_t (NULL = the default stream).  Every call only
  *   enqueues work on it and returns; nothing is synchronised.
  * - The return value reports host-detectable errors (CORTEX_E_*).  When a
@@ -181,11 +188,15 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *   CORTEX_KNOB_BARRIER_TIMEOUT_US  spin limit of one device-wide barrier wait in
  *                                   microseconds (default 5,000,000; 0 makes every
  *                                   wait time out at once, for tests of that path)
+ *   CORTEX_KNOB_COOPERATIVE         1 = always use the cooperative launch
+ *                                   (0 = only when the grid exceeds one
+ *                                   workgroup per compute unit)
  * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value.
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0
 #define CORTEX_KNOB_FWD_NODE_GROUPS 1
 #define CORTEX_KNOB_BARRIER_TIMEOUT_US 2
+#define CORTEX_KNOB_COOPERATIVE 3
 int cortex_set_knob(int32_t knob, int64_t value);
 int64_t cortex_get_knob(int32_t knob);
 

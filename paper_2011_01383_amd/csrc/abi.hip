@@ -1,17 +1,49 @@
 // Library-wide host state: launch knobs, the grids of the last launches and
 // the version string.
 #include <atomic>
+#include <map>
+#include <mutex>
 
 #include "cortex_host.hpp"
 
 namespace cortex {
 
-static std::atomic<int64_t> g_knobs[3] = {{0}, {0}, {5000000}};
+constexpr int kKnobs = 4;
+static std::atomic<int64_t> g_knobs[kKnobs] = {{0}, {0}, {5000000}, {0}};
 static std::atomic<int32_t> g_last_grid[2] = {{0}, {0}};
 
 int64_t knob(int32_t which) {
-  if (which < 0 || which > 2) return 0;
+  if (which < 0 || which >= kKnobs) return 0;
   return g_knobs[which].load();
+}
+
+// Per-device CU counts and per-kernel occupancies, queried once.
+constexpr int kMaxDevices = 64;
+static std::atomic<int> g_cus[kMaxDevices];
+static std::mutex g_occ_mu;
+static std::map<std::pair<const void *, int>, int> g_occ;
+
+int num_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  int c = g_cus[dev].load();
+  if (c > 0) return c;
+  if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  g_cus[dev].store(c);
+  return c;
+}
+
+int cached_occupancy(const void *kernel, int threads) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  std::lock_guard<std::mutex> lock(g_occ_mu);
+  auto key = std::make_pair(kernel, dev * 65536 + threads);
+  auto it = g_occ.find(key);
+  if (it != g_occ.end()) return it->second;
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return -1;
+  g_occ[key] = per_cu;
+  return per_cu;
 }
 
 void set_last_grid(int which, int32_t grid) {
@@ -21,7 +53,7 @@ void set_last_grid(int which, int32_t grid) {
 }  // namespace cortex
 
 extern "C" int cortex_set_knob(int32_t which, int64_t value) {
-  if (which < 0 || which > 2 || value < 0) return CORTEX_E_INVAL;
+  if (which < 0 || which >= cortex::kKnobs || value < 0) return CORTEX_E_INVAL;
   cortex::g_knobs[which].store(value);
   return CORTEX_OK;
 }

@@ -11,18 +11,28 @@
 namespace cortex {
 
 // ---------------------------------------------------------------------------
-// Workspace header.  Every persistent launch keeps its synchronisation words at
-// the start of the caller's workspace, each in its own 128-byte line.
+// Workspace header of a persistent launch.
+//   line 0            the barrier generation (written by workgroup 0 only)
+//   arrive[kMaxGrid]  one arrival word per workgroup (written by its owner only)
+//   slot[2][kMaxGrid] per-workgroup values a kernel exchanges between barriers,
+//                     double-buffered by round parity (x2 for two values)
+// Nothing here needs resetting between launches: barrier epochs are derived
+// from the generation, which only grows, so old arrival words never match a
+// future epoch.  After a launch that ends with a non-zero status the caller
+// must zero the workspace again (the abort can leave arrival words ahead).
 // ---------------------------------------------------------------------------
+constexpr int kMaxGrid = 4096;
+constexpr size_t kSyncBytes = 128 + sizeof(unsigned int) * (size_t)kMaxGrid * (1 + 4);
+
 struct SyncWords {
-  static constexpr int kLine = 32;                 // ints per 128-byte line
   unsigned int *base;
-  __device__ unsigned int *count() const { return base; }              // barrier arrivals
-  __device__ unsigned int *gen() const { return base + kLine; }        // barrier generation
-  __device__ unsigned int *exits() const { return base + 2 * kLine; }  // workgroups finished
-  __device__ unsigned int *word(int i) const { return base + (3 + i) * kLine; }  // kernel-specific
+  __device__ unsigned int *gen() const { return base; }
+  __device__ unsigned int *arrive(int b) const { return base + 32 + b; }
+  // value v (0 or 1) of round parity p for workgroup b
+  __device__ unsigned int *slot(int v, int p, int b) const {
+    return base + 32 + kMaxGrid + ((v * 2 + p) * kMaxGrid) + b;
+  }
 };
-constexpr size_t kSyncBytes = 16 * 128;            // 16 lines: 3 barrier + 13 kernel words
 
 __device__ __forceinline__ int load_status(const int32_t *status) {
   return __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -35,79 +45,99 @@ __device__ __forceinline__ void raise_status(int32_t *status, int code) {
                                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
+__device__ __forceinline__ unsigned int ld_agent(const unsigned int *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(unsigned int *p, unsigned int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wait until every global store this wave issued has completed.  A plain
+// __syncthreads() does not do this on gfx950, and the agent-scope release
+// below is issued by one wave only.
+__device__ __forceinline__ void wave_stores_complete() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // ---------------------------------------------------------------------------
-// Device-wide barrier for a cooperative (co-resident) launch.
+// Device-wide barrier for a persistent launch (all workgroups co-resident).
 //
 // One barrier per level is what the dependence structure needs: no node of a
 // level is a child of another node of the same level, so the dependence is
 // carried by the level loop only (Appendix A.4).
 //
-// Protocol (generation counter): every wave publishes its stores with an
-// agent-scope release fence (L2 write-back on gfx950), the workgroup meets at
-// s_barrier, then one lane reads the generation, adds itself to the arrival
-// count and either (last arriver) resets the count and bumps the generation,
-// or spins on the generation with a wall-clock limit.  Every wave then
-// acquires at agent scope (L2 invalidate) so the next level reads fresh rows.
+// Lock-free flag barrier: every wave drains its stores, one lane per
+// workgroup releases at agent scope (L2 write-back), reads the generation g
+// and writes g+1 to its own arrival word.  Workgroup 0 polls all arrival
+// words in parallel (one lane per workgroup), then publishes generation g+1;
+// the others poll the generation and acquire (L2 invalidate).  No atomic
+// read-modify-write is involved, so the cost does not grow with the number
+// of workgroups the way a shared arrival counter does (device-scope atomics
+// on one address serialise).
 //
-// A wait that passes its limit raises CORTEX_ST_BARRIER_TIMEOUT; a waiter that
-// sees any non-zero status gives up too.  The function returns false when the
-// kernel must stop (status set), true otherwise.  With a single workgroup it
-// reduces to __syncthreads.
+// Every wait is bounded by a wall-clock limit; a wait that passes it raises
+// CORTEX_ST_BARRIER_TIMEOUT.  A waiter that sees any non-zero status gives up.
+// Returns false when the kernel must stop.  With one workgroup it reduces to
+// __syncthreads.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ bool grid_sync(const SyncWords &sw, int32_t *status, uint64_t timeout_ticks) {
   if (gridDim.x == 1) {
     __syncthreads();
     return load_status(status) == 0;
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
+  __shared__ unsigned int s_gen;
   __shared__ int s_ok;
+  wave_stores_complete();
+  __syncthreads();
   if (threadIdx.x == 0) {
-    int ok = 1;
-    unsigned int g = __hip_atomic_load(sw.gen(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    unsigned int arrived = __hip_atomic_fetch_add(sw.count(), 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    if (arrived == gridDim.x - 1) {
-      __hip_atomic_store(sw.count(), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(sw.gen(), g + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    } else {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    const unsigned int g = ld_agent(sw.gen());
+    s_gen = g;
+    s_ok = 1;
+    if (blockIdx.x != 0) st_agent(sw.arrive(blockIdx.x), g + 1u);
+  }
+  __syncthreads();
+  const unsigned int g = s_gen;
+  if (blockIdx.x == 0) {
+    int fail = 0;
+    for (int b = 1 + (int)threadIdx.x; b < (int)gridDim.x && !fail; b += (int)blockDim.x) {
       const uint64_t t0 = wall_clock64();
-      while (__hip_atomic_load(sw.gen(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == g) {
-        if (load_status(status) != 0) { ok = 0; break; }
+      while (ld_agent(sw.arrive(b)) != g + 1u) {
+        if (load_status(status) != 0) { fail = 1; break; }
         if (wall_clock64() - t0 > timeout_ticks) {
           raise_status(status, CORTEX_ST_BARRIER_TIMEOUT);
-          ok = 0;
+          fail = 1;
           break;
         }
-        __builtin_amdgcn_s_sleep(1);
       }
     }
+    if (fail) s_ok = 0;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
+      if (s_ok && load_status(status) == 0) {
+        st_agent(sw.gen(), g + 1u);
+      } else {
+        s_ok = 0;
+        st_agent(sw.gen(), g + 2u);        // release the waiters; they will see the status
+      }
+    }
+  } else if (threadIdx.x == 0) {
+    const uint64_t t0 = wall_clock64();
+    int ok = 1;
+    while (ld_agent(sw.gen()) == g) {
+      if (load_status(status) != 0) { ok = 0; break; }
+      if (wall_clock64() - t0 > timeout_ticks) {
+        raise_status(status, CORTEX_ST_BARRIER_TIMEOUT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     if (ok && load_status(status) != 0) ok = 0;
     s_ok = ok;
   }
   __syncthreads();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   return s_ok != 0;
-}
-
-// Called by every workgroup as its last action.  The last one to finish
-// returns the barrier and the kernel-specific words to zero, so the workspace
-// is ready for the next launch even after a timeout.
-__device__ __forceinline__ void grid_exit(const SyncWords &sw, int n_words) {
-  if (gridDim.x == 1) {
-    __syncthreads();
-    if (threadIdx.x < (unsigned)n_words) *sw.word(threadIdx.x) = 0u;
-    return;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    unsigned int done = __hip_atomic_fetch_add(sw.exits(), 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    if (done == gridDim.x - 1) {
-      __hip_atomic_store(sw.count(), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      for (int i = 0; i < n_words; ++i)
-        __hip_atomic_store(sw.word(i), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(sw.exits(), 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
 }
 
 // ---------------------------------------------------------------------------

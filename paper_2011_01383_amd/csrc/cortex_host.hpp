@@ -19,31 +19,36 @@ inline uint64_t barrier_timeout_ticks() {
   return (uint64_t)us * 100u;
 }
 
-// Largest grid of `kernel` (block threads, dynamic LDS) that can be co-resident.
+int num_cus();
+int cached_occupancy(const void *kernel, int threads);
+
+// Largest grid of `kernel` (block threads, no dynamic LDS) that can be co-resident.
 template <typename Kernel>
-int max_coresident(Kernel kernel, int threads, size_t dyn_lds) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return -1;
-  int cus = 0, per_cu = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, dyn_lds) != hipSuccess) return -1;
+int max_coresident(Kernel kernel, int threads) {
+  const int cus = num_cus();
+  const int per_cu = cached_occupancy((const void *)kernel, threads);
+  if (cus <= 0 || per_cu <= 0) return -1;
   return cus * per_cu;
 }
 
-inline int num_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  return cus;
-}
-
-// Cooperative launch of a persistent kernel whose single argument is a struct.
+// Launch of a persistent kernel whose single argument is a struct.  A grid of
+// at most one workgroup per CU is launched plainly: on a GPU that is not
+// shared with other work every workgroup is resident at once, and a barrier
+// wait that never completes (a GPU shared with other persistent work) ends at
+// its spin limit with CORTEX_ST_BARRIER_TIMEOUT instead of hanging.  Larger
+// grids, or CORTEX_KNOB_COOPERATIVE = 1, use the cooperative launch, which
+// guarantees co-residency at a higher launch cost.
 template <typename Kernel, typename Args>
-int launch_coop(Kernel kernel, int grid, int threads, size_t dyn_lds, const Args &args, void *stream) {
+int launch_persistent(Kernel kernel, int grid, int threads, const Args &args, void *stream) {
   void *kargs[] = {(void *)&args};
-  hipError_t e = hipLaunchCooperativeKernel((const void *)kernel, dim3(grid), dim3(threads), kargs,
-                                            (unsigned int)dyn_lds, (hipStream_t)stream);
-  if (e == hipErrorCooperativeLaunchTooLarge) return CORTEX_E_TOO_LARGE;
+  hipError_t e;
+  if (knob(CORTEX_KNOB_COOPERATIVE) == 0 && grid <= num_cus()) {
+    e = hipLaunchKernel((const void *)kernel, dim3(grid), dim3(threads), kargs, 0, (hipStream_t)stream);
+  } else {
+    e = hipLaunchCooperativeKernel((const void *)kernel, dim3(grid), dim3(threads), kargs, 0,
+                                   (hipStream_t)stream);
+    if (e == hipErrorCooperativeLaunchTooLarge) return CORTEX_E_TOO_LARGE;
+  }
   return e == hipSuccess ? CORTEX_OK : CORTEX_E_HIP;
 }
 

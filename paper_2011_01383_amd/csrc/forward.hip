@@ -165,7 +165,7 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   const int hbase = slice * J;
 
   bool ok = load_status(a.status) == 0;
-  if (!ok) { grid_exit(sw, 0); return; }
+  if (!ok) return;
 
   load_weight_slice<CELL, H>(a, hbase, W_s, bias_s);
   __syncthreads();
@@ -173,7 +173,6 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   const int L = *a.num_levels;
   if (L < 1 || L > a.N) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
-    grid_exit(sw, 0);
     return;
   }
 
@@ -387,7 +386,6 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
     }
     if (l + 1 < L) ok = grid_sync(sw, a.status, a.timeout);
   }
-  grid_exit(sw, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -416,7 +414,7 @@ __global__ void __launch_bounds__(kFwdThreads) mvrnn_forward_kernel(FwdArgs a) {
   const int rblk = blockIdx.x & 3, ngroup = blockIdx.x >> 2, ngroups = gridDim.x >> 2;
 
   bool ok = load_status(a.status) == 0;
-  if (!ok) { grid_exit(sw, 0); return; }
+  if (!ok) return;
   for (int idx = tid; idx < 16 * 2 * D; idx += kFwdThreads) {
     const int r = idx / (2 * D), k = idx % (2 * D);
     WM_s[r * kMvLd + k] = a.W_M[(size_t)(rblk * 16 + r) * 2 * D + k];
@@ -425,7 +423,6 @@ __global__ void __launch_bounds__(kFwdThreads) mvrnn_forward_kernel(FwdArgs a) {
   const int L = *a.num_levels;
   if (L < 1 || L > a.N) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
-    grid_exit(sw, 0);
     return;
   }
   // leaves: (p, P) = (x_table[x], leaf_mat[x]) or zeros; rows spread over all workgroups
@@ -506,7 +503,6 @@ __global__ void __launch_bounds__(kFwdThreads) mvrnn_forward_kernel(FwdArgs a) {
     }
     if (l + 1 < L) ok = grid_sync(sw, a.status, a.timeout);
   }
-  grid_exit(sw, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -549,7 +545,7 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   if (!pick(cell, H, inst)) return CORTEX_E_INVAL;
   if (ws_bytes < cortex_forward_workspace_bytes(cell == CELL_DAG ? -1 : cell, lin->num_nodes, H))
     return CORTEX_E_WORKSPACE;
-  const int cap = max_coresident(inst.fn, kFwdThreads, 0);
+  const int cap = max_coresident(inst.fn, kFwdThreads);
   if (cap <= 0) return CORTEX_E_HIP;
   const int cus = num_cus();
   int S, G;
@@ -563,13 +559,13 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   }
   if (q < 1) q = 1;
   G = (int)(S * q);
-  if (G > cap) return CORTEX_E_TOO_LARGE;
+  if (G > cap || G > kMaxGrid) return CORTEX_E_TOO_LARGE;
   a.S = S;
   a.Q = (int32_t)q;
   a.sync = (unsigned int *)d_ws;
   a.timeout = barrier_timeout_ticks();
   set_last_grid(1, G);
-  return launch_coop(inst.fn, G, kFwdThreads, 0, a, stream);
+  return launch_persistent(inst.fn, G, kFwdThreads, a, stream);
 }
 
 static void fill_lin(FwdArgs &a, const cortex_lin_t *lin) {

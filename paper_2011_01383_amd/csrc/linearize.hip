@@ -28,10 +28,6 @@ constexpr int kSubsPerWave = kSubs / kLinWaves;
 constexpr int kMaxChunk = 8192;              // heights per workgroup held in LDS
 constexpr int kTargetChunk = 1024;           // default chunk when the grid is free
 
-// kernel-specific sync words
-constexpr int kWordFlag0 = 0;                // 3 rotating "changed" flags: words 0..2
-constexpr int kWordMaxH = 3;
-constexpr int kLinWords = 4;
 
 struct LinArgs {
   const int32_t *children;
@@ -50,6 +46,18 @@ __device__ __forceinline__ int lds_load(const int *p) {
 }
 __device__ __forceinline__ void lds_store(int *p, int v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Maximum over the workgroup (tmp: kLinThreads ints of LDS); every thread gets it.
+__device__ __forceinline__ int block_max(int v, int *tmp) {
+  for (int off = 32; off > 0; off >>= 1) v = max(v, __shfl_xor(v, off));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) tmp[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int m = tmp[0];
+  for (int w = 1; w < kLinWaves; ++w) m = max(m, tmp[w]);
+  __syncthreads();
+  return m;
 }
 
 __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
@@ -71,9 +79,8 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   for (int i = tid; i < n; i += kLinThreads) hs[i] = 0;
   __syncthreads();
   int round = 0;
+  int L = 0;
   while (ok) {
-    if (G > 1 && blockIdx.x == 0 && tid == 0)
-      __hip_atomic_store(sw.word(kWordFlag0 + (round + 1) % 3), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     int block_changed = (round == 0);
     int local_max = 0;
     for (;;) {
@@ -112,34 +119,35 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     }
     for (int i = tid; i < n; i += kLinThreads) {
       const int hv = hs[i];
-      a.height[lo + i] = hv;
+      __hip_atomic_store(&a.height[lo + i], hv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       local_max = max(local_max, hv);
     }
-    // block-wide max of the chunk, folded into the global maximum
-    for (int off = 32; off > 0; off >>= 1) local_max = max(local_max, __shfl_xor(local_max, off));
-    if ((tid & 63) == 0) scan_tmp[tid >> 6] = local_max;
-    __syncthreads();
+    local_max = block_max(local_max, scan_tmp);
+    if (G == 1) {
+      L = local_max + 1;
+      ok = grid_sync(sw, a.status, a.timeout);
+      break;                                      // one chunk: the local fixed point is global
+    }
+    // publish (changed, max) in this round's parity slot, then combine all of them
     if (tid == 0) {
-      int mx = 0;
-      for (int w = 0; w < kLinWaves; ++w) mx = max(mx, scan_tmp[w]);
-      if (G == 1) {
-        *sw.word(kWordMaxH) = (unsigned)mx;
-      } else {
-        __hip_atomic_fetch_max(sw.word(kWordMaxH), (unsigned)mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (block_changed)
-          __hip_atomic_fetch_or(sw.word(kWordFlag0 + round % 3), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+      st_agent(sw.slot(0, round & 1, blockIdx.x), (unsigned)block_changed);
+      st_agent(sw.slot(1, round & 1, blockIdx.x), (unsigned)local_max);
     }
     ok = grid_sync(sw, a.status, a.timeout);
     if (!ok) break;
-    if (G == 1) break;                                  // one chunk: local fixed point is global
-    const unsigned f = __hip_atomic_load(sw.word(kWordFlag0 + round % 3), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int any = 0, mx = 0;
+    for (int b = tid; b < G; b += kLinThreads) {
+      any |= (int)ld_agent(sw.slot(0, round & 1, b));
+      mx = max(mx, (int)ld_agent(sw.slot(1, round & 1, b)));
+    }
+    any = __syncthreads_or(any);
+    mx = block_max(mx, scan_tmp);
     ++round;
-    if (f == 0) break;
+    if (!any) {
+      L = mx + 1;
+      break;
+    }
   }
-
-  int L = 0;
-  if (ok) L = 1 + (int)__hip_atomic_load(sw.word(kWordMaxH), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
   // ---------------- 2. stable counting sort on height ----------------
   int passes = 1;
@@ -258,7 +266,6 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       *a.num_levels = L;
     }
   }
-  grid_exit(sw, kLinWords);
 }
 
 static size_t lin_tiles(int32_t N) { return (size_t)(N + kTile - 1) / kTile; }
@@ -288,13 +295,14 @@ extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K,
     return CORTEX_E_INVAL;
   if (ws_bytes < cortex_linearize_workspace_bytes(N, K)) return CORTEX_E_WORKSPACE;
 
-  const int cap = max_coresident(linearize_kernel, kLinThreads, 0);
+  int cap = max_coresident(linearize_kernel, kLinThreads);
   if (cap <= 0) return CORTEX_E_HIP;
   int64_t g = knob(CORTEX_KNOB_LIN_BLOCKS);
   if (g <= 0) g = (N + kTargetChunk - 1) / kTargetChunk;
   const int64_t g_min = (N + kMaxChunk - 1) / kMaxChunk;
   if (g < g_min) g = g_min;
   if (g > N) g = N;
+  if (cap > kMaxGrid) cap = kMaxGrid;
   if (g > cap) {
     if (g_min > cap) return CORTEX_E_TOO_LARGE;
     g = cap;
@@ -322,5 +330,5 @@ extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K,
   a.chunk = (int32_t)((N + g - 1) / g);
   a.timeout = barrier_timeout_ticks();
   set_last_grid(0, (int32_t)g);
-  return launch_coop(linearize_kernel, (int)g, kLinThreads, 0, a, stream);
+  return launch_persistent(linearize_kernel, (int)g, kLinThreads, a, stream);
 }

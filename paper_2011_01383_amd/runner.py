@@ -73,7 +73,10 @@ class DeviceWorkload:
         return int(self.status.item())
 
     def reset_status(self) -> None:
+        """Clear the status word and, as the ABI requires after an error, the workspaces."""
         self.status.zero_()
+        self.ws_lin.zero_()
+        self.ws_fwd.zero_()
 
     def lin_host(self) -> Dict[str, np.ndarray]:
         torch.cuda.synchronize()

@@ -177,9 +177,10 @@ def test_forced_barrier_timeout_then_recovery():
     assert seen <= {0, C.CORTEX_ST_BARRIER_TIMEOUT}
     assert C.CORTEX_ST_BARRIER_TIMEOUT in seen
     C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 5000000)
-    # reuse the same workspace after the timeouts
+    # after an error the ABI asks for a zeroed workspace; then it is reusable
     lin, status, ws, d_children = keep
     status.zero_()
+    ws.zero_()
     C.check(C.cortex_linearize(d_children, wl.N, 2, lin, status, ws), "cortex_linearize")
     torch.cuda.synchronize()
     assert int(status.item()) == 0
