@@ -21,7 +21,7 @@ int64_t knob(int32_t which) {
 constexpr int kMaxDevices = 64;
 static std::atomic<int> g_cus[kMaxDevices];
 static std::mutex g_occ_mu;
-static std::map<std::pair<const void *, int>, int> g_occ;
+static std::map<std::pair<const void *, long long>, int> g_occ;
 
 int num_cus() {
   int dev = 0;
@@ -33,15 +33,16 @@ int num_cus() {
   return c;
 }
 
-int cached_occupancy(const void *kernel, int threads) {
+int cached_occupancy(const void *kernel, int threads, size_t dyn_lds) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   std::lock_guard<std::mutex> lock(g_occ_mu);
-  auto key = std::make_pair(kernel, dev * 65536 + threads);
+  auto key = std::make_pair(kernel, ((long long)dev << 40) | ((long long)threads << 24) | (long long)dyn_lds);
   auto it = g_occ.find(key);
   if (it != g_occ.end()) return it->second;
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return -1;
+  if (dyn_lds > 0) hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, dyn_lds) != hipSuccess) return -1;
   g_occ[key] = per_cu;
   return per_cu;
 }

@@ -52,6 +52,135 @@ __device__ __forceinline__ void st_agent(unsigned int *p, unsigned int v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ---------------------------------------------------------------------------
+// Device-coherent view of a float array written by other workgroups of the
+// same launch.  Loads and stores carry the device scope bit (sc1): a store is
+// written through to the device coherence point, a load is served from it,
+// and neither is satisfied by a CU's L1 or an XCD's L2 copy.  Out-of-range
+// offsets read zero and drop stores (buffer bounds check).  Offsets are bytes.
+// ---------------------------------------------------------------------------
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kScopeDevice = 16;            // buffer cache-policy bit sc1
+constexpr int kRawBufferWord3 = 0x00020000;  // 32-bit data format, raw access
+
+struct DevBuf {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ DevBuf(const float *p, uint32_t bytes)
+      : r(__builtin_amdgcn_make_buffer_rsrc((void *)p, (short)0, (int)bytes, kRawBufferWord3)) {}
+  __device__ __forceinline__ float4 load4(uint32_t off) const {
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kScopeDevice));
+  }
+  __device__ __forceinline__ float load1(uint32_t off) const {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kScopeDevice));
+  }
+  __device__ __forceinline__ void store4(uint32_t off, float4 v) const {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, kScopeDevice);
+  }
+  __device__ __forceinline__ void store1(uint32_t off, float v) const {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, v), r, off, 0, kScopeDevice);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Tagged staging of states for dataflow between workgroups (no barrier).
+// Every element is an 8-byte (value bits, tag) pair written with one
+// device-scope 64-bit store, so a reader sees either an old pair or the new
+// one, never half of each.  A launch uses a tag no earlier launch on the same
+// workspace used, so a pair carrying the launch's tag is a value written by
+// this launch.  Offsets are in elements.
+// ---------------------------------------------------------------------------
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+// Bit casts through a value parameter: clang's __builtin_bit_cast applied
+// directly to an ext-vector element (v.z) reads element 0 instead.
+__device__ __forceinline__ float as_float(unsigned int u) { return __builtin_bit_cast(float, u); }
+__device__ __forceinline__ unsigned int as_uint(float f) { return __builtin_bit_cast(unsigned int, f); }
+
+// Byte offset beyond every buffer this library builds (sizes are < 2^31):
+// a load there returns zeros without touching memory.  Loads whose source is
+// absent use it instead of a branch, so they are always issued and their
+// results never have to be merged (which would force an early wait).
+constexpr uint32_t kNoSource = 0x80000000u;
+
+struct TagBuf {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ TagBuf(const void *p, uint32_t bytes)
+      : r(__builtin_amdgcn_make_buffer_rsrc((void *)p, (short)0, (int)bytes, kRawBufferWord3)) {}
+  // by byte offset (kNoSource reads zeros)
+  __device__ __forceinline__ u32x4 load2_at(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kScopeDevice);
+  }
+  __device__ __forceinline__ u32x2 load1_at(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kScopeDevice);
+  }
+  // elements e and e+1: (v0, t0, v1, t1)
+  __device__ __forceinline__ u32x4 load2(uint32_t e) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, e * 8u, 0, kScopeDevice);
+  }
+  __device__ __forceinline__ u32x2 load1(uint32_t e) const {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, e * 8u, 0, kScopeDevice);
+  }
+  __device__ __forceinline__ void store1(uint32_t e, float v, uint32_t tag) const {
+    u32x2 w;
+    w.x = as_uint(v);
+    w.y = tag;
+    __builtin_amdgcn_raw_buffer_store_b64(w, r, e * 8u, 0, kScopeDevice);
+  }
+};
+
+// Read-only input rows (embedding tables, DAG inputs) through the ordinary
+// cache hierarchy; out-of-range offsets read zeros.  Offsets are bytes.
+struct InBuf {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ InBuf(const void *p, uint32_t bytes)
+      : r(__builtin_amdgcn_make_buffer_rsrc((void *)p, (short)0, (int)bytes, kRawBufferWord3)) {}
+  __device__ __forceinline__ u32x4 load4(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  }
+};
+
+__device__ __forceinline__ float4 as_float4(u32x4 v) {
+  return make_float4(as_float(v.x), as_float(v.y), as_float(v.z), as_float(v.w));
+}
+
+// Four consecutive k values of an operand row: either four staged elements as
+// two (value, tag) pairs of pairs, or (raw) four plain floats in lo with hi
+// unused.  Keeping a plain load in its destination registers lets it stay in
+// flight until the value is consumed.
+struct Frag4 {
+  u32x4 lo, hi;
+  __device__ __forceinline__ bool staged_ready(uint32_t tag) const {
+    return lo.y == tag && lo.w == tag && hi.y == tag && hi.w == tag;
+  }
+  __device__ __forceinline__ float4 value(bool raw) const {
+    const unsigned int b = raw ? lo.y : lo.z, c = raw ? lo.z : hi.x, d = raw ? lo.w : hi.z;
+    return make_float4(as_float(lo.x), as_float(b), as_float(c), as_float(d));
+  }
+  __device__ static __forceinline__ Frag4 zero() {
+    Frag4 f;
+    f.lo = u32x4{0u, 0u, 0u, 0u};
+    f.hi = u32x4{0u, 0u, 0u, 0u};
+    return f;
+  }
+};
+
+// Bounded wait used by consumers of staged values: true while waiting may
+// go on, false (after raising CORTEX_ST_BARRIER_TIMEOUT on the limit) when the
+// consumer must give up because of the limit or another error.  The sleep
+// between polls grows from ~30 ns to ~0.2 us so that many waiting waves do
+// not flood the memory system with polls.
+__device__ __forceinline__ bool keep_waiting(int32_t *status, uint64_t t0, uint64_t timeout_ticks, int &naps) {
+  if (load_status(status) != 0) return false;
+  if (wall_clock64() - t0 > timeout_ticks) {
+    raise_status(status, CORTEX_ST_BARRIER_TIMEOUT);
+    return false;
+  }
+  if (naps < 8) __builtin_amdgcn_s_sleep(1);
+  else __builtin_amdgcn_s_sleep(8);
+  ++naps;
+  return true;
+}
+
 // Wait until every global store this wave issued has completed.  A plain
 // __syncthreads() does not do this on gfx950, and the agent-scope release
 // below is issued by one wave only.
@@ -73,11 +202,17 @@ __device__ __forceinline__ void wave_stores_complete() { __builtin_amdgcn_s_wait
 // of workgroups the way a shared arrival counter does (device-scope atomics
 // on one address serialise).
 //
+// kFenced = false is for kernels whose cross-workgroup data all moves through
+// DevBuf (device-scope stores and loads): a completed device-scope store is
+// already visible at the coherence point, so release reduces to the store
+// wait and no L2 write-back or invalidate is needed.
+//
 // Every wait is bounded by a wall-clock limit; a wait that passes it raises
 // CORTEX_ST_BARRIER_TIMEOUT.  A waiter that sees any non-zero status gives up.
 // Returns false when the kernel must stop.  With one workgroup it reduces to
 // __syncthreads.
 // ---------------------------------------------------------------------------
+template <bool kFenced = true>
 __device__ __forceinline__ bool grid_sync(const SyncWords &sw, int32_t *status, uint64_t timeout_ticks) {
   if (gridDim.x == 1) {
     __syncthreads();
@@ -88,7 +223,7 @@ __device__ __forceinline__ bool grid_sync(const SyncWords &sw, int32_t *status, 
   wave_stores_complete();
   __syncthreads();
   if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (kFenced) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     const unsigned int g = ld_agent(sw.gen());
     s_gen = g;
     s_ok = 1;
@@ -112,7 +247,7 @@ __device__ __forceinline__ bool grid_sync(const SyncWords &sw, int32_t *status, 
     if (fail) s_ok = 0;
     __syncthreads();
     if (threadIdx.x == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
+      if (kFenced) __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
       if (s_ok && load_status(status) == 0) {
         st_agent(sw.gen(), g + 1u);
       } else {
@@ -132,7 +267,7 @@ __device__ __forceinline__ bool grid_sync(const SyncWords &sw, int32_t *status, 
       }
       __builtin_amdgcn_s_sleep(1);
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (kFenced) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     if (ok && load_status(status) != 0) ok = 0;
     s_ok = ok;
   }

@@ -20,13 +20,13 @@ inline uint64_t barrier_timeout_ticks() {
 }
 
 int num_cus();
-int cached_occupancy(const void *kernel, int threads);
+int cached_occupancy(const void *kernel, int threads, size_t dyn_lds = 0);
 
 // Largest grid of `kernel` (block threads, no dynamic LDS) that can be co-resident.
 template <typename Kernel>
 int max_coresident(Kernel kernel, int threads) {
   const int cus = num_cus();
-  const int per_cu = cached_occupancy((const void *)kernel, threads);
+  const int per_cu = cached_occupancy((const void *)kernel, threads, 0);
   if (cus <= 0 || per_cu <= 0) return -1;
   return cus * per_cu;
 }
@@ -39,14 +39,14 @@ int max_coresident(Kernel kernel, int threads) {
 // grids, or CORTEX_KNOB_COOPERATIVE = 1, use the cooperative launch, which
 // guarantees co-residency at a higher launch cost.
 template <typename Kernel, typename Args>
-int launch_persistent(Kernel kernel, int grid, int threads, const Args &args, void *stream) {
+int launch_persistent(Kernel kernel, int grid, int threads, size_t dyn_lds, const Args &args, void *stream) {
   void *kargs[] = {(void *)&args};
   hipError_t e;
   if (knob(CORTEX_KNOB_COOPERATIVE) == 0 && grid <= num_cus()) {
-    e = hipLaunchKernel((const void *)kernel, dim3(grid), dim3(threads), kargs, 0, (hipStream_t)stream);
+    e = hipLaunchKernel((const void *)kernel, dim3(grid), dim3(threads), kargs, dyn_lds, (hipStream_t)stream);
   } else {
-    e = hipLaunchCooperativeKernel((const void *)kernel, dim3(grid), dim3(threads), kargs, 0,
-                                   (hipStream_t)stream);
+    e = hipLaunchCooperativeKernel((const void *)kernel, dim3(grid), dim3(threads), kargs,
+                                   (unsigned int)dyn_lds, (hipStream_t)stream);
     if (e == hipErrorCooperativeLaunchTooLarge) return CORTEX_E_TOO_LARGE;
   }
   return e == hipSuccess ? CORTEX_OK : CORTEX_E_HIP;

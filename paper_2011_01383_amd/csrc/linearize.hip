@@ -60,6 +60,45 @@ __device__ __forceinline__ int block_max(int v, int *tmp) {
   return m;
 }
 
+// Exclusive prefix sum of data[0..n) in LDS by the whole workgroup: each
+// thread scans a contiguous segment, segment sums are scanned with wave
+// shuffles and the wave totals in wsum[THREADS/64 + 1].  Returns the total.
+template <int THREADS>
+__device__ int block_exclusive_scan(int *data, int n, int *wsum) {
+  constexpr int W = THREADS / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int seg = (n + THREADS - 1) / THREADS;
+  const int lo = min(n, tid * seg), hi = min(n, lo + seg);
+  int sum = 0;
+  for (int i = lo; i < hi; ++i) sum += data[i];
+  int x = sum;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int w = 0; w < W; ++w) {
+      const int t = wsum[w];
+      wsum[w] = run;
+      run += t;
+    }
+    wsum[W] = run;
+  }
+  __syncthreads();
+  int run = wsum[wave] + x - sum;
+  for (int i = lo; i < hi; ++i) {
+    const int t = data[i];
+    data[i] = run;
+    run += t;
+  }
+  const int total = wsum[W];
+  __syncthreads();
+  return total;
+}
+
 __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   __shared__ int hs[kMaxChunk];
   __shared__ int cnt[kSubs][256];
@@ -180,22 +219,21 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     ok = grid_sync(sw, a.status, a.timeout);
     if (!ok) break;
 
-    // (b) exclusive scan of the 256*T counts, by workgroup 0
+    // (b) exclusive scan of the 256*T counts, by workgroup 0, through LDS in
+    //     chunks of kSubs*256 (the cnt array), carrying the running total
     if (blockIdx.x == 0) {
       const int M = 256 * T;
-      const int seg = (M + kLinThreads - 1) / kLinThreads;
-      const int b0 = min(M, tid * seg), b1 = min(M, b0 + seg);
-      int sum = 0;
-      for (int i = b0; i < b1; ++i) sum += a.tile_hist[i];
-      scan_tmp[tid] = sum;
-      __syncthreads();
-      if (tid == 0) {
-        int run = 0;
-        for (int w = 0; w < kLinThreads; ++w) { int x = scan_tmp[w]; scan_tmp[w] = run; run += x; }
+      int carry = 0;
+      int *buf = &cnt[0][0];
+      for (int c0 = 0; c0 < M; c0 += kSubs * 256) {
+        const int n = min(kSubs * 256, M - c0);
+        for (int i = tid; i < n; i += kLinThreads) buf[i] = a.tile_hist[c0 + i];
+        __syncthreads();
+        const int total = block_exclusive_scan<kLinThreads>(buf, n, scan_tmp);
+        for (int i = tid; i < n; i += kLinThreads) a.tile_hist[c0 + i] = buf[i] + carry;
+        carry += total;
+        __syncthreads();
       }
-      __syncthreads();
-      int run = scan_tmp[tid];
-      for (int i = b0; i < b1; ++i) { int x = a.tile_hist[i]; a.tile_hist[i] = run; run += x; }
     }
     ok = grid_sync(sw, a.status, a.timeout);
     if (!ok) break;
@@ -268,6 +306,195 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Small batches: one workgroup does the whole linearization in LDS.
+//   children -> LDS; height sweeps until nothing changes (a value >= N proves
+//   a cycle); a stable counting sort on height with 8-bit digits (one pass
+//   while L <= 256): a global digit histogram gives each digit's first row,
+//   then 1024-node chunks in id order are ranked with wave ballots, per-wave
+//   digit counts and a running cursor per digit; finally every output array
+//   is written once, coalesced.
+// LDS (ints): children N*K, height N, perm 2N, node_row N, level count N+1,
+// wave-digit counts 16*256, digit cursors 256*2.
+// ---------------------------------------------------------------------------
+#ifdef CORTEX_TRACE
+#define CORTEX_LIN_STAMP(k)                                         \
+  do {                                                              \
+    if (threadIdx.x == 0) ((uint64_t *)a.sync)[(k)] = wall_clock64(); \
+  } while (0)
+#else
+#define CORTEX_LIN_STAMP(k) \
+  do {                      \
+  } while (0)
+#endif
+
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / 64;
+constexpr int kSmallPer = 4;                         // nodes per thread: N <= 4096
+constexpr size_t kSmallLdsMax = 150 * 1024;
+
+static size_t small_lds_bytes(int32_t N, int32_t K) {
+  return sizeof(int) * ((size_t)N * K + 5 * (size_t)N + 1 + kSmallWaves * 256 + 2 * 256 + 64);
+}
+
+__global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs a) {
+  extern __shared__ int sm[];
+  const int N = a.N, K = a.K;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  int *ch = sm;                       // [N*K]
+  int *hgt = ch + N * K;              // [N]
+  int *perm0 = hgt + N;               // [N]
+  int *perm1 = perm0 + N;             // [N]
+  int *nrow = perm1 + N;              // [N]
+  int *lcount = nrow + N;             // [N+1]
+  int *wcnt = lcount + N + 1;         // [16][256]
+  int *dstart = wcnt + kSmallWaves * 256;   // [256]
+  int *cursor = dstart + 256;         // [256]
+  int *flags = cursor + 256;          // [64] scratch
+
+  CORTEX_LIN_STAMP(0);
+  if (load_status(a.status) != 0) return;
+  // 1. children: into registers for the sweeps (node v = tid + j*threads) and
+  //    into LDS for the output phase; range check
+  int myc[kSmallPer][4], myh[kSmallPer];
+  int bad = 0;
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    const int v = tid + j * kSmallThreads;
+    myh[j] = 0;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      int c = (v < N && s < K) ? a.children[(size_t)v * K + s] : -1;
+      if (c < -1 || c >= N) { bad = 1; c = -1; }
+      myc[j][s] = c;
+      if (v < N && s < K) ch[v * K + s] = c;
+    }
+    if (v < N) hgt[v] = 0;
+  }
+  if (tid < 3) flags[tid] = 0;      // sweep change flags (3, rotating)
+  if (tid == 0) flags[3] = 0;       // cycle flag
+  if (__syncthreads_or(bad)) {
+    if (tid == 0) raise_status(a.status, CORTEX_ST_CHILD_RANGE);
+    return;
+  }
+  CORTEX_LIN_STAMP(1);
+  // 2. heights: monotone sweeps to the fixed point, one barrier per sweep.
+  //    Sweep k raises flags[k % 3]; flags[(k+2) % 3] is cleared for sweep k+2
+  //    while no thread can still be reading it.
+  for (int k = 0;; ++k) {
+    if (tid == 0) flags[(k + 2) % 3] = 0;
+    int changed = 0, cyc = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallPer; ++j) {
+      const int v = tid + j * kSmallThreads;
+      if (v >= N) continue;
+      int m = -1;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        if (myc[j][s] >= 0) m = max(m, lds_load(&hgt[myc[j][s]]));
+      if (m + 1 > myh[j]) {
+        myh[j] = m + 1;
+        lds_store(&hgt[v], m + 1);
+        changed = 1;
+        if (m + 1 >= N) cyc = 1;
+      }
+    }
+    if (changed) lds_store(&flags[k % 3], 1);
+    if (cyc) lds_store(&flags[3], 1);
+    __syncthreads();
+    if (lds_load(&flags[3])) {
+      if (tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
+      return;
+    }
+    if (!lds_load(&flags[k % 3])) break;
+  }
+  __syncthreads();                  // every exit decision has read flags before they are reused
+  CORTEX_LIN_STAMP(2);
+  // L = 1 + max height, level counts
+  int mx = 0;
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) mx = max(mx, myh[j]);
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
+  if (lane == 0) flags[wave] = mx;
+  for (int i = tid; i <= N; i += kSmallThreads) lcount[i] = 0;
+  __syncthreads();
+  int L = 0;
+  for (int w = 0; w < kSmallWaves; ++w) L = max(L, flags[w]);
+  L += 1;
+  for (int v = tid; v < N; v += kSmallThreads) atomicAdd(&lcount[hgt[v]], 1);
+  __syncthreads();
+  CORTEX_LIN_STAMP(3);
+  // 3. stable LSD counting sort on height, 8-bit digits
+  int passes = 1;
+  for (int v = (L - 1) >> 8; v > 0; v >>= 8) ++passes;
+  const unsigned long long lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+  for (int p = 0; p < passes; ++p) {
+    const int shift = 8 * p;
+    const int *in = (p & 1) ? perm0 : perm1;    // pass 0 reads ids directly
+    int *out = (p & 1) ? perm1 : perm0;
+    if (tid < 256) dstart[tid] = 0;
+    __syncthreads();
+    for (int i = tid; i < N; i += kSmallThreads) {
+      const int v = p == 0 ? i : in[i];
+      atomicAdd(&dstart[(hgt[v] >> shift) & 255], 1);
+    }
+    __syncthreads();
+    block_exclusive_scan<kSmallThreads>(dstart, 256, flags);
+    if (tid < 256) cursor[tid] = 0;
+    __syncthreads();
+    for (int base = 0; base < N; base += kSmallThreads) {
+      const int idx = base + tid;
+      const bool valid = idx < N;
+      const int item = valid ? (p == 0 ? idx : in[idx]) : 0;
+      const int dig = valid ? ((hgt[item] >> shift) & 255) : 0;
+      unsigned long long peers = __ballot(valid);
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const bool bit = (dig >> b) & 1;
+        const unsigned long long m = __ballot(bit);
+        peers &= bit ? m : ~m;
+      }
+      const int rank = __popcll(peers & lt_mask);
+      for (int i = tid; i < kSmallWaves * 256; i += kSmallThreads) wcnt[i] = 0;
+      __syncthreads();
+      if (valid && rank == 0) wcnt[wave * 256 + dig] = __popcll(peers);
+      __syncthreads();
+      if (tid < 256) {             // per digit: wave offsets within the chunk, then advance the cursor
+        int run = cursor[tid];
+        for (int w = 0; w < kSmallWaves; ++w) { const int x = wcnt[w * 256 + tid]; wcnt[w * 256 + tid] = run; run += x; }
+        cursor[tid] = run;
+      }
+      __syncthreads();
+      if (valid) out[dstart[dig] + wcnt[wave * 256 + dig] + rank] = item;
+      __syncthreads();
+    }
+  }
+  CORTEX_LIN_STAMP(4);
+  const int *order = ((passes - 1) & 1) ? perm1 : perm0;
+  for (int r = tid; r < N; r += kSmallThreads) nrow[order[r]] = r;
+  __syncthreads();
+  // 4. outputs
+  for (int r = tid; r < N; r += kSmallThreads) {
+    const int v = order[r];
+    a.level_nodes[r] = v;
+    a.node_row[v] = r;
+    a.height[r] = hgt[r];             // by node id (r doubles as a node id here)
+    for (int s = 0; s < K; ++s) {
+      const int c = ch[v * K + s];
+      a.child_rows[(size_t)r * K + s] = c < 0 ? -1 : nrow[c];
+    }
+  }
+  CORTEX_LIN_STAMP(5);
+  const int total = block_exclusive_scan<kSmallThreads>(lcount, L, flags);
+  for (int l = tid; l < L; l += kSmallThreads) a.level_offsets[l] = lcount[l];
+  if (tid == 0) {
+    a.level_offsets[L] = total;
+    *a.num_levels = L;
+  }
+  CORTEX_LIN_STAMP(6);
+}
+
 static size_t lin_tiles(int32_t N) { return (size_t)(N + kTile - 1) / kTile; }
 
 }  // namespace cortex
@@ -295,6 +522,24 @@ extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K,
     return CORTEX_E_INVAL;
   if (ws_bytes < cortex_linearize_workspace_bytes(N, K)) return CORTEX_E_WORKSPACE;
 
+  const size_t small_lds = small_lds_bytes(N, K);
+  if (knob(CORTEX_KNOB_LIN_BLOCKS) == 0 && small_lds <= kSmallLdsMax && N <= kSmallThreads * kSmallPer) {
+    LinArgs s = {};
+    s.children = d_children;
+    s.N = N;
+    s.K = K;
+    s.num_levels = lin->num_levels;
+    s.height = lin->height;
+    s.level_offsets = lin->level_offsets;
+    s.level_nodes = lin->level_nodes;
+    s.node_row = lin->node_row;
+    s.child_rows = lin->child_rows;
+    s.status = d_status;
+    s.sync = (unsigned int *)d_ws;
+    if (cached_occupancy((const void *)linearize_small_kernel, kSmallThreads, small_lds) <= 0) return CORTEX_E_HIP;
+    set_last_grid(0, 1);
+    return launch_persistent(linearize_small_kernel, 1, kSmallThreads, small_lds, s, stream);
+  }
   int cap = max_coresident(linearize_kernel, kLinThreads);
   if (cap <= 0) return CORTEX_E_HIP;
   int64_t g = knob(CORTEX_KNOB_LIN_BLOCKS);
@@ -330,5 +575,5 @@ extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K,
   a.chunk = (int32_t)((N + g - 1) / g);
   a.timeout = barrier_timeout_ticks();
   set_last_grid(0, (int32_t)g);
-  return launch_persistent(linearize_kernel, (int)g, kLinThreads, a, stream);
+  return launch_persistent(linearize_kernel, (int)g, kLinThreads, 0, a, stream);
 }
