@@ -73,6 +73,43 @@ def bound_of(flops, byts):
     return "mfma" if t_f >= t_b else "hbm"
 
 
+FORWARD_SOURCES = ("paper_2011_01383_amd/csrc/forward.hip", "paper_2011_01383_amd/csrc/cortex_device.hpp",
+                   "paper_2011_01383_amd/csrc/cortex_host.hpp")
+
+
+def forward_source_hash():
+    """sha256 over the forward kernel's sources, to tell whether stored
+    counter readings still describe the kernel that is built."""
+    import hashlib
+    h = hashlib.sha256()
+    for rel in FORWARD_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(wl):
+    """HBM bytes per forward launch from the rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary kept in profiles/ for this workload (each counter scaled by its
+    reading on a plain copy of known size), or None when there is no summary
+    or the forward sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "hbm_counters_%s.md" % wl.name)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and line.split(":", 1)[0].strip().isidentifier():
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha256") != forward_source_hash():
+        return None
+    try:
+        return float(fields["forward_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(wl, seconds):
     """The fp64 oracle (linearize + recursive forward) on a bounded sample."""
     from oracle import cortex_oracle as O
@@ -106,6 +143,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--node-groups", type=int, default=0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB mebibytes (reads MIB, writes MIB) "
+                         "five times, to scale HBM byte counters; prints one JSON line")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -114,6 +154,16 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.rand(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_mib": args.calibrate_copy, "launches": 5,
+                          "bytes_read_per_launch": n * 4, "bytes_written_per_launch": n * 4}))
+        return
     from paper_2011_01383_amd import cortex as C
     from paper_2011_01383_amd import inputs as I
     from paper_2011_01383_amd.runner import DeviceWorkload
@@ -151,24 +201,28 @@ def main():
     assert dw.status_code() == 0
     ms_per_step = total_ms / args.steps
 
-    # ---- per-kernel timing (HIP events on the launch stream) ----
-    def time_calls(fn, n):
-        es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-        for a, b in es:
-            a.record(stream)
-            fn()
-            b.record(stream)
+    # ---- per-kernel timing: n launches back to back between two HIP events
+    #      on the launch stream (average launch duration, as a kernel trace
+    #      reports it), plus single-launch samples for percentiles ----
+    def time_back_to_back(fn, n):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        return np.array([a.elapsed_time(b) for a, b in es])
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
 
     n_k = max(20, min(args.steps, 200))
-    lin_ms = time_calls(dw.linearize, n_k)
-    fwd_ms = time_calls(dw.forward, n_k)
+    lin_avg_ms = time_back_to_back(dw.linearize, n_k)
+    fwd_avg_ms = time_back_to_back(dw.forward, n_k)
     assert dw.status_code() == 0
 
     flops, byts = algorithmic_work(wl)
     bound = bound_of(flops, byts)
-    fwd_avg_s = float(fwd_ms.mean()) / 1e3
+    fwd_avg_s = fwd_avg_ms / 1e3
     if bound == "mfma":
         achieved = flops / fwd_avg_s / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
@@ -177,8 +231,10 @@ def main():
         achieved = byts / fwd_avg_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+    roof["traffic"] = measured_traffic(wl)
+    roof["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = "forward (%s)" % wl.cell
-    roof["kernel_avg_ms"] = float(fwd_ms.mean())
+    roof["kernel_avg_ms"] = fwd_avg_ms
     roof["algorithmic_flops"] = flops
     roof["algorithmic_bytes"] = byts
 
@@ -209,8 +265,8 @@ def main():
             "latency_ms_p10": float(np.percentile(step_ms, 10)),
             "latency_ms_p50": float(np.percentile(step_ms, 50)),
             "latency_ms_p90": float(np.percentile(step_ms, 90)),
-            "linearize_ms_p50": float(np.median(lin_ms)),
-            "forward_ms_p50": float(np.median(fwd_ms)),
+            "linearize_kernel_avg_ms": lin_avg_ms,
+            "forward_kernel_avg_ms": fwd_avg_ms,
             "host_wall_s": wall,
         },
     }

@@ -11,11 +11,17 @@
  *                           (dynamic batching, Sec. 3.1) and child rows.
  *   2. cortex_tree_forward / cortex_dag_forward
  *                         - the lowered loop nest of Sec. 4.1 ("RA Lowering":
- *                           a leaf loop, then a loop over batches of nodes with
- *                           one barrier per batch, Appendix A.4), run as ONE
- *                           persistent kernel with the cell weights resident
- *                           on chip (kernel fusion and model persistence,
- *                           Sec. 7.2 and 7.3).
+ *                           a leaf loop, then a loop over batches of nodes
+ *                           whose dependence is carried by the batch loop,
+ *                           Appendix A.4), run as ONE persistent kernel with
+ *                           the cell weights resident on chip (kernel fusion
+ *                           and model persistence, Sec. 7.2 and 7.3).  The
+ *                           tree, child-sum and DAG kernels order levels per
+ *                           datum: each state element is also published as a
+ *                           (value, launch tag) pair in the workspace and a
+ *                           consumer waits for exactly the elements it reads;
+ *                           the MV-RNN kernel uses one device-wide barrier
+ *                           per level.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -29,8 +35,9 @@
  * - The kernels are persistent: every workgroup of a launch must be resident
  *   at once.  A grid of at most one workgroup per compute unit is launched
  *   with a plain launch (it is resident at once on a GPU not shared with
- *   other persistent work); larger grids use the cooperative launch.  A
- *   device-wide barrier never waits past its spin limit.
+ *   other persistent work); larger grids use the cooperative launch.  No
+ *   wait (device-wide barrier or per-datum wait) spins past its limit: it
+ *   then writes CORTEX_ST_BARRIER_TIMEOUT, and every other wait ends.
  * - stream is a hipStream_t (NULL = the default stream).  Every call only
  *   enqueues work on it and returns; nothing is synchronised.
  * - The return value reports host-detectable errors (CORTEX_E_*).  When a
@@ -70,7 +77,7 @@ extern "C" {
 #define CORTEX_ST_OK 0
 #define CORTEX_ST_CHILD_RANGE 1      /* a child index outside [-1, N) */
 #define CORTEX_ST_CYCLE 2            /* the structure has a cycle (not a DAG) */
-#define CORTEX_ST_BARRIER_TIMEOUT 3  /* a device-wide barrier waited past its limit */
+#define CORTEX_ST_BARRIER_TIMEOUT 3  /* a barrier or per-datum wait passed its limit */
 #define CORTEX_ST_BAD_LINEARIZATION 4 /* forward was handed an inconsistent linearization */
 #define CORTEX_ST_INPUT_RANGE 5      /* an input index outside [-1, rows of the input table) */
 
@@ -185,7 +192,7 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *   CORTEX_KNOB_LIN_BLOCKS          workgroups of the linearizer (0 = chosen from N)
  *   CORTEX_KNOB_FWD_NODE_GROUPS     node groups of the forward; workgroups =
  *                                   hidden slices x node groups (0 = fill the GPU)
- *   CORTEX_KNOB_BARRIER_TIMEOUT_US  spin limit of one device-wide barrier wait in
+ *   CORTEX_KNOB_BARRIER_TIMEOUT_US  spin limit of one barrier or per-datum wait in
  *                                   microseconds (default 5,000,000; 0 makes every
  *                                   wait time out at once, for tests of that path)
  *   CORTEX_KNOB_COOPERATIVE         1 = always use the cooperative launch
