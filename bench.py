@@ -143,6 +143,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--node-groups", type=int, default=0)
+    ap.add_argument("--slice-units", type=int, default=0, help="hidden units per forward slice (0 = default)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB mebibytes (reads MIB, writes MIB) "
                          "five times, to scale HBM byte counters; prints one JSON line")
@@ -174,6 +175,7 @@ def main():
     torch.cuda.set_device(0)
     wl = I.make_workload(args.workload)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, args.node_groups)
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, args.slice_units)
     dw = DeviceWorkload(wl)
     stream = torch.cuda.current_stream()
 

@@ -198,12 +198,18 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *   CORTEX_KNOB_COOPERATIVE         1 = always use the cooperative launch
  *                                   (0 = only when the grid exceeds one
  *                                   workgroup per compute unit)
+ *   CORTEX_KNOB_FWD_SLICE_UNITS     hidden units per workgroup slice of the
+ *                                   forward (0 = the default of the cell;
+ *                                   other values are used where the library
+ *                                   has a kernel for them: 2 for the N-ary
+ *                                   TreeLSTM at H = 256)
  * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value.
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0
 #define CORTEX_KNOB_FWD_NODE_GROUPS 1
 #define CORTEX_KNOB_BARRIER_TIMEOUT_US 2
 #define CORTEX_KNOB_COOPERATIVE 3
+#define CORTEX_KNOB_FWD_SLICE_UNITS 4
 int cortex_set_knob(int32_t knob, int64_t value);
 int64_t cortex_get_knob(int32_t knob);
 

@@ -40,6 +40,7 @@ CORTEX_KNOB_LIN_BLOCKS = 0
 CORTEX_KNOB_FWD_NODE_GROUPS = 1
 CORTEX_KNOB_BARRIER_TIMEOUT_US = 2
 CORTEX_KNOB_COOPERATIVE = 3
+CORTEX_KNOB_FWD_SLICE_UNITS = 4
 
 CELL_IDS = {"tree_rnn": CORTEX_TREE_RNN, "nary_treelstm": CORTEX_NARY_TREELSTM,
             "childsum_treelstm": CORTEX_CHILDSUM_TREELSTM, "mvrnn": CORTEX_MVRNN}

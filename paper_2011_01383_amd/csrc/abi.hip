@@ -8,8 +8,8 @@
 
 namespace cortex {
 
-constexpr int kKnobs = 4;
-static std::atomic<int64_t> g_knobs[kKnobs] = {{0}, {0}, {5000000}, {0}};
+constexpr int kKnobs = 5;
+static std::atomic<int64_t> g_knobs[kKnobs] = {{0}, {0}, {5000000}, {0}, {0}};
 static std::atomic<int32_t> g_last_grid[2] = {{0}, {0}};
 
 int64_t knob(int32_t which) {

@@ -60,6 +60,7 @@ __device__ __forceinline__ void st_agent(unsigned int *p, unsigned int v) {
 // offsets read zero and drop stores (buffer bounds check).  Offsets are bytes.
 // ---------------------------------------------------------------------------
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kScopeDevice = 16;            // buffer cache-policy bit sc1
 constexpr int kRawBufferWord3 = 0x00020000;  // 32-bit data format, raw access
 
@@ -69,6 +70,9 @@ struct DevBuf {
       : r(__builtin_amdgcn_make_buffer_rsrc((void *)p, (short)0, (int)bytes, kRawBufferWord3)) {}
   __device__ __forceinline__ float4 load4(uint32_t off) const {
     return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kScopeDevice));
+  }
+  __device__ __forceinline__ u32x4 load4u(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kScopeDevice);
   }
   __device__ __forceinline__ float load1(uint32_t off) const {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kScopeDevice));
@@ -81,16 +85,6 @@ struct DevBuf {
   }
 };
 
-// ---------------------------------------------------------------------------
-// Tagged staging of states for dataflow between workgroups (no barrier).
-// Every element is an 8-byte (value bits, tag) pair written with one
-// device-scope 64-bit store, so a reader sees either an old pair or the new
-// one, never half of each.  A launch uses a tag no earlier launch on the same
-// workspace used, so a pair carrying the launch's tag is a value written by
-// this launch.  Offsets are in elements.
-// ---------------------------------------------------------------------------
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-
 // Bit casts through a value parameter: clang's __builtin_bit_cast applied
 // directly to an ext-vector element (v.z) reads element 0 instead.
 __device__ __forceinline__ float as_float(unsigned int u) { return __builtin_bit_cast(float, u); }
@@ -102,24 +96,26 @@ __device__ __forceinline__ unsigned int as_uint(float f) { return __builtin_bit_
 // results never have to be merged (which would force an early wait).
 constexpr uint32_t kNoSource = 0x80000000u;
 
+// ---------------------------------------------------------------------------
+// Per-datum ordering between workgroups of one launch (no barrier).  Every
+// state element is also staged as an 8-byte (value bits, tag) pair written
+// with one device-scope 64-bit store, so a reader sees either an old pair or
+// the new one, never half of each.  A launch uses a tag no earlier launch on
+// the same workspace used, so a pair carrying the launch's tag is a value
+// written by this launch and the staging never needs resetting.  Offsets are
+// in bytes; kNoSource reads zeros (tag 0, which no launch uses).
+// ---------------------------------------------------------------------------
 struct TagBuf {
   __amdgpu_buffer_rsrc_t r;
   __device__ TagBuf(const void *p, uint32_t bytes)
       : r(__builtin_amdgcn_make_buffer_rsrc((void *)p, (short)0, (int)bytes, kRawBufferWord3)) {}
-  // by byte offset (kNoSource reads zeros)
   __device__ __forceinline__ u32x4 load2_at(uint32_t off) const {
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kScopeDevice);
   }
   __device__ __forceinline__ u32x2 load1_at(uint32_t off) const {
     return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kScopeDevice);
   }
-  // elements e and e+1: (v0, t0, v1, t1)
-  __device__ __forceinline__ u32x4 load2(uint32_t e) const {
-    return __builtin_amdgcn_raw_buffer_load_b128(r, e * 8u, 0, kScopeDevice);
-  }
-  __device__ __forceinline__ u32x2 load1(uint32_t e) const {
-    return __builtin_amdgcn_raw_buffer_load_b64(r, e * 8u, 0, kScopeDevice);
-  }
+  // element e
   __device__ __forceinline__ void store1(uint32_t e, float v, uint32_t tag) const {
     u32x2 w;
     w.x = as_uint(v);
@@ -143,48 +139,11 @@ __device__ __forceinline__ float4 as_float4(u32x4 v) {
   return make_float4(as_float(v.x), as_float(v.y), as_float(v.z), as_float(v.w));
 }
 
-// Four consecutive k values of an operand row: either four staged elements as
-// two (value, tag) pairs of pairs, or (raw) four plain floats in lo with hi
-// unused.  Keeping a plain load in its destination registers lets it stay in
-// flight until the value is consumed.
-struct Frag4 {
-  u32x4 lo, hi;
-  __device__ __forceinline__ bool staged_ready(uint32_t tag) const {
-    return lo.y == tag && lo.w == tag && hi.y == tag && hi.w == tag;
-  }
-  __device__ __forceinline__ float4 value(bool raw) const {
-    const unsigned int b = raw ? lo.y : lo.z, c = raw ? lo.z : hi.x, d = raw ? lo.w : hi.z;
-    return make_float4(as_float(lo.x), as_float(b), as_float(c), as_float(d));
-  }
-  __device__ static __forceinline__ Frag4 zero() {
-    Frag4 f;
-    f.lo = u32x4{0u, 0u, 0u, 0u};
-    f.hi = u32x4{0u, 0u, 0u, 0u};
-    return f;
-  }
-};
-
-// Bounded wait used by consumers of staged values: true while waiting may
-// go on, false (after raising CORTEX_ST_BARRIER_TIMEOUT on the limit) when the
-// consumer must give up because of the limit or another error.  The sleep
-// between polls grows from ~30 ns to ~0.2 us so that many waiting waves do
-// not flood the memory system with polls.
-__device__ __forceinline__ bool keep_waiting(int32_t *status, uint64_t t0, uint64_t timeout_ticks, int &naps) {
-  if (load_status(status) != 0) return false;
-  if (wall_clock64() - t0 > timeout_ticks) {
-    raise_status(status, CORTEX_ST_BARRIER_TIMEOUT);
-    return false;
-  }
-  if (naps < 8) __builtin_amdgcn_s_sleep(1);
-  else __builtin_amdgcn_s_sleep(8);
-  ++naps;
-  return true;
-}
-
 // Wait until every global store this wave issued has completed.  A plain
 // __syncthreads() does not do this on gfx950, and the agent-scope release
 // below is issued by one wave only.
-__device__ __forceinline__ void wave_stores_complete() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+constexpr int kWaitVmcntZero = 0x0F70;       // s_waitcnt vmcnt(0), other counters not waited on
+__device__ __forceinline__ void wave_stores_complete() { __builtin_amdgcn_s_waitcnt(kWaitVmcntZero); }
 
 // ---------------------------------------------------------------------------
 // Device-wide barrier for a persistent launch (all workgroups co-resident).
@@ -299,11 +258,18 @@ __device__ __forceinline__ floatx4 mfma_k16(float4 a4, float4 b4, floatx4 c) {
 }
 
 // ---------------------------------------------------------------------------
-// Scalar math.  tanhf/expf are the ROCm device-library functions (accurate to
-// a few ulp); sigmoid is written from its definition 1/(1+exp(-z)).
+// Gate nonlinearities from their definitions, on the hardware base-2
+// exponential and reciprocal (v_exp_f32, v_rcp_f32, about 1 ulp each):
+//   sigmoid(z) = 1 / (1 + e^-z),   tanh(z) = 1 - 2 / (1 + e^2z).
+// Overflow of the exponential gives the right limits (1/inf = 0).  The
+// absolute error is a few 1e-7 over the whole range; tanh near 0 loses
+// relative, not absolute, accuracy to the cancellation.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + expf(-z)); }
-__device__ __forceinline__ float tanh_f(float z) { return tanhf(z); }
+__device__ __forceinline__ float exp_fast(float z) { return __builtin_amdgcn_exp2f(z * 1.4426950408889634f); }
+__device__ __forceinline__ float sigmoidf(float z) { return __builtin_amdgcn_rcpf(1.0f + exp_fast(-z)); }
+__device__ __forceinline__ float tanh_f(float z) {
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + exp_fast(2.0f * z));
+}
 
 template <typename T>
 __device__ __forceinline__ T ld_nt(const T *p) { return __builtin_nontemporal_load(p); }

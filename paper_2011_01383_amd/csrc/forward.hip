@@ -4,23 +4,23 @@
 // One launch runs every level.  Workgroup b owns hidden slice s = b % S
 // (J hidden units, all gates of those units) and node group q = b / S.  Its
 // slice of the cell weights is loaded into LDS once and stays there for the
-// whole pass (persistence).  Rows are cut into 16-row tiles on a fixed grid
-// (tile t = rows [16t, 16t+16)); at level l, group q takes the tiles t = q
-// (mod Q) that intersect the level's rows.  For a tile, each of the 8 waves
-// loads its share of the input rows (child states, and the node input where
-// the cell fuses it) straight into registers in the MFMA operand layout,
-// contracts it with the resident weight slice on the fp32 MFMA units, and the
-// partial sums meet in LDS for the gate nonlinearities, which write the
-// slice's J columns of the new states.  The next tile's rows are requested
-// before the current tile's contraction, so load latency overlaps compute.
+// whole pass (persistence).  The rows of level l are cut into 16-row tiles
+// starting at the level's first row; group q takes the tiles u with
+// (u + l) % Q == q.  For a tile, each of the 8 waves loads its share of the
+// operand rows (child states, and the node input where the cell fuses it)
+// straight into registers in the MFMA operand layout and contracts it with the
+// resident weight slice on the fp32 MFMA units; the partial sums meet in LDS,
+// where the threads of the workgroup apply the gate nonlinearities together
+// and write the slice's J columns of the new states.
 //
-// A device-wide barrier separates levels (the dependence is carried by the
-// level loop only, Appendix A.4).  States written by other workgroups move
-// through device-scope loads and stores (DevBuf), so the barrier needs no L2
-// write-back or invalidate.  TreeRNN and N-ary TreeLSTM leaves are the inputs
-// themselves (specialization, Sec. 3.1; zero initial memory cell, Sec. 4.3):
-// a level reading a leaf child takes the row from the input table directly,
-// which removes the barrier after the leaf level.
+// Levels are ordered per datum, not by a device-wide barrier.  The dependence
+// is carried by the level loop (Appendix A.4) and a level only reads lower
+// levels, so it suffices that every state element is also published as a
+// (value, launch tag) pair with one device-scope store and that a consumer
+// waits for exactly the elements it reads.  TreeRNN and N-ary TreeLSTM leaves
+// are the inputs themselves (specialization, Sec. 3.1; zero initial memory
+// cell, Sec. 4.3): a level reading a leaf child takes the row from the input
+// table directly, so nothing ever waits on the leaf level.
 #include <atomic>
 
 #include "cortex_device.hpp"
@@ -35,26 +35,37 @@ constexpr int CELL_DAG = 16;                 // internal id of the DAG-RNN cell
 
 // Optional timeline (builds with -DCORTEX_TRACE only): every workgroup (up to
 // kTraceBlocks) stamps the 100 MHz wall clock at phase boundaries of every
-// level into trace[block][kTraceLevels][8] (uint64), placed in the workspace
-// after the barrier words.  Row kTraceLevels-1 holds kernel-wide stamps:
-// entry, weights loaded, structure ready, exit.
+// level into trace[block][kTraceLevels][16] (uint64), placed in the workspace
+// after the barrier words: slots 0-5 are phases seen by wave 0, slot 8 + w is
+// the time wave w had all its operands.  Row kTraceLevels-1 holds kernel-wide
+// stamps: entry, weights loaded, structure ready, exit.
 constexpr int kTraceLevels = 64;
 constexpr int kTraceBlocks = 256;
+constexpr int kTraceSlots = 16;
 #ifdef CORTEX_TRACE
-constexpr size_t kTraceBytes = (size_t)kTraceBlocks * kTraceLevels * 8 * sizeof(uint64_t);
-#define CORTEX_TRACE_AT(row, k)                                                              \
-  do {                                                                                      \
-    if (threadIdx.x == 0 && blockIdx.x < kTraceBlocks)                                      \
-      a.trace[((size_t)blockIdx.x * kTraceLevels + (row)) * 8 + (k)] = wall_clock64();       \
+constexpr size_t kTraceBytes = (size_t)kTraceBlocks * kTraceLevels * kTraceSlots * sizeof(uint64_t);
+#define CORTEX_TRACE_AT(row, k)                                                                        \
+  do {                                                                                                \
+    if (threadIdx.x == 0 && blockIdx.x < kTraceBlocks)                                                \
+      a.trace[((size_t)blockIdx.x * kTraceLevels + (row)) * kTraceSlots + (k)] = wall_clock64();      \
   } while (0)
 #define CORTEX_TRACE_POINT(lvl, k) CORTEX_TRACE_AT(min((lvl), kTraceLevels - 2), k)
 #define CORTEX_TRACE_KERNEL(k) CORTEX_TRACE_AT(kTraceLevels - 1, k)
+#define CORTEX_TRACE_WAVE(lvl)                                                                          \
+  do {                                                                                                \
+    if ((threadIdx.x & 63) == 0 && blockIdx.x < kTraceBlocks)                                         \
+      a.trace[((size_t)blockIdx.x * kTraceLevels + min((lvl), kTraceLevels - 2)) * kTraceSlots + 8 +   \
+              (threadIdx.x >> 6)] = wall_clock64();                                                   \
+  } while (0)
 #else
 constexpr size_t kTraceBytes = 0;
 #define CORTEX_TRACE_POINT(lvl, k) \
   do {                             \
   } while (0)
 #define CORTEX_TRACE_KERNEL(k) \
+  do {                         \
+  } while (0)
+#define CORTEX_TRACE_WAVE(lvl) \
   do {                         \
   } while (0)
 #endif
@@ -92,44 +103,40 @@ struct Structure {
   __device__ int node_of(int r) const { return node[r]; }
 };
 
+// Gates, contraction depth and default units per slice of each cell.
 template <int CELL, int H>
-struct Cfg;
+struct Cell;
 template <int H>
-struct Cfg<CORTEX_TREE_RNN, H> {
-  static constexpr int J = (H <= 64) ? H : 16, GATES = 1, KA = 2 * H;
+struct Cell<CORTEX_TREE_RNN, H> {
+  static constexpr int GATES = 1, KA = 2 * H, J = (H <= 64) ? H : 16;
 };
 template <int H>
-struct Cfg<CORTEX_NARY_TREELSTM, H> {
-  static constexpr int J = 4, GATES = 5, KA = 2 * H;
+struct Cell<CORTEX_NARY_TREELSTM, H> {
+  static constexpr int GATES = 5, KA = 2 * H, J = 4;
 };
 template <int H>
-struct Cfg<CORTEX_CHILDSUM_TREELSTM, H> {
-  static constexpr int J = 4, GATES = 4, KA = 2 * H;
+struct Cell<CORTEX_CHILDSUM_TREELSTM, H> {
+  static constexpr int GATES = 4, KA = 2 * H, J = 4;
 };
 template <int H>
-struct Cfg<CELL_DAG, H> {
-  static constexpr int J = 16, GATES = 1, KA = 3 * H;
+struct Cell<CELL_DAG, H> {
+  static constexpr int GATES = 1, KA = 3 * H, J = 16;
 };
 
-template <int CELL, int H>
+template <int CELL, int H, int J_>
 struct Dims {
-  using C = Cfg<CELL, H>;
-  static constexpr int J = C::J, GATES = C::GATES, KA = C::KA;
-  static constexpr int MPAD = (GATES * J + 15) / 16 * 16;
+  static constexpr int J = J_, GATES = Cell<CELL, H>::GATES, KA = Cell<CELL, H>::KA;
+  static constexpr int GJ = GATES * J;                     // weight-slice rows
+  static constexpr int MPAD = (GJ + 15) / 16 * 16;
   static constexpr int NT = MPAD / 16;
   static constexpr bool kChildSum = CELL == CORTEX_CHILDSUM_TREELSTM;
-  static constexpr bool kLeafInputs = CELL == CORTEX_TREE_RNN || CELL == CORTEX_NARY_TREELSTM;
-  static constexpr bool kCells = CELL == CORTEX_NARY_TREELSTM || CELL == CORTEX_CHILDSUM_TREELSTM;
-  // generic path: k range per wave, padded to whole 16-blocks (zeros beyond KA)
+  // k range per wave, padded to whole 16-blocks (zeros beyond KA)
   static constexpr int KW = ((KA + kFwdWaves * 16 - 1) / (kFwdWaves * 16)) * 16;
-  static constexpr int NB = KW / 16;                       // float4 loads per lane per tile
-  // child-sum: node part over 4 waves, edge part (64 edge rows) over 8 waves
+  static constexpr int NB = KW / 16;                       // float4 operand loads per lane per tile
+  // child-sum: node part over 4 waves, edge part (64 edge rows) in two k halves
   static constexpr int KWX = H / 4, NBX = KWX / 16;
   static constexpr int KWE = H / 2, NBE = KWE / 16;
   static constexpr int LDW = kChildSum ? (2 * H + 4) : (kFwdWaves * KW + 4);   // weight row stride
-  static constexpr int C_FLOATS = kChildSum ? (4 * 16 * 16 + 2 * 64 * 16) : kFwdWaves * 16 * MPAD;
-  static constexpr int EPI = kTileM * J;                   // epilogue (row, unit) pairs
-  static constexpr int EPI_PER_THREAD = (EPI + kFwdThreads - 1) / kFwdThreads;
   static_assert(H % J == 0, "slices must tile H");
   static_assert(H % 64 == 0, "H must be a multiple of 64");
 };
@@ -140,35 +147,45 @@ __device__ __forceinline__ int childsum_gate(int gslot) {
   return gslot == 0 ? 0 : (gslot == 1 ? 2 : (gslot == 2 ? 3 : 1));
 }
 
-template <int CELL, int H>
+// Copies the workgroup's weight slice into LDS: every load of a thread is
+// issued before the first store, so the copy costs about one round trip.
+template <int CELL, int H, int J>
 __device__ void load_weight_slice(const FwdArgs &a, int hbase, float *W_s, float *bias_s) {
-  using D = Dims<CELL, H>;
+  using D = Dims<CELL, H, J>;
   constexpr int ROW4 = (D::LDW - 4) / 4, SEG4 = H / 4, KA4 = D::KA / 4;
-  for (int idx = threadIdx.x; idx < D::MPAD * ROW4; idx += kFwdThreads) {
+  constexpr int ITEMS = D::MPAD * ROW4, PER = (ITEMS + kFwdThreads - 1) / kFwdThreads;
+  float4 v[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = threadIdx.x + k * kFwdThreads;
     const int m = idx / ROW4, c4 = idx % ROW4;
-    const int g = m / D::J, j = m % D::J, hj = hbase + j;
+    const int g = m / J, j = m % J, hj = hbase + j;
     const int sg = c4 / SEG4, o4 = c4 % SEG4;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (m < D::GATES * D::J && c4 < KA4) {
+    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (idx < ITEMS && m < D::GJ && c4 < KA4) {
       const float *src = nullptr;
       if (CELL == CORTEX_TREE_RNN) src = a.W + (size_t)hj * 2 * H + sg * H;
       if (CELL == CORTEX_NARY_TREELSTM) src = a.U + ((size_t)(sg * 5 + g) * H + hj) * H;
       if (CELL == CORTEX_CHILDSUM_TREELSTM)
         src = (sg == 0 ? a.W : a.U) + ((size_t)childsum_gate(g) * H + hj) * H;
       if (CELL == CELL_DAG) src = (sg == 0 ? a.W : a.U + (size_t)(sg - 1) * H * H) + (size_t)hj * H;
-      v = *(const float4 *)(src + o4 * 4);
+      v[k] = *(const float4 *)(src + o4 * 4);
     }
-    *(float4 *)&W_s[m * D::LDW + c4 * 4] = v;
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = threadIdx.x + k * kFwdThreads;
+    if (idx < ITEMS) *(float4 *)&W_s[(idx / ROW4) * D::LDW + (idx % ROW4) * 4] = v[k];
   }
   for (int m = threadIdx.x; m < D::MPAD; m += kFwdThreads) {
-    const int g = m / D::J, j = m % D::J, hj = hbase + j;
-    float v = 0.f;
-    if (m < D::GATES * D::J) {
-      if (CELL == CORTEX_TREE_RNN || CELL == CELL_DAG) v = a.b[hj];
-      if (CELL == CORTEX_NARY_TREELSTM) v = a.b[g * H + hj];
-      if (CELL == CORTEX_CHILDSUM_TREELSTM) v = a.b[childsum_gate(g) * H + hj];
+    const int g = m / J, j = m % J, hj = hbase + j;
+    float bv = 0.f;
+    if (m < D::GJ) {
+      if (CELL == CORTEX_TREE_RNN || CELL == CELL_DAG) bv = a.b[hj];
+      if (CELL == CORTEX_NARY_TREELSTM) bv = a.b[g * H + hj];
+      if (CELL == CORTEX_CHILDSUM_TREELSTM) bv = a.b[childsum_gate(g) * H + hj];
     }
-    bias_s[m] = v;
+    bias_s[m] = bv;
   }
 }
 
@@ -211,14 +228,13 @@ __device__ bool setup_structure(const FwdArgs &a, int *cache, Structure<kCached>
   __syncthreads();
   // offsets: 0 = off[0] <= ... <= off[L] = N
   int bad = 0;
-  for (int l = threadIdx.x; kCached && l < L; l += kFwdThreads) {
+  for (int l = threadIdx.x; l < L; l += kFwdThreads) {
     const int o0 = st.offset(l), o1 = st.offset(l + 1);
     if (o1 < o0 || (l == 0 && o0 != 0) || (l == L - 1 && o1 != N)) bad = 1;
   }
   // every child row lies in a strictly lower level than its parent row; the
-  // level of a row is found by binary search over the offsets.  (Uncached
-  // structures are checked tile by tile as the level loop reads them.)
-  for (int r = threadIdx.x; kCached && r < N && !bad; r += kFwdThreads) {
+  // level of a row is found by binary search over the offsets
+  for (int r = threadIdx.x; r < N && !bad; r += kFwdThreads) {
     int lo = 0, hi = L - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -243,34 +259,25 @@ template <bool kCached>
 __device__ __forceinline__ int input_row_of(const FwdArgs &a, const Structure<kCached> &st, int r) {
   if (kCached) return st.input_row(r);
   const int v = a.level_nodes[r];
-  if (v < 0 || v >= a.N) {
-    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
-    return -1;
-  }
   const int xi = a.x_index[v];
-  if (xi < -1 || xi >= a.x_rows) {
-    raise_status(a.status, CORTEX_ST_INPUT_RANGE);
-    return -1;
-  }
-  return xi;
+  return (xi < -1 || xi >= a.x_rows) ? -1 : xi;
 }
 
-// Structure of up to kChunkTiles of a workgroup's tiles in one level, staged
-// into LDS in one round trip when the whole linearization is not cached: the
-// operand addresses of a tile then never wait on a global load.
+// Child rows and input rows of up to kChunkTiles of a workgroup's tiles in one
+// level (child-sum kernel), staged into LDS in one pass when the whole
+// linearization is not cached: operand addresses then never wait on a global
+// load.  Chunk tile k is level tile u0 + k*Q, rows r0 + 16*(u0 + k*Q) + i.
 constexpr int kChunkTiles = 16;
 struct ChunkRows {
-  int crow[kChunkTiles][kTileM][4];
-  int node[kChunkTiles][kTileM];
+  int crow[kChunkTiles][kTileM][4];     // child rows, -1 = none
   int xrow[kChunkTiles][kTileM];
 };
 
-template <bool kNeedX, bool kNeedNode>
-__device__ void stage_chunk(const FwdArgs &a, ChunkRows &cr, int c0, int ntiles, int Q, int r0, int r1) {
+__device__ void stage_chunk(const FwdArgs &a, ChunkRows &cr, int u0, int ntiles, int Q, int r0, int r1) {
   for (int idx = threadIdx.x; idx < ntiles * kTileM; idx += kFwdThreads) {
-    const int u = idx / kTileM, i = idx % kTileM;
-    const int row = (c0 + u * Q) * kTileM + i;
-    const bool live = row >= r0 && row < r1;
+    const int k = idx / kTileM, i = idx % kTileM;
+    const int row = r0 + (u0 + k * Q) * kTileM + i;
+    const bool live = row < r1;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       int c = (live && s < a.K) ? a.child_rows[(size_t)row * a.K + s] : -1;
@@ -278,68 +285,249 @@ __device__ void stage_chunk(const FwdArgs &a, ChunkRows &cr, int c0, int ntiles,
         raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
         c = -1;
       }
-      cr.crow[u][i][s] = c;
+      cr.crow[k][i][s] = c;
     }
     int v = live ? a.level_nodes[row] : -1;
     if (v < -1 || v >= a.N) {
       raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
       v = -1;
     }
-    if (kNeedNode) cr.node[u][i] = v;
-    if (kNeedX) {
-      int xi = v >= 0 ? a.x_index[v] : -1;
+    int xi = v >= 0 ? a.x_index[v] : -1;
+    if (xi < -1 || xi >= a.x_rows) {
+      raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+      xi = -1;
+    }
+    cr.xrow[k][i] = xi;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Operand sources of the slice kernels.  A row of the contraction operand is
+// SEGS segments of H values (the two child slots; for DAG-RNN the node input,
+// then the two child slots).  Each (row, segment) gets one code:
+//   c >= 0    the staged state of row c (a child computed in this launch)
+//   c <= -2   plain row -2-c: the input-table row of a leaf child (TreeRNN,
+//             N-ary TreeLSTM, whose leaves are their inputs) or the node's own
+//             input row (DAG-RNN, segment 0)
+//   -1        no source: the segment reads zeros
+// so that forming a tile's load addresses takes one LDS read per segment.
+// ---------------------------------------------------------------------------
+template <int CELL>
+struct SrcCfg {
+  static constexpr int SEGS = CELL == CELL_DAG ? 3 : 2;
+  static constexpr bool kLeafX = CELL == CORTEX_TREE_RNN || CELL == CORTEX_NARY_TREELSTM;
+  static constexpr bool kDag = CELL == CELL_DAG;
+};
+// Largest N whose codes are kept in LDS (the host checks the same bound).
+constexpr int kMaxCachedRows = 2560;
+constexpr int kCachedRowsPerThread = (kMaxCachedRows + kFwdThreads - 1) / kFwdThreads;
+
+// Cached: off[L+1], codes[N*SEGS] and (leaf-input cells) the input row of
+// every row, xrow[N], all in LDS.  Uncached: offsets from global memory and
+// codes staged per chunk of tiles.  Validates 1 <= L <= N, monotone offsets
+// from 0 to N, child rows in a strictly lower level, node ids and input rows
+// in range.
+template <int CELL, bool kCached>
+__device__ bool setup_sources(const FwdArgs &a, int *cache, int &L, const int *&off, const int *&codes,
+                              const int *&xrow) {
+  using SC = SrcCfg<CELL>;
+  constexpr int SEGS = SC::SEGS;
+  const int N = a.N, K = a.K;
+  const int tid = threadIdx.x;
+  L = *a.num_levels;
+  if (L < 1 || L > N) {
+    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+    return false;
+  }
+  int bad = 0;
+  if (!kCached) {
+    off = a.level_offsets;
+    codes = nullptr;
+    xrow = nullptr;
+    for (int l = tid; l < L; l += kFwdThreads) {
+      const int o0 = off[l], o1 = off[l + 1];
+      if (o1 < o0 || (l == 0 && o0 != 0) || (l == L - 1 && o1 != N)) bad = 1;
+    }
+    if (__syncthreads_or(bad)) {
+      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      return false;
+    }
+    return true;
+  }
+  int *o = cache, *cd = cache + (L + 1), *xr = cd + N * SEGS;
+  // one round of independent loads: offsets, node ids (and their input
+  // rows), child rows into registers
+  int ch[kCachedRowsPerThread][2];
+#pragma unroll
+  for (int k = 0; k < kCachedRowsPerThread; ++k) {
+    const int r = tid + k * kFwdThreads;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) ch[k][s] = (r < N && s < K) ? a.child_rows[r * K + s] : -1;
+  }
+  for (int i = tid; i <= L; i += kFwdThreads) o[i] = a.level_offsets[i];
+  for (int r = tid; r < N; r += kFwdThreads) {
+    const int v = a.level_nodes[r];
+    if (v < 0 || v >= N) bad = 1;
+    if (SC::kLeafX) {
+      int xi = (v >= 0 && v < N) ? a.x_index[v] : -1;
       if (xi < -1 || xi >= a.x_rows) {
         raise_status(a.status, CORTEX_ST_INPUT_RANGE);
         xi = -1;
       }
-      cr.xrow[u][i] = xi;
+      xr[r] = xi;
+    }
+    if (SC::kDag) cd[r * SEGS] = (v >= 0 && v < N) ? -2 - v : -1;
+  }
+  __syncthreads();
+  for (int l = tid; l < L; l += kFwdThreads) {
+    const int o0 = o[l], o1 = o[l + 1];
+    if (o1 < o0 || (l == 0 && o0 != 0) || (l == L - 1 && o1 != N)) bad = 1;
+  }
+  const int off1 = o[1];
+#pragma unroll
+  for (int k = 0; k < kCachedRowsPerThread; ++k) {
+    const int r = tid + k * kFwdThreads;
+    if (r >= N) break;
+    // the level of row r, by binary search over the offsets
+    int lo = 0, hi = L - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (o[mid] <= r) lo = mid;
+      else hi = mid - 1;
+    }
+    const int start = o[lo];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      int c = ch[k][s];
+      if (c < -1 || c >= start) {          // a child must sit in a strictly lower level
+        bad = 1;
+        c = -1;
+      }
+      if (SC::kLeafX && c >= 0 && c < off1) c = xr[c] >= 0 ? -2 - xr[c] : -1;
+      if (s < K) cd[r * SEGS + (SC::kDag ? s + 1 : s)] = c;
+    }
+  }
+  if (__syncthreads_or(bad)) {
+    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+    return false;
+  }
+  off = o;
+  codes = cd;
+  xrow = xr;
+  return true;
+}
+
+// Codes of up to kChunkTiles of a workgroup's tiles in one level (uncached
+// linearization), staged into LDS in one pass.  Chunk tile k is level tile
+// u0 + k*Q, rows r0 + 16*(u0 + k*Q) + i.
+struct ChunkSrc {
+  int code[kChunkTiles][kTileM][3];
+};
+
+template <int CELL>
+__device__ void stage_chunk_codes(const FwdArgs &a, ChunkSrc &cs, int u0, int ntiles, int Q, int r0, int r1,
+                                  int off1) {
+  using SC = SrcCfg<CELL>;
+  for (int idx = threadIdx.x; idx < ntiles * kTileM; idx += kFwdThreads) {
+    const int k = idx / kTileM, i = idx % kTileM;
+    const int row = r0 + (u0 + k * Q) * kTileM + i;
+    const bool live = row < r1;
+    if (SC::kDag) {
+      const int v = live ? a.level_nodes[row] : -1;
+      if (v < -1 || v >= a.N) raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      cs.code[k][i][0] = (v >= 0 && v < a.N) ? -2 - v : -1;
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      int c = (live && s < a.K) ? a.child_rows[(size_t)row * a.K + s] : -1;
+      if (c < -1 || c >= r0) {                    // a child must sit in a lower level
+        raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+        c = -1;
+      }
+      if (SC::kLeafX && c >= 0 && c < off1) {     // a leaf child: its input row
+        const int v = a.level_nodes[c];
+        int xi = -1;
+        if (v < 0 || v >= a.N) raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+        else xi = a.x_index[v];
+        if (xi < -1 || xi >= a.x_rows) {
+          raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+          xi = -1;
+        }
+        c = xi >= 0 ? -2 - xi : -1;
+      }
+      cs.code[k][i][SC::kDag ? s + 1 : s] = c;
     }
   }
 }
 
-// Leaf level of TreeRNN / N-ary TreeLSTM, spread evenly over every thread of
-// the launch: h = input row (or 0), c = 0, staged for the level above and
-// written to the outputs.
-template <int H, bool kCached, bool kWithC>
-__device__ void stage_leaves(const FwdArgs &a, const Structure<kCached> &st, const TagBuf &hs, const TagBuf &cs,
-                             int r1, uint32_t tag) {
-  const int total = r1 * H;
+// Leaf level of TreeRNN / N-ary TreeLSTM, spread over every thread of the
+// launch: h = input row (or 0), c = 0.  Nothing waits on these rows (parents
+// read leaf children from the input table), so they are not staged.
+template <int H, bool kWithC>
+__device__ void write_leaf_outputs(const FwdArgs &a, const int *xrow, int r1) {
+  constexpr int H4 = H / 4;
+  const int total = r1 * H4;
   for (int e = blockIdx.x * kFwdThreads + threadIdx.x; e < total; e += gridDim.x * kFwdThreads) {
-    const int r = e / H, col = e % H;
-    const int xr = input_row_of(a, st, r);
-    const float v = xr >= 0 ? a.x_table[(size_t)xr * H + col] : 0.f;
-    hs.store1((uint32_t)e, v, tag);
-    a.h[e] = v;
-    if (kWithC) {
-      cs.store1((uint32_t)e, 0.f, tag);
-      a.c[e] = 0.f;
+    const int r = e / H4, c4 = e % H4;
+    int xr;
+    if (xrow) {
+      xr = xrow[r];
+    } else {
+      const int v = a.level_nodes[r];
+      xr = (v >= 0 && v < a.N) ? a.x_index[v] : -1;
+      if (xr < -1 || xr >= a.x_rows) {
+        raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+        xr = -1;
+      }
     }
+    const float4 v = xr >= 0 ? *(const float4 *)&a.x_table[(size_t)xr * H + 4 * c4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    *(float4 *)&a.h[(size_t)e * 4] = v;
+    if (kWithC) *(float4 *)&a.c[(size_t)e * 4] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
 }
+
+// Operand fragment: four consecutive k of one tile row, either staged (two
+// (value, tag) pairs of pairs in lo and hi) or plain (four floats in lo: an
+// input row, or zeros for an absent source).  Each lane issues only the loads
+// its source needs.
+struct Frag {
+  u32x4 lo, hi;
+  __device__ __forceinline__ bool ready(uint32_t tag) const {
+    return lo.y == tag && lo.w == tag && hi.y == tag && hi.w == tag;
+  }
+  __device__ __forceinline__ float4 value(bool staged) const {
+    return make_float4(as_float(lo.x), as_float(staged ? lo.z : lo.y), as_float(staged ? hi.x : lo.z),
+                       as_float(staged ? hi.z : lo.w));
+  }
+};
 
 // ---------------------------------------------------------------------------
 // TreeRNN, N-ary TreeLSTM and DAG-RNN.
-//   A row of a tile = [h(slot 0) | h(slot 1)]   (TreeRNN, N-ary TreeLSTM)
-//                   = [x | h(slot 0) | h(slot 1)]   (DAG-RNN)
-// Wave w owns the columns [w*KW, (w+1)*KW) of A (zero beyond KA).
-//
-// No device-wide barrier: a workgroup moves on to the next level as soon as
-// its own tiles are done.  Child states come from the tagged staging buffers
-// (hs, cs); a fragment whose tag is not yet this launch's is loaded again
-// until it is, with a wall-clock limit.  Levels only read lower levels and
-// every workgroup walks the levels upwards, so the waits always end.
+//   A row of a tile = [h(slot 0) | h(slot 1)]        (TreeRNN, N-ary TreeLSTM)
+//                   = [x | h(slot 0) | h(slot 1)]    (DAG-RNN)
+// Wave w owns the columns [w*KW, (w+1)*KW) of A (zero beyond KA); in block b
+// lane group g (lanes 16g .. 16g+15) takes the columns w*KW + 16b + 4g ..+3,
+// so the four lane groups of a row read one 128-byte span of staged pairs
+// with each pair of load instructions.
 // ---------------------------------------------------------------------------
-template <int CELL, int H, bool kCached>
+template <int CELL, int H, int J, bool kCached>
 __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
-  using D = Dims<CELL, H>;
-  constexpr int J = D::J, MPAD = D::MPAD, NT = D::NT, LDW = D::LDW, KW = D::KW, NB = D::NB;
-  constexpr int KA = D::KA, EPT = D::EPI_PER_THREAD;
-  constexpr bool kLeafInputs = D::kLeafInputs;
+  using D = Dims<CELL, H, J>;
+  constexpr int GJ = D::GJ, MPAD = D::MPAD, NT = D::NT, LDW = D::LDW, KW = D::KW, NB = D::NB, KA = D::KA;
+  constexpr bool kLeafInputs = CELL == CORTEX_TREE_RNN || CELL == CORTEX_NARY_TREELSTM;
+  constexpr bool kLstm = CELL == CORTEX_NARY_TREELSTM;
+  constexpr int EPI = kTileM * J;          // (row, unit) pairs of a tile
+  constexpr int SEGS = SrcCfg<CELL>::SEGS;
+  // A block's 16 columns never straddle two operand segments (H is a
+  // multiple of 16), so the segment of block b is the same for the whole
+  // wave; a wave's range touches at most two segments (KW <= H).
+  static_assert(KA == SEGS * H && KA <= kFwdWaves * KW && KW <= H && H % 16 == 0, "block layout");
 
   __shared__ __attribute__((aligned(16))) float W_s[MPAD * LDW];
-  __shared__ __attribute__((aligned(16))) float C_s[D::C_FLOATS];
+  __shared__ __attribute__((aligned(16))) float C_s[kFwdWaves * kTileM * MPAD];
+  __shared__ float Z_s[kLstm ? kTileM * GJ : 1];
   __shared__ float bias_s[MPAD];
-  __shared__ ChunkRows chunk;
+  __shared__ ChunkSrc chunk;
   extern __shared__ int cache[];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -349,155 +537,147 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   const int N = a.N;
   const uint32_t tag = a.tag;
   const TagBuf hs(a.hs, (uint32_t)N * H * 8);
-  const TagBuf cs(a.cs, a.cs ? (uint32_t)N * H * 8 : 0u);
-  const InBuf xin(a.x, a.x ? (uint32_t)N * H * 4 : 0u);
+  const TagBuf cs(a.cs, kLstm ? (uint32_t)N * H * 8 : 0u);
+  // plain operand rows: the input table (leaf children) or the DAG inputs
+  const InBuf xin(CELL == CELL_DAG ? (const void *)a.x : (const void *)a.x_table,
+                  CELL == CELL_DAG ? (a.x ? (uint32_t)N * H * 4 : 0u)
+                                   : (kLeafInputs && a.x_table ? (uint32_t)a.x_rows * H * 4 : 0u));
+  // this wave's columns: segment sgA from column o0 within it, crossing into
+  // segment sgA + 1 at block cross_b (NB when it does not)
+  const int kw = wave * KW;
+  const int sgA = kw / H, o0 = kw % H;
+  const int cross_b = (H - o0) / 16 < NB ? (H - o0) / 16 : NB;
 
   CORTEX_TRACE_KERNEL(0);
   if (load_status(a.status) != 0) return;
-  load_weight_slice<CELL, H>(a, hbase, W_s, bias_s);
+  load_weight_slice<CELL, H, J>(a, hbase, W_s, bias_s);
   CORTEX_TRACE_KERNEL(1);
-  Structure<kCached> st;
   int L;
-  if (!setup_structure<kCached, kLeafInputs, CELL == CELL_DAG>(a, cache, st, L)) return;
+  const int *off, *codes, *xrow;
+  if (!setup_sources<CELL, kCached>(a, cache, L, off, codes, xrow)) return;
   CORTEX_TRACE_KERNEL(2);
+  const int off1 = off[1];
+  int gave_up = 0;
 
   for (int l = 0; l < L; ++l) {
     CORTEX_TRACE_POINT(l, 0);
-    const int r0 = st.offset(l), r1 = st.offset(l + 1);
+    const int r0 = off[l], r1 = off[l + 1];
     if (!kCached && (r1 < r0 || r1 > N || (l == 0 && r0 != 0))) {
       raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
       return;
     }
-    const int t_lo = r0 / kTileM, t_hi = (r1 - 1) / kTileM;
-    const int t_first = t_lo + ((group - t_lo % Q) % Q + Q) % Q;
-
     if (kLeafInputs && l == 0) {
-      stage_leaves<H, kCached, CELL == CORTEX_NARY_TREELSTM>(a, st, hs, cs, r1, tag);
+      write_leaf_outputs<H, kLstm>(a, kCached ? xrow : nullptr, r1);
       continue;
     }
+    const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
+    int u0 = ((group - l) % Q + Q) % Q;            // first tile of the current chunk
 
-    // structure accessors of the current chunk of tiles
-    int c0 = t_first;
-    auto crow = [&](int t, int i, int s) -> int {
-      if (kCached) return s < a.K ? st.child(t * kTileM + i, s) : -1;
-      return chunk.crow[(t - c0) / Q][i][s];
+    // source code of tile u, row i, segment sg (cached, or the staged chunk)
+    auto code_of = [&](int u, int i, int sg) __attribute__((always_inline)) -> int {
+      if (kCached) return codes[(r0 + u * kTileM + i) * SEGS + sg];
+      return chunk.code[(u - u0) / Q][i][sg];
     };
-    auto node_of = [&](int t, int i) -> int {
-      if (kCached) return st.node_of(t * kTileM + i);
-      return chunk.node[(t - c0) / Q][i];
+    auto code_b = [&](const int (&cd)[2], int b) __attribute__((always_inline)) -> int {
+      return b >= cross_b ? cd[1] : cd[0];
     };
-
-    // A fragment of (tile t, lane row i16, wave-uniform k block kk).  Both
-    // loads are always issued (an absent source reads zeros); returns the
-    // staged element index to wait on, or -1 (raw = plain input or zeros).
-    auto load_a = [&](int t, int kk, Frag4 &f, bool &raw) -> int {
-      const int row = t * kTileM + i16;
-      const bool live = row >= r0 && row < r1 && kk < KA;
-      const int sg = kk / H, o = kk % H + 4 * g4;
-      const bool is_x = CELL == CELL_DAG && sg == 0;
-      uint32_t xoff = kNoSource, soff = kNoSource;
-      int e = -1;
-      if (live && is_x) {
-        const int nd = node_of(t, i16);
-        if (nd >= 0 && nd < N) xoff = (uint32_t)((nd * H + o) * 4);
-      } else if (live) {
-        const int cr = crow(t, i16, CELL == CELL_DAG ? sg - 1 : sg);
-        if (cr >= 0) e = cr * H + o;
-      }
-      if (e >= 0) soff = (uint32_t)e * 8u;
-      if (CELL == CELL_DAG) {
-        // x blocks and state blocks are wave-uniform; one of the two loads reads zeros
-        const u32x4 xv = xin.load4(xoff);
-        f.lo = hs.load2_at(soff);
-        f.hi = hs.load2_at(soff + 16u);
-        if (is_x) f.lo = xv;
-      } else {
-        f.lo = hs.load2_at(soff);
-        f.hi = hs.load2_at(soff + 16u);
-      }
-      raw = e < 0;
-      return e;
-    };
-    // staged memory cells of the children of epilogue pair e (N-ary only)
-    auto load_cc = [&](int t, u32x2 (&cc)[EPT][2], int (&ce)[EPT][2]) {
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          cc[e][s] = u32x2{0u, tag};
-          ce[e][s] = -1;
-        }
-        if (!D::kCells) continue;
-        const int p = tid + e * kFwdThreads;
-        const int row = t * kTileM + p / J, hj = hbase + p % J;
-        const bool live = p < D::EPI && row >= r0 && row < r1;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const int cr = live ? crow(t, p / J, s) : -1;
-          if (cr >= 0 && cr < r0) ce[e][s] = cr * H + hj;
-          cc[e][s] = cs.load1_at(ce[e][s] >= 0 ? (uint32_t)ce[e][s] * 8u : kNoSource);
-        }
-      }
+    auto col_b = [&](int b) __attribute__((always_inline)) -> int {   // this lane's first column in block b
+      return (b >= cross_b ? o0 + 16 * b - H : o0 + 16 * b) + 4 * g4;
     };
 
-    Frag4 fa[NB], fn[NB];
-    int ea[NB], en[NB];
-    bool ra[NB], rn[NB];
-    u32x2 cc[EPT][2], ccn[EPT][2];
-    int cea[EPT][2], cen[EPT][2];
-    for (; c0 <= t_hi; c0 += Q * kChunkTiles) {
-    const int c_last = min(t_hi, c0 + Q * (kChunkTiles - 1));
-    if (!kCached) {
-      __syncthreads();                // the previous chunk's structure is no longer read
-      stage_chunk<false, CELL == CELL_DAG>(a, chunk, c0, (c_last - c0) / Q + 1, Q, r0, r1);
-      __syncthreads();
-    }
-#pragma unroll
-    for (int b = 0; b < NB; ++b) ea[b] = load_a(c0, wave * KW + 16 * b, fa[b], ra[b]);
-    load_cc(c0, cc, cea);
-    for (int t = c0; t <= c_last; t += Q) {
-      const int tn = t + Q;
-      if (tn <= c_last) {               // request the next tile before computing this one
-#pragma unroll
-        for (int b = 0; b < NB; ++b) en[b] = load_a(tn, wave * KW + 16 * b, fn[b], rn[b]);
-        load_cc(tn, ccn, cen);
+    // Operands of tile u for this lane: fragments f, the row's source codes
+    // cd (this lane's segment and the next), and (N-ary) the staged memory
+    // cells cc of pair tid's non-leaf children (elements ce).
+    auto issue = [&](int u, Frag (&f)[NB], int (&cd)[2], u32x2 (&cc)[2], int (&ce)[2]) __attribute__((always_inline)) {
+      const int row = r0 + u * kTileM + i16;
+      cd[0] = cd[1] = -1;
+      if (row < r1 && sgA < SEGS) {
+        cd[0] = code_of(u, i16, sgA);
+        if (cross_b < NB && sgA + 1 < SEGS) cd[1] = code_of(u, i16, sgA + 1);
       }
-      CORTEX_TRACE_POINT(l, 1);
-      // ---- wait for staged fragments that are not this launch's yet: poll
-      //      one element, then load the fragment again ----
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        if (ea[b] >= 0 && !fa[b].staged_ready(tag)) {
-          const uint64_t t0 = wall_clock64();
-          int naps = 0;
-          do {
-            while (hs.load1((uint32_t)ea[b] + 3).y != tag && keep_waiting(a.status, t0, a.timeout, naps)) {
-            }
-            fa[b].lo = hs.load2((uint32_t)ea[b]);
-            fa[b].hi = hs.load2((uint32_t)ea[b] + 2);
-          } while (!fa[b].staged_ready(tag) && keep_waiting(a.status, t0, a.timeout, naps));
+        const int c = code_b(cd, b), o = col_b(b);
+        if (c >= 0) {
+          const uint32_t so = (uint32_t)(c * H + o) * 8u;
+          f[b].lo = hs.load2_at(so);
+          f[b].hi = hs.load2_at(so + 16u);
+        } else {
+          // both halves written on both paths: a store to a selected half
+          // would force the fragments out of registers
+          f[b].lo = xin.load4(c <= -2 ? (uint32_t)(((-2 - c) * H + o) * 4) : kNoSource);
+          f[b].hi = u32x4{0u, 0u, 0u, 0u};
         }
       }
+      if (kLstm) {
+        const int prow = r0 + u * kTileM + tid / J;
+        const bool live = tid < EPI && prow < r1;
 #pragma unroll
-      for (int e = 0; e < EPT; ++e)
+        for (int s = 0; s < 2; ++s) {
+          const int c = live ? code_of(u, tid / J, s) : -1;
+          ce[s] = c >= 0 ? c * H + hbase + tid % J : -1;
+          cc[s] = cs.load1_at(ce[s] >= 0 ? (uint32_t)ce[s] * 8u : kNoSource);
+        }
+      }
+    };
+    auto all_ready = [&](const Frag (&f)[NB], const int (&cd)[2], const u32x2 (&cc)[2],
+                         const int (&ce)[2]) __attribute__((always_inline)) -> bool {
+      bool r = true;
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
-          if (cea[e][s] >= 0 && cc[e][s].y != tag) {
-            const uint64_t t0 = wall_clock64();
-            int naps = 0;
-            do {
-              cc[e][s] = cs.load1((uint32_t)cea[e][s]);
-            } while (cc[e][s].y != tag && keep_waiting(a.status, t0, a.timeout, naps));
+      for (int b = 0; b < NB; ++b) r = r && (code_b(cd, b) < 0 || f[b].ready(tag));
+      if (kLstm) {
+#pragma unroll
+        for (int s = 0; s < 2; ++s) r = r && (ce[s] < 0 || cc[s].y == tag);
+      }
+      return r;
+    };
+
+    // One tile: wait for its staged operands, request the next tile's, contract,
+    // apply the gates, write the states.
+    auto process = [&](int u, Frag (&f)[NB], int (&cd)[2], u32x2 (&cc)[2], int (&ce)[2], bool more,
+                       Frag (&fn)[NB], int (&cdn)[2], u32x2 (&ccn)[2], int (&cen)[2]) __attribute__((always_inline)) {
+      CORTEX_TRACE_POINT(l, 1);
+      if (!gave_up && !all_ready(f, cd, cc, ce)) {
+        const uint64_t t0 = wall_clock64();
+        for (;;) {
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int b = 0; b < NB; ++b) {
+            const int c = code_b(cd, b);
+            if (c >= 0 && !f[b].ready(tag)) {
+              const uint32_t so = (uint32_t)(c * H + col_b(b)) * 8u;
+              f[b].lo = hs.load2_at(so);
+              f[b].hi = hs.load2_at(so + 16u);
+            }
           }
+          if (kLstm) {
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+              if (ce[s] >= 0 && cc[s].y != tag) cc[s] = cs.load1_at((uint32_t)ce[s] * 8u);
+          }
+          const int stv = load_status(a.status);
+          if (all_ready(f, cd, cc, ce)) break;
+          if (stv != 0) {
+            gave_up = 1;
+            break;
+          }
+          if (wall_clock64() - t0 > a.timeout) {
+            raise_status(a.status, CORTEX_ST_BARRIER_TIMEOUT);
+            gave_up = 1;
+            break;
+          }
+        }
+      }
       CORTEX_TRACE_POINT(l, 2);
+      if (more) issue(u + Q, fn, cdn, ccn, cen);   // in flight during this tile's contraction
       // ---- contraction: partial sums of this wave's k range ----
       floatx4 acc0[NT], acc1[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc0[nt] = acc1[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      const float *brow = &W_s[i16 * LDW + wave * KW + 4 * g4];
+      const float *brow = &W_s[i16 * LDW + kw + 4 * g4];
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        const float4 av = fa[b].value(ra[b]);
+        const float4 av = f[b].value(code_b(cd, b) >= 0);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           const float4 bv = *(const float4 *)(brow + nt * 16 * LDW + 16 * b);
@@ -505,58 +685,84 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
           else acc0[nt] = mfma_k16(av, bv, acc0[nt]);
         }
       }
+      CORTEX_TRACE_WAVE(l);
+      // The next tile's loads complete here, before this tile's stores: no
+      // load is then pending behind a store, and the next tile starts with
+      // its operands in registers.
+      __builtin_amdgcn_s_waitcnt(kWaitVmcntZero);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
-          C_s[(wave * 16 + 4 * g4 + v) * MPAD + nt * 16 + i16] = acc0[nt][v] + acc1[nt][v];
+          C_s[(wave * kTileM + 4 * g4 + v) * MPAD + nt * 16 + i16] = acc0[nt][v] + acc1[nt][v];
       __syncthreads();
       CORTEX_TRACE_POINT(l, 3);
-      // ---- epilogue: gates and the slice's columns of the new states ----
+      // ---- gates: one thread per (row, gate row) sums the wave partials
+      //      and applies the nonlinearity; TreeRNN / DAG-RNN rows are done
+      //      here, N-ary TreeLSTM combines the gates below ----
+      for (int p = tid; p < kTileM * GJ; p += kFwdThreads) {
+        const int i = p / GJ, m = p % GJ;
+        float sum = bias_s[m];
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        const int p = tid + e * kFwdThreads;
-        if (p >= D::EPI) continue;
-        const int i = p / J, j = p % J;
-        const int row = t * kTileM + i, hj = hbase + j;
-        if (row < r0 || row >= r1) continue;
-        float z[D::GATES];
-#pragma unroll
-        for (int gg = 0; gg < D::GATES; ++gg) {
-          const int m = gg * J + j;
-          float sum = bias_s[m];
-#pragma unroll
-          for (int w = 0; w < kFwdWaves; ++w) sum += C_s[(w * 16 + i) * MPAD + m];
-          z[gg] = sum;
-        }
-        const uint32_t el = (uint32_t)(row * H + hj);
-        float hv;
-        if constexpr (CELL == CORTEX_NARY_TREELSTM) {    // gates (i, f_l, f_r, o, u)
-          const float cl = as_float(cc[e][0].x), cr = as_float(cc[e][1].x);
-          const float cn = sigmoidf(z[0]) * tanh_f(z[4]) + sigmoidf(z[1]) * cl + sigmoidf(z[2]) * cr;
-          hv = sigmoidf(z[3]) * tanh_f(cn);
-          cs.store1(el, cn, tag);
-          a.c[el] = cn;
+        for (int w = 0; w < kFwdWaves; ++w) sum += C_s[(w * kTileM + i) * MPAD + m];
+        if constexpr (kLstm) {
+          Z_s[p] = m >= 4 * J ? tanh_f(sum) : sigmoidf(sum);      // gates (i, f_l, f_r, o | u)
         } else {
-          hv = tanh_f(z[0]);
+          const int row = r0 + u * kTileM + i;
+          if (row < r1) {
+            const uint32_t el = (uint32_t)(row * H + hbase + m);
+            const float hv = tanh_f(sum);
+            hs.store1(el, hv, tag);
+            a.h[el] = hv;
+          }
         }
-        hs.store1(el, hv, tag);
-        a.h[el] = hv;
+      }
+      if constexpr (kLstm) {
+        __syncthreads();
+        const int row = r0 + u * kTileM + tid / J;
+        if (tid < EPI && row < r1) {
+          const int j = tid % J;
+          const float *z = &Z_s[(tid / J) * GJ];
+          const float cn = z[j] * z[4 * J + j] + z[J + j] * as_float(cc[0].x) + z[2 * J + j] * as_float(cc[1].x);
+          const float hv = z[3 * J + j] * tanh_f(cn);
+          const uint32_t el = (uint32_t)(row * H + hbase + j);
+          cs.store1(el, cn, tag);
+          hs.store1(el, hv, tag);
+          a.c[el] = cn;
+          a.h[el] = hv;
+        }
       }
       __syncthreads();
       CORTEX_TRACE_POINT(l, 4);
-      if (tn <= c_last) {
-#pragma unroll
-        for (int b = 0; b < NB; ++b) fa[b] = fn[b], ea[b] = en[b], ra[b] = rn[b];
-#pragma unroll
-        for (int e = 0; e < EPT; ++e)
-#pragma unroll
-          for (int s = 0; s < 2; ++s) cc[e][s] = ccn[e][s], cea[e][s] = cen[e][s];
+    };
+
+    // Two operand sets in turn: the next tile's loads are in flight while
+    // the current tile is computed, with no register copies between tiles.
+    Frag fa[NB], fb[NB];
+    int cda[2], cdb[2], cea[2] = {-1, -1}, ceb[2] = {-1, -1};
+    u32x2 cca[2], ccb[2];
+    for (; u0 < ntile; u0 += Q * kChunkTiles) {
+      const int u_last = min(ntile - 1, u0 + Q * (kChunkTiles - 1));
+      if (!kCached) {
+        __syncthreads();                // the previous chunk's codes are no longer read
+        stage_chunk_codes<CELL>(a, chunk, u0, (u_last - u0) / Q + 1, Q, r0, r1, off1);
+        __syncthreads();
+      }
+      issue(u0, fa, cda, cca, cea);
+      CORTEX_TRACE_POINT(l, 6);
+      for (int u = u0;;) {
+        bool more = u + Q <= u_last;
+        process(u, fa, cda, cca, cea, more, fb, cdb, ccb, ceb);
+        u += Q;
+        if (!more) break;
+        more = u + Q <= u_last;
+        process(u, fb, cdb, ccb, ceb, more, fa, cda, cca, cea);
+        u += Q;
+        if (!more) break;
       }
     }
-    }
     CORTEX_TRACE_POINT(l, 5);
-    if (load_status(a.status) != 0) return;
+    if (__syncthreads_or(gave_up)) return;
   }
   CORTEX_TRACE_KERNEL(3);
 }
@@ -564,25 +770,28 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
 // ---------------------------------------------------------------------------
 // Child-sum TreeLSTM.  Per tile of 16 nodes: the node part x W^T (k split
 // over waves 0-3) and the edge part h_k U^T for the 16 x 4 child slots (edge
-// tile m = wave & 3, k half = wave >> 2).  The epilogue forms
+// tile m = wave & 3, k half = wave >> 2).  The gates are then
 //   i, o, u = s(W x + sum_k U h_k + b),  f_k = s(W_f x + U_f h_k + b_f),
 //   c = i*u + sum_k f_k * c_k,  h = o * tanh(c)
-// (U h~ is taken as sum_k U h_k: the same sum in another order).  Child states
-// are read from the tagged staging buffers as in the kernel above.
+// (U h~ is taken as sum_k U h_k: the same sum in another order; an absent
+// slot reads zero rows, so it adds exactly zero).  Child states come from the
+// tagged staging as in the kernel above.
 // ---------------------------------------------------------------------------
 template <int H, bool kCached>
 __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a) {
-  using D = Dims<CORTEX_CHILDSUM_TREELSTM, H>;
-  constexpr int J = D::J, LDW = D::LDW, NBX = D::NBX, NBE = D::NBE, KWX = D::KWX, KWE = D::KWE;
-  static_assert(D::MPAD == 16 && D::EPI <= kFwdThreads, "one n-tile, one pair per thread");
+  constexpr int J = 4;
+  using D = Dims<CORTEX_CHILDSUM_TREELSTM, H, J>;
+  constexpr int LDW = D::LDW, NBX = D::NBX, NBE = D::NBE, KWX = D::KWX, KWE = D::KWE;
+  constexpr int ZW = 7 * J;                 // per row: i, o, u, then f_k * c_k for 4 slots
+  static_assert(D::MPAD == 16 && kTileM * ZW <= kFwdThreads, "one n-tile, one gate item per thread");
 
   __shared__ __attribute__((aligned(16))) float W_s[16 * LDW];
-  __shared__ __attribute__((aligned(16))) float C_s[D::C_FLOATS];
+  __shared__ __attribute__((aligned(16))) float Cx[4 * 16 * 16];     // [4 waves][16 nodes][16]
+  __shared__ __attribute__((aligned(16))) float Ce[2 * 64 * 16];     // [2 halves][64 edges][16]
+  __shared__ float Z_s[kTileM * ZW];
   __shared__ float bias_s[16];
   __shared__ ChunkRows chunk;
   extern __shared__ int cache[];
-  float *Cx = C_s;                    // [4 waves][16 nodes][16]
-  float *Ce = C_s + 4 * 16 * 16;      // [2 halves][64 edges][16]
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
@@ -595,15 +804,27 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
   const InBuf xin(a.x_table, (uint32_t)a.x_rows * H * 4);
   const int em = wave & 3, ehalf = wave >> 2;           // edge m-tile and k half of this wave
   const int e_node = (16 * em + i16) >> 2, e_slot = (16 * em + i16) & 3;
+  const int ek = ehalf * KWE + 4 * g4;                  // this lane's edge column in block 0 (16 per block)
+  // gate item of this thread: row zi, slot zk (0..2 = i, o, u; 3.. = forget of child zk-3), unit zj
+  const int zi = tid / ZW, zk = (tid % ZW) / J, zj = tid % J;
 
   CORTEX_TRACE_KERNEL(0);
   if (load_status(a.status) != 0) return;
-  load_weight_slice<CORTEX_CHILDSUM_TREELSTM, H>(a, hbase, W_s, bias_s);
+  load_weight_slice<CORTEX_CHILDSUM_TREELSTM, H, J>(a, hbase, W_s, bias_s);
   CORTEX_TRACE_KERNEL(1);
   Structure<kCached> st;
   int L;
   if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
   CORTEX_TRACE_KERNEL(2);
+  int gave_up = 0;
+
+  struct TileOps {
+    u32x4 xv[NBX];
+    Frag ev[NBE];
+    int ecr;
+    u32x2 cc;
+    int ce;
+  };
 
   for (int l = 0; l < L; ++l) {
     CORTEX_TRACE_POINT(l, 0);
@@ -612,145 +833,142 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
       raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
       return;
     }
-    const int t_lo = r0 / kTileM, t_hi = (r1 - 1) / kTileM;
-    const int t_first = t_lo + ((group - t_lo % Q) % Q + Q) % Q;
+    const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
+    int u0 = ((group - l) % Q + Q) % Q;
 
-    // structure accessors of the current chunk of tiles
-    int c0 = t_first;
-    auto child = [&](int t, int i, int s) -> int {
-      const int row = t * kTileM + i;
-      if (row < r0 || row >= r1 || s >= K) return -1;
+    auto child = [&](int u, int i, int s) __attribute__((always_inline)) -> int {
+      const int row = r0 + u * kTileM + i;
+      if (row >= r1 || s >= K) return -1;
       if (kCached) return st.child(row, s);
-      return chunk.crow[(t - c0) / Q][i][s];
+      return chunk.crow[(u - u0) / Q][i][s];
     };
-    auto xrow_of = [&](int t, int i) -> int {
-      if (kCached) return st.input_row(t * kTileM + i);
-      return chunk.xrow[(t - c0) / Q][i];
+    auto xrow_of = [&](int u, int i) __attribute__((always_inline)) -> int {
+      if (kCached) return st.input_row(r0 + u * kTileM + i);
+      return chunk.xrow[(u - u0) / Q][i];
     };
-    // x fragments (waves 0-3), edge fragments (all waves), children's cells (pairs)
-    // every load is issued; absent sources read zeros (no merge, no early wait)
-    auto load_tile = [&](int t, u32x4 (&xv)[NBX], Frag4 (&ev)[NBE], int &ecr, u32x2 (&cc)[4],
-                         int (&ce)[4]) {
-      const int row = t * kTileM + i16;
+    // x fragments (waves 0-3), edge fragments, the child cell of the
+    // forget-gate item; absent sources read zeros
+    auto issue = [&](int u, TileOps &t) __attribute__((always_inline)) {
+      const int row = r0 + u * kTileM + i16;
       int xr = -1;
-      if (wave < 4 && row >= r0 && row < r1) xr = xrow_of(t, i16);
+      if (wave < 4 && row < r1) xr = xrow_of(u, i16);
 #pragma unroll
       for (int b = 0; b < NBX; ++b)
-        xv[b] = xin.load4(xr >= 0 ? (uint32_t)((xr * H + wave * KWX + 16 * b + 4 * g4) * 4) : kNoSource);
-      ecr = child(t, e_node, e_slot);
-#pragma unroll
-      for (int b = 0; b < NBE; ++b) {
-        const uint32_t off = ecr >= 0 ? (uint32_t)(ecr * H + ehalf * KWE + 16 * b + 4 * g4) * 8u : kNoSource;
-        ev[b].lo = hs.load2_at(off);
-        ev[b].hi = hs.load2_at(off + 16u);
-      }
-      const int hj = hbase + tid % J;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int cr = tid < D::EPI ? child(t, tid / J, s) : -1;
-        ce[s] = cr >= 0 ? cr * H + hj : -1;
-        cc[s] = cs.load1_at(ce[s] >= 0 ? (uint32_t)ce[s] * 8u : kNoSource);
-      }
-    };
-
-    u32x4 xv[NBX], xn[NBX];
-    Frag4 ev[NBE], evn[NBE];
-    u32x2 cc[4], ccn[4];
-    int ce[4], cen[4];
-    int ecr = -1, ecrn = -1;
-    for (; c0 <= t_hi; c0 += Q * kChunkTiles) {
-    const int c_last = min(t_hi, c0 + Q * (kChunkTiles - 1));
-    if (!kCached) {
-      __syncthreads();                // the previous chunk's structure is no longer read
-      stage_chunk<true, false>(a, chunk, c0, (c_last - c0) / Q + 1, Q, r0, r1);
-      __syncthreads();
-    }
-    load_tile(c0, xv, ev, ecr, cc, ce);
-    for (int t = c0; t <= c_last; t += Q) {
-      const int tn = t + Q;
-      if (tn <= c_last) load_tile(tn, xn, evn, ecrn, ccn, cen);
-      CORTEX_TRACE_POINT(l, 1);
-      if (ecr >= 0) {
+        t.xv[b] = xin.load4(xr >= 0 ? (uint32_t)((xr * H + wave * KWX + 16 * b + 4 * g4) * 4) : kNoSource);
+      t.ecr = child(u, e_node, e_slot);
+      if (t.ecr >= 0) {
 #pragma unroll
         for (int b = 0; b < NBE; ++b) {
-          if (!ev[b].staged_ready(tag)) {
-            const uint32_t e = (uint32_t)(ecr * H + ehalf * KWE + 16 * b + 4 * g4);
-            const uint64_t t0 = wall_clock64();
-            int naps = 0;
-            do {
-              while (hs.load1(e + 3).y != tag && keep_waiting(a.status, t0, a.timeout, naps)) {
+          const uint32_t so = (uint32_t)(t.ecr * H + ek + 16 * b) * 8u;
+          t.ev[b].lo = hs.load2_at(so);
+          t.ev[b].hi = hs.load2_at(so + 16u);
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < NBE; ++b) t.ev[b].lo = t.ev[b].hi = u32x4{0u, 0u, 0u, 0u};
+      }
+      const int cr = (tid < kTileM * ZW && zk >= 3) ? child(u, zi, zk - 3) : -1;
+      t.ce = cr >= 0 ? cr * H + hbase + zj : -1;
+      t.cc = cs.load1_at(t.ce >= 0 ? (uint32_t)t.ce * 8u : kNoSource);
+    };
+    auto all_ready = [&](const TileOps &t) __attribute__((always_inline)) -> bool {
+      bool r = t.ce < 0 || t.cc.y == tag;
+      if (t.ecr >= 0) {
+#pragma unroll
+        for (int b = 0; b < NBE; ++b) r = r && t.ev[b].ready(tag);
+      }
+      return r;
+    };
+
+    auto process = [&](int u, TileOps &t, bool more, TileOps &tn) __attribute__((always_inline)) {
+      CORTEX_TRACE_POINT(l, 1);
+      if (!gave_up && !all_ready(t)) {
+        const uint64_t t0 = wall_clock64();
+        for (;;) {
+          __builtin_amdgcn_s_sleep(1);
+          if (t.ecr >= 0) {
+#pragma unroll
+            for (int b = 0; b < NBE; ++b)
+              if (!t.ev[b].ready(tag)) {
+                const uint32_t so = (uint32_t)(t.ecr * H + ek + 16 * b) * 8u;
+                t.ev[b].lo = hs.load2_at(so);
+                t.ev[b].hi = hs.load2_at(so + 16u);
               }
-              ev[b].lo = hs.load2(e);
-              ev[b].hi = hs.load2(e + 2);
-            } while (!ev[b].staged_ready(tag) && keep_waiting(a.status, t0, a.timeout, naps));
+          }
+          if (t.ce >= 0 && t.cc.y != tag) t.cc = cs.load1_at((uint32_t)t.ce * 8u);
+          const int stv = load_status(a.status);
+          if (all_ready(t)) break;
+          if (stv != 0) {
+            gave_up = 1;
+            break;
+          }
+          if (wall_clock64() - t0 > a.timeout) {
+            raise_status(a.status, CORTEX_ST_BARRIER_TIMEOUT);
+            gave_up = 1;
+            break;
           }
         }
       }
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        if (ce[s] >= 0 && cc[s].y != tag) {
-          const uint64_t t0 = wall_clock64();
-          int naps = 0;
-          do {
-            cc[s] = cs.load1((uint32_t)ce[s]);
-          } while (cc[s].y != tag && keep_waiting(a.status, t0, a.timeout, naps));
-        }
       CORTEX_TRACE_POINT(l, 2);
+      if (more) issue(u + Q, tn);
+      floatx4 xacc0 = {0.f, 0.f, 0.f, 0.f}, xacc1 = {0.f, 0.f, 0.f, 0.f};
       if (wave < 4) {
-        floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
         const float *brow = &W_s[i16 * LDW + wave * KWX + 4 * g4];
 #pragma unroll
         for (int b = 0; b < NBX; ++b) {
           const float4 bv = *(const float4 *)(brow + 16 * b);
-          if (b & 1) acc1 = mfma_k16(as_float4(xv[b]), bv, acc1);
-          else acc0 = mfma_k16(as_float4(xv[b]), bv, acc0);
+          if (b & 1) xacc1 = mfma_k16(as_float4(t.xv[b]), bv, xacc1);
+          else xacc0 = mfma_k16(as_float4(t.xv[b]), bv, xacc0);
         }
-#pragma unroll
-        for (int v = 0; v < 4; ++v) Cx[(wave * 16 + 4 * g4 + v) * 16 + i16] = acc0[v] + acc1[v];
       }
-      {
-        floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-        if (__ballot(ecr >= 0) != 0) {      // skip edge tiles with no child at all (leaves)
-          const float *brow = &W_s[i16 * LDW + H + ehalf * KWE + 4 * g4];
+      floatx4 eacc0 = {0.f, 0.f, 0.f, 0.f}, eacc1 = {0.f, 0.f, 0.f, 0.f};
+      if (__ballot(t.ecr >= 0) != 0) {      // skip edge tiles with no child at all (leaves)
+        const float *brow = &W_s[i16 * LDW + H + ek];
 #pragma unroll
-          for (int b = 0; b < NBE; ++b) {
-            const float4 bv = *(const float4 *)(brow + 16 * b);
-            if (b & 1) acc1 = mfma_k16(ev[b].value(false), bv, acc1);
-            else acc0 = mfma_k16(ev[b].value(false), bv, acc0);
-          }
+        for (int b = 0; b < NBE; ++b) {
+          const float4 bv = *(const float4 *)(brow + 16 * b);
+          if (b & 1) eacc1 = mfma_k16(t.ev[b].value(true), bv, eacc1);
+          else eacc0 = mfma_k16(t.ev[b].value(true), bv, eacc0);
         }
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          Ce[(ehalf * 64 + 16 * em + 4 * g4 + v) * 16 + i16] = acc0[v] + acc1[v];
       }
+      CORTEX_TRACE_WAVE(l);
+      // the next tile's loads complete before this tile's stores
+      __builtin_amdgcn_s_waitcnt(kWaitVmcntZero);
+      if (wave < 4) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) Cx[(wave * 16 + 4 * g4 + v) * 16 + i16] = xacc0[v] + xacc1[v];
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) Ce[(ehalf * 64 + 16 * em + 4 * g4 + v) * 16 + i16] = eacc0[v] + eacc1[v];
       __syncthreads();
       CORTEX_TRACE_POINT(l, 3);
-      if (tid < D::EPI) {
-        const int i = tid / J, j = tid % J;
-        const int row = t * kTileM + i, hj = hbase + j;
-        if (row >= r0 && row < r1) {
-          float z[4];       // gate slots (i, o, u, f): x part + bias
+      // ---- gate items: i, o, u of each (row, unit), and f_k * c_k of each
+      //      child slot, one per thread ----
+      if (tid < kTileM * ZW) {
+        const int gs = zk < 3 ? zk : 3, m = gs * J + zj;
+        float sum = bias_s[m] + Cx[(0 * 16 + zi) * 16 + m] + Cx[(1 * 16 + zi) * 16 + m] +
+                    Cx[(2 * 16 + zi) * 16 + m] + Cx[(3 * 16 + zi) * 16 + m];
+        float zv;
+        if (zk < 3) {
 #pragma unroll
-          for (int gs = 0; gs < 4; ++gs) {
-            const int m = gs * J + j;
-            z[gs] = bias_s[m] + Cx[(0 * 16 + i) * 16 + m] + Cx[(1 * 16 + i) * 16 + m] +
-                    Cx[(2 * 16 + i) * 16 + m] + Cx[(3 * 16 + i) * 16 + m];
-          }
-          float hs_i = 0.f, hs_o = 0.f, hs_u = 0.f, cpart = 0.f;
-#pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            if (ce[s] >= 0) {
-              const float *e0 = &Ce[(0 * 64 + i * 4 + s) * 16];
-              const float *e1 = &Ce[(1 * 64 + i * 4 + s) * 16];
-              hs_i += e0[0 * J + j] + e1[0 * J + j];
-              hs_o += e0[1 * J + j] + e1[1 * J + j];
-              hs_u += e0[2 * J + j] + e1[2 * J + j];
-              cpart += sigmoidf(z[3] + e0[3 * J + j] + e1[3 * J + j]) * as_float(cc[s].x);
-            }
-          }
-          const float cn = sigmoidf(z[0] + hs_i) * tanh_f(z[2] + hs_u) + cpart;
-          const float hv = sigmoidf(z[1] + hs_o) * tanh_f(cn);
-          const uint32_t el = (uint32_t)(row * H + hj);
+          for (int s = 0; s < 4; ++s)
+            sum += Ce[(0 * 64 + zi * 4 + s) * 16 + m] + Ce[(1 * 64 + zi * 4 + s) * 16 + m];
+          zv = zk == 2 ? tanh_f(sum) : sigmoidf(sum);
+        } else {
+          const int s = zk - 3;
+          sum += Ce[(0 * 64 + zi * 4 + s) * 16 + m] + Ce[(1 * 64 + zi * 4 + s) * 16 + m];
+          zv = t.ce >= 0 ? sigmoidf(sum) * as_float(t.cc.x) : 0.f;
+        }
+        Z_s[tid] = zv;
+      }
+      __syncthreads();
+      if (tid < kTileM * J) {
+        const int i = tid / J, j = tid % J, row = r0 + u * kTileM + i;
+        if (row < r1) {
+          const float *z = &Z_s[i * ZW];
+          const float cn = z[j] * z[2 * J + j] + ((z[3 * J + j] + z[4 * J + j]) + (z[5 * J + j] + z[6 * J + j]));
+          const float hv = z[J + j] * tanh_f(cn);
+          const uint32_t el = (uint32_t)(row * H + hbase + j);
           cs.store1(el, cn, tag);
           hs.store1(el, hv, tag);
           a.c[el] = cn;
@@ -759,19 +977,31 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
       }
       __syncthreads();
       CORTEX_TRACE_POINT(l, 4);
-      if (tn <= c_last) {
-#pragma unroll
-        for (int b = 0; b < NBX; ++b) xv[b] = xn[b];
-#pragma unroll
-        for (int b = 0; b < NBE; ++b) ev[b] = evn[b];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) cc[s] = ccn[s], ce[s] = cen[s];
-        ecr = ecrn;
+    };
+
+    TileOps ta, tb;
+    for (; u0 < ntile; u0 += Q * kChunkTiles) {
+      const int u_last = min(ntile - 1, u0 + Q * (kChunkTiles - 1));
+      if (!kCached) {
+        __syncthreads();
+        stage_chunk(a, chunk, u0, (u_last - u0) / Q + 1, Q, r0, r1);
+        __syncthreads();
+      }
+      issue(u0, ta);
+      CORTEX_TRACE_POINT(l, 6);
+      for (int u = u0;;) {
+        bool more = u + Q <= u_last;
+        process(u, ta, more, tb);
+        u += Q;
+        if (!more) break;
+        more = u + Q <= u_last;
+        process(u, tb, more, ta);
+        u += Q;
+        if (!more) break;
       }
     }
-    }
     CORTEX_TRACE_POINT(l, 5);
-    if (load_status(a.status) != 0) return;
+    if (__syncthreads_or(gave_up)) return;
   }
   CORTEX_TRACE_KERNEL(3);
 }
@@ -922,28 +1152,35 @@ struct Instance {
 constexpr size_t kStructCacheBudget = 40 * 1024;    // bytes of LDS for the cached linearization
 
 // ints of the structure cache: offsets (<= N+1), child rows, input rows, node ids
+// (child-sum: offsets, child rows, input rows; the slice kernels: offsets,
+// source codes, input rows of the leaf-input cells)
 static size_t cache_ints(int cell, int32_t N, int32_t K) {
-  size_t n = (size_t)N + 1 + (size_t)N * K;
-  if (cell == CORTEX_TREE_RNN || cell == CORTEX_NARY_TREELSTM || cell == CORTEX_CHILDSUM_TREELSTM) n += N;
-  if (cell == CELL_DAG) n += N;
-  return n;
+  if (cell == CORTEX_CHILDSUM_TREELSTM) return (size_t)N + 1 + (size_t)N * K + N;
+  const size_t segs = cell == CELL_DAG ? 3 : 2;
+  return (size_t)N + 1 + (size_t)N * segs + (cell == CELL_DAG ? 0 : N);
 }
 
-template <int CELL, int H>
+template <int CELL, int H, int J>
 static void pick_slice(bool cached, Instance &out) {
-  out.J = Cfg<CELL, H>::J;
+  out.J = J;
   out.threads = kFwdThreads;
   if constexpr (CELL == CORTEX_CHILDSUM_TREELSTM)
     out.fn = cached ? childsum_forward_kernel<H, true> : childsum_forward_kernel<H, false>;
   else
-    out.fn = cached ? slice_forward_kernel<CELL, H, true> : slice_forward_kernel<CELL, H, false>;
+    out.fn = cached ? slice_forward_kernel<CELL, H, J, true> : slice_forward_kernel<CELL, H, J, false>;
 }
 
+// units per slice: the knob's value where an instance exists, else the default
 static bool pick(int cell, int H, bool cached, Instance &out) {
-#define CORTEX_CASE(CELLID, HH)          \
-  if (cell == CELLID && H == HH) {        \
-    pick_slice<CELLID, HH>(cached, out);  \
-    return true;                          \
+  const int64_t units = knob(CORTEX_KNOB_FWD_SLICE_UNITS);
+  if (cell == CORTEX_NARY_TREELSTM && H == 256 && units == 2) {
+    pick_slice<CORTEX_NARY_TREELSTM, 256, 2>(cached, out);
+    return true;
+  }
+#define CORTEX_CASE(CELLID, HH)                                      \
+  if (cell == CELLID && H == HH) {                                    \
+    pick_slice<CELLID, HH, Cell<CELLID, HH>::J>(cached, out);         \
+    return true;                                                      \
   }
   CORTEX_CASE(CORTEX_TREE_RNN, 64)
   CORTEX_CASE(CORTEX_TREE_RNN, 256)
@@ -963,8 +1200,8 @@ static bool pick(int cell, int H, bool cached, Instance &out) {
   return false;
 }
 
-// Workspace of a forward launch: barrier words, the trace area, then the tagged
-// staging of h (and of c for the LSTM cells), 8 bytes per element.
+// Workspace of a forward launch: barrier words, the trace area, then the
+// tagged staging of h (and of c for the LSTM cells), 8 bytes per element.
 static size_t staging_bytes(int32_t N, int32_t H) { return align_up((size_t)N * H * 8, 256); }
 static size_t staging_offset() { return align_up(kSyncBytes + kTraceBytes, 256); }
 size_t trace_offset() { return kSyncBytes; }
@@ -986,14 +1223,15 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
                           void *stream) {
   // state and staging arrays are addressed with 32-bit byte offsets
   const uint64_t state_bytes = (uint64_t)lin->num_nodes * H * (cell == CORTEX_MVRNN ? H : 1) * 8;
-  if (state_bytes > 0x7fffffffull) return CORTEX_E_TOO_LARGE;
+  const uint64_t table_bytes = (uint64_t)(a.x_rows > 0 ? a.x_rows : 0) * H * (cell == CORTEX_MVRNN ? H : 1) * 4;
+  if (state_bytes > 0x7fffffffull || table_bytes > 0x7fffffffull) return CORTEX_E_TOO_LARGE;
   if (ws_bytes < cortex_forward_workspace_bytes(cell == CELL_DAG ? -1 : cell, lin->num_nodes, H))
     return CORTEX_E_WORKSPACE;
   size_t dyn = 0;
   bool cached = false;
   if (cell != CORTEX_MVRNN) {
     dyn = cache_ints(cell, lin->num_nodes, lin->max_arity) * sizeof(int);
-    cached = dyn <= kStructCacheBudget;
+    cached = dyn <= kStructCacheBudget && (cell == CORTEX_CHILDSUM_TREELSTM || lin->num_nodes <= kMaxCachedRows);
     if (!cached) dyn = 0;
   }
   Instance inst;

@@ -22,6 +22,7 @@ def _gpu():
     yield
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, 0)
     C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, 0)
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
 
 
 def run(wl, groups=0):
@@ -68,6 +69,41 @@ def test_small_ragged(name, seed, groups):
     announce("small %s seed %d groups %d N=%d" % (name, seed, groups, wl.N))
     dw = run(wl, groups)
     compare_states(dw.states_by_node(), O.forward_workload(wl), name)
+
+
+# Batches whose linearization does not fit the LDS structure cache: the
+# kernels then stage each chunk of tiles' structure from global memory.
+LARGE = {
+    "tree_rnn_h256": lambda: I.tree_rnn_workload(31, n_leaves=1800, H=256),
+    "nary_h256": lambda: I.nary_treelstm_workload(32, batch=120, H=256),
+    "childsum_h256": lambda: I.childsum_treelstm_workload(33, batch=110, H=256),
+}
+
+
+@pytest.mark.parametrize("name", sorted(LARGE))
+def test_uncached_structure(name):
+    wl = LARGE[name]()
+    assert wl.N > 2600, "must exceed the structure cache"
+    announce("uncached structure %s N=%d" % (name, wl.N))
+    dw = run(wl)
+    compare_states(dw.states_by_node(), O.forward_workload(wl), name)
+
+
+@pytest.mark.parametrize("groups", [0, 1])
+def test_slice_units_change_only_the_schedule(groups):
+    """Two hidden units per slice instead of four: the same sums in the same
+    order, so the states are bitwise identical."""
+    wl = cached_workload(1, groups)
+    announce("slice units 2 vs default, seed %d, groups %d" % (groups, groups))
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
+    ref = run(wl).states_by_node()
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 2)
+    dw = run(wl, groups)
+    assert C.cortex_last_grid(1) == 128 * (groups if groups else 2)
+    got = dw.states_by_node()
+    for key in ref:
+        assert np.array_equal(ref[key], got[key]), key
+    compare_states(got, cached_oracle(1, groups), wl.name)
 
 
 def test_single_leaf_trees():
