@@ -1,0 +1,162 @@
+"""Per-level timeline of one forward launch (trace build of the library).
+
+    python -m paper_2011_01383_amd.timeline --workload 1 [--json out.json]
+
+Loads ``libcortex_trace.so`` (built by ``python -m paper_2011_01383_amd.build
+--trace``, i.e. with -DCORTEX_TRACE), runs a few warm passes of one workload,
+clears the timeline, runs one more pass and reads the stamps the forward
+kernel left in its workspace: every workgroup (the first 256) stamps the
+100 MHz wall clock at fixed points of every level.  The report gives, per
+level, when the first workgroup entered it and when the last one left it
+(both relative to the earliest kernel entry), the critical-path time of the
+level (its last exit minus the previous level's last exit), and the longest
+operand wait, contraction and epilogue of any workgroup's last tile there.
+
+Stamp layout (uint64 ``trace[block][64][16]`` at byte offset
+``SYNC_BYTES`` of the forward workspace): row ``l`` < 63 is level ``l``
+(deeper levels share row 62); slot 0 level entry, 1 tile wait begins,
+2 operands ready, 3 partial sums reduced, 4 tile written, 5 level exit,
+6 first operands requested, 8 + w wave w finished its products.  Row 63
+holds kernel-wide stamps: 0 entry, 1 weights resident, 2 structure ready,
+3 exit.  Only the slice kernels (TreeRNN, N-ary and child-sum TreeLSTM,
+DAG-RNN) stamp.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+TRACE_LIB = os.path.join(HERE, "libcortex_trace.so")
+
+SYNC_BYTES = 128 + 4 * 4096 * 5          # barrier words ahead of the timeline
+TRACE_BLOCKS, TRACE_LEVELS, TRACE_SLOTS = 256, 64, 16
+TICKS_PER_US = 100.0
+
+
+def read_timeline(dw):
+    """The timeline of the last forward launch of ``dw`` as uint64 [256, 64, 16]."""
+    import torch
+    torch.cuda.synchronize()
+    n = TRACE_BLOCKS * TRACE_LEVELS * TRACE_SLOTS * 8
+    raw = dw.ws_fwd[SYNC_BYTES:SYNC_BYTES + n].cpu().numpy()
+    return raw.view(np.uint64).reshape(TRACE_BLOCKS, TRACE_LEVELS, TRACE_SLOTS)
+
+
+def summarize(tr, num_levels, grid):
+    """Per-level breakdown in microseconds from the raw stamps."""
+    blocks = min(grid, TRACE_BLOCKS)
+    tr = tr[:blocks].astype(np.int64)
+    kern = tr[:, TRACE_LEVELS - 1, :]
+    t0 = kern[:, 0][kern[:, 0] > 0].min()
+    us = lambda t: float(t - t0) / TICKS_PER_US
+
+    def span(a, b):
+        """Largest b - a over blocks that stamped both."""
+        m = (a > 0) & (b > 0)
+        return float((b[m] - a[m]).max()) / TICKS_PER_US if m.any() else None
+
+    out = {"kernel": {
+        "entry_last_us": us(kern[:, 0][kern[:, 0] > 0].max()),
+        "weights_resident_us": us(kern[:, 1].max()),
+        "structure_ready_us": us(kern[:, 2].max()),
+        "exit_us": us(kern[:, 3].max()),
+    }, "levels": []}
+    prev_exit = kern[:, 2].max()
+    for l in range(min(num_levels, TRACE_LEVELS - 2)):
+        row = tr[:, l, :]
+        entered = row[:, 0][row[:, 0] > 0]
+        exited = row[:, 5][row[:, 5] > 0]
+        if entered.size == 0 or exited.size == 0:
+            continue
+        last_exit = exited.max()
+        out["levels"].append({
+            "level": l,
+            "enter_first_us": us(entered.min()),
+            "exit_last_us": us(last_exit),
+            "critical_us": float(last_exit - prev_exit) / TICKS_PER_US,
+            "wait_max_us": span(row[:, 1], row[:, 2]),
+            "contract_max_us": span(row[:, 2], row[:, 3]),
+            "epilogue_max_us": span(row[:, 3], row[:, 4]),
+        })
+        prev_exit = last_exit
+    return out
+
+
+def as_markdown(rep, title):
+    k = rep["kernel"]
+    lines = ["# Forward timeline: %s" % title, "",
+             "Kernel: last entry %.2f us, weights resident %.2f us, structure ready %.2f us, exit %.2f us "
+             "(all from the first workgroup's entry)." % (k["entry_last_us"], k["weights_resident_us"],
+                                                          k["structure_ready_us"], k["exit_us"]), "",
+             "| level | first entry (us) | last exit (us) | critical (us) | max wait (us) | max contraction (us) | max epilogue (us) |",
+             "|---|---|---|---|---|---|---|"]
+    f = lambda v: "-" if v is None else "%.2f" % v
+    for r in rep["levels"]:
+        lines.append("| %d | %s | %s | %s | %s | %s | %s |" % (
+            r["level"], f(r["enter_first_us"]), f(r["exit_last_us"]), f(r["critical_us"]),
+            f(r["wait_max_us"]), f(r["contract_max_us"]), f(r["epilogue_max_us"])))
+    return "\n".join(lines)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--warm", type=int, default=5)
+    ap.add_argument("--json", default=None)
+    ap.add_argument("--markdown", default=None)
+    args = ap.parse_args()
+
+    import torch
+    from . import cortex as C
+    from . import inputs as I
+    from .runner import DeviceWorkload
+
+    if not os.path.exists(TRACE_LIB):
+        raise RuntimeError("%s is not built; run python -m paper_2011_01383_amd.build --trace" % TRACE_LIB)
+    C.load(TRACE_LIB)
+    torch.cuda.set_device(0)
+    wl = I.make_workload(args.workload)
+    dw = DeviceWorkload(wl)
+    for _ in range(args.warm):
+        dw.step()
+    torch.cuda.synchronize()
+    n = TRACE_BLOCKS * TRACE_LEVELS * TRACE_SLOTS * 8
+    dw.ws_fwd[SYNC_BYTES:SYNC_BYTES + n].zero_()
+    dw.ws_lin.zero_()                     # a zeroed workspace is always a valid start
+    dw.linearize()
+    torch.cuda.synchronize()
+    lin_stamps = dw.ws_lin[:56].cpu().numpy().view(np.uint64).astype(np.int64)
+    dw.forward()
+    st = dw.status_code()
+    if st != 0:
+        raise RuntimeError("device status %d" % st)
+    L = int(dw.lin_host()["num_levels"])
+    rep = summarize(read_timeline(dw), L, C.cortex_last_grid(1))
+    rep["workload"] = wl.name
+    rep["grid"] = C.cortex_last_grid(1)
+    rep["num_levels"] = L
+    if C.cortex_last_grid(0) == 1 and lin_stamps[0] > 0:
+        # single-workgroup linearizer: entry, children loaded, heights done,
+        # level counts, sort done, outputs written, offsets written
+        rep["linearize_phases_us"] = [float(t - lin_stamps[0]) / TICKS_PER_US for t in lin_stamps]
+    md = as_markdown(rep, "%s (grid %d, %d levels)" % (wl.name, rep["grid"], L))
+    if "linearize_phases_us" in rep:
+        md += ("\n\nLinearizer (one workgroup), from its entry: children loaded %.2f, heights %.2f, "
+               "level counts %.2f, sort %.2f, outputs %.2f, offsets %.2f us." % tuple(rep["linearize_phases_us"][1:]))
+    print(md)
+    sys.stdout.flush()
+    if args.json:
+        with open(args.json, "w") as f:
+            json.dump(rep, f, indent=1)
+    if args.markdown:
+        with open(args.markdown, "w") as f:
+            f.write(md + "\n")
+
+
+if __name__ == "__main__":
+    main()
