@@ -768,6 +768,367 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// DAG-RNN at H = 256 with four hidden slices of 64 units:
+//   h(v) = tanh(W x(v) + U_0 h(slot 0) + U_1 h(slot 1) + b).
+// Fewer, wider slices than the kernel above: every slice re-reads the child
+// rows it contracts, so four slices move a quarter of the operand bytes of
+// sixteen.  Each wave keeps its 64 recurrent columns x 64 units of U_0 / U_1
+// in registers for the whole launch and the input weights W sit in LDS.  Per
+// 16-row tile, wave w contracts input columns [32w, 32w+32) first — they do
+// not depend on any child — and only then waits for the children and
+// contracts recurrent columns [64w, 64w+64) of [h(slot 0) | h(slot 1)]; the
+// eight partial sums meet in LDS.  When the grid is a multiple of 32, the
+// four slices of node group q are workgroups 32m + r + 8s (r = q mod 8,
+// m = q div 8, s = 0..3), which round-robin dispatch places on one XCD, so
+// the input row of a node is fetched into one L2 once.
+//
+// At entry each workgroup lists its own tiles of every level (the tiles u of
+// level l with u = q - l mod Q) with their operand sources in LDS, so the
+// level loop never goes back to the linearization in memory, and the next
+// tile's operands, in the same level or the next, are requested while the
+// current tile is contracted.  A group whose list does not fit the LDS
+// budget walks the levels instead, staging each chunk of tiles' sources.
+// ---------------------------------------------------------------------------
+constexpr int kDagH = 256, kDagJ = 64, kDagS = kDagH / kDagJ;
+constexpr int kDagTileInts = 4 + kTileM * 3;        // level, level start, first row, level end, codes[16][3]
+constexpr int kDagTileCap = 240;                    // tiles per workgroup list (dynamic LDS)
+constexpr size_t kDagListBytes = (size_t)kDagTileCap * kDagTileInts * sizeof(int);
+
+// Exclusive prefix sum of one value per thread over the workgroup; wsum
+// holds kFwdWaves + 1 ints of LDS.  Returns the exclusive sum, *total the sum.
+__device__ __forceinline__ int block_excl_scan(int v, int *wsum, int *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int w = 0; w < kFwdWaves; ++w) {
+      const int t = wsum[w];
+      wsum[w] = run;
+      run += t;
+    }
+    wsum[kFwdWaves] = run;
+  }
+  __syncthreads();
+  const int ex = wsum[wave] + x - v;
+  *total = wsum[kFwdWaves];
+  __syncthreads();
+  return ex;
+}
+
+__global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
+  constexpr int H = kDagH, J = kDagJ, NT = J / 16;
+  constexpr int KX = H / kFwdWaves, NBX = KX / 16;          // input columns per wave, 16-blocks
+  constexpr int KR = 2 * H / kFwdWaves, NBR = KR / 16;      // recurrent columns per wave, 16-blocks
+  constexpr int LDX = H + 4;                                // W row stride in LDS
+  constexpr int LDC = J + 4;                                // partial-sum row stride
+  constexpr int EPI = kTileM * J / kFwdThreads;             // outputs per thread per tile
+  constexpr int TI = kDagTileInts;
+  constexpr int R = 4;                                      // listed rows loaded per thread per round
+  static_assert(NBX * 16 == KX && NBR * 16 == KR && EPI * kFwdThreads == kTileM * J, "tiling");
+  static_assert(KR == 64 && H % KR == 0, "a wave's recurrent columns lie in one child slot");
+
+  __shared__ __attribute__((aligned(16))) float Wx_s[J * LDX];
+  __shared__ __attribute__((aligned(16))) float C_s[kFwdWaves * kTileM * LDC];
+  __shared__ float bias_s[J];
+  __shared__ ChunkSrc chunk;
+  __shared__ int wsum[kFwdWaves + 1];
+  extern __shared__ int list[];               // [kDagTileCap][kDagTileInts]
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int bid = blockIdx.x;
+  const bool xcd_map = (gridDim.x & 31) == 0;
+  const int slice = xcd_map ? ((bid >> 3) & 3) : bid % kDagS;
+  const int group = xcd_map ? ((bid & 7) + 8 * (bid >> 5)) : bid / kDagS;
+  const int Q = a.Q;
+  const int hbase = slice * J;
+  const int N = a.N;
+  const uint32_t tag = a.tag;
+  const TagBuf hs(a.hs, (uint32_t)N * H * 8);
+  const InBuf xin(a.x, (uint32_t)N * H * 4);
+  const int rslot = wave >> 2;                 // child slot of this wave's recurrent columns
+  const int rcol = KR * (wave & 3);            // their first column within that child's h
+  const int xcol = KX * wave;                  // this wave's first input column
+
+  CORTEX_TRACE_KERNEL(0);
+  // the status, the level count and the weights are requested together: one
+  // memory round trip for all of them
+  const int status0 = load_status(a.status);
+  const int L = *a.num_levels;
+  // recurrent weights: wr[b][nt] = U_rslot[hbase + 16 nt + i16][rcol + 16 b + 4 g4 .. +3]
+  float4 wr[NBR][NT];
+#pragma unroll
+  for (int b = 0; b < NBR; ++b)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      wr[b][nt] = *(const float4 *)(a.U + ((size_t)rslot * H + hbase + 16 * nt + i16) * H + rcol + 16 * b + 4 * g4);
+  {
+    constexpr int ITEMS = J * H / 4, PER = ITEMS / kFwdThreads;
+    float4 v[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      v[k] = *(const float4 *)(a.W + (size_t)(hbase + idx / (H / 4)) * H + 4 * (idx % (H / 4)));
+    }
+    if (tid < J) bias_s[tid] = a.b[hbase + tid];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      *(float4 *)&Wx_s[(idx / (H / 4)) * LDX + 4 * (idx % (H / 4))] = v[k];
+    }
+  }
+  if (status0 != 0) return;
+  if (L < 1 || L > N) {
+    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+    return;
+  }
+  CORTEX_TRACE_KERNEL(1);
+
+  // ---- this group's tiles of every level, one level per thread per round ----
+  int total = 0, bad = 0;
+  for (int lb = 0; lb < L; lb += kFwdThreads) {
+    const int l = lb + tid;
+    int cnt = 0, r0 = 0, r1 = 0, uf = 0;
+    if (l < L) {
+      r0 = a.level_offsets[l];
+      r1 = a.level_offsets[l + 1];
+      const bool ok = r0 >= 0 && r1 >= r0 && r1 <= N && (l != 0 || r0 == 0) && (l != L - 1 || r1 == N);
+      if (!ok) bad = 1;
+      const int ntile = ok ? (r1 - r0 + kTileM - 1) / kTileM : 0;
+      uf = ((group - l) % Q + Q) % Q;
+      cnt = uf < ntile ? (ntile - 1 - uf) / Q + 1 : 0;
+    }
+    int round_total;
+    const int pos = total + block_excl_scan(cnt, wsum, &round_total);
+    for (int j = 0; j < cnt && pos + j < kDagTileCap; ++j) {
+      int *t = &list[(pos + j) * TI];
+      t[0] = l;
+      t[1] = r0;
+      t[2] = r0 + kTileM * (uf + j * Q);
+      t[3] = r1;
+    }
+    total += round_total;
+  }
+  // (each level's end is the next level's start, so the levels tile [0, N))
+  if (__syncthreads_or(bad)) {
+    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+    return;
+  }
+  const bool listed = total <= kDagTileCap;
+  if (listed) {
+    // operand sources of every listed row: code 0 = -2 - node id (its input
+    // row), codes 1 and 2 = child rows, which must lie below the row's level
+    for (int base = 0; base < total * kTileM; base += R * kFwdThreads) {
+      int v[R], c[R][2];
+#pragma unroll
+      for (int k = 0; k < R; ++k) {
+        const int idx = base + k * kFwdThreads + tid;
+        v[k] = -1;
+        c[k][0] = c[k][1] = -1;
+        if (idx < total * kTileM) {
+          const int *t = &list[(idx / kTileM) * TI];
+          const int row = t[2] + idx % kTileM;
+          if (row < t[3]) {
+            v[k] = a.level_nodes[row];
+            c[k][0] = a.child_rows[(size_t)row * 2];
+            c[k][1] = a.child_rows[(size_t)row * 2 + 1];
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < R; ++k) {
+        const int idx = base + k * kFwdThreads + tid;
+        if (idx < total * kTileM) {
+          int *t = &list[(idx / kTileM) * TI];
+          const int row = t[2] + idx % kTileM, lstart = t[1];
+          int *cd = &t[4 + (idx % kTileM) * 3];
+          if (row < t[3] && (v[k] < 0 || v[k] >= N)) bad = 1;
+          cd[0] = (v[k] >= 0 && v[k] < N) ? -2 - v[k] : -1;
+#pragma unroll
+          for (int s = 0; s < 2; ++s) {
+            int ch = c[k][s];
+            if (ch < -1 || ch >= lstart) {
+              bad = 1;
+              ch = -1;
+            }
+            cd[1 + s] = ch;
+          }
+        }
+      }
+    }
+    if (__syncthreads_or(bad)) {
+      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      return;
+    }
+  }
+  CORTEX_TRACE_KERNEL(2);
+  int gave_up = 0;
+
+  struct Ops {
+    u32x4 xv[NBX];     // input fragments (plain)
+    Frag hv[NBR];      // child-state fragments (staged pairs)
+    int cr;            // child row of this lane's tile row, -1 = none
+  };
+  // Operands of the tile whose rows start at rowbase (rows < rend live) and
+  // whose sources are cd[16][3].
+  auto issue = [&](const int *cd, int rowbase, int rend, Ops &t) __attribute__((always_inline)) {
+    int xc = -1, cr = -1;
+    if (rowbase + i16 < rend) {
+      xc = cd[i16 * 3];
+      cr = cd[i16 * 3 + 1 + rslot];
+    }
+#pragma unroll
+    for (int b = 0; b < NBX; ++b)
+      t.xv[b] = xin.load4(xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 16 * b + 4 * g4) * 4) : kNoSource);
+    t.cr = cr;
+#pragma unroll
+    for (int b = 0; b < NBR; ++b) {
+      const uint32_t so = cr >= 0 ? (uint32_t)(cr * H + rcol + 16 * b + 4 * g4) * 8u : kNoSource;
+      t.hv[b].lo = hs.load2_at(so);
+      t.hv[b].hi = hs.load2_at(so + 16u);
+    }
+  };
+  auto ready = [&](const Ops &t) __attribute__((always_inline)) -> bool {
+    bool r = true;
+#pragma unroll
+    for (int b = 0; b < NBR; ++b) r = r && t.hv[b].ready(tag);
+    return t.cr < 0 || r;
+  };
+  // One tile: input part, wait, request the next tile's operands (ncd !=
+  // nullptr), recurrent part, epilogue.  Returns true when the kernel must stop.
+  auto process = [&](int l, int rowbase, int rend, Ops &t, const int *ncd, int nrow, int nrend,
+                     Ops &tn) __attribute__((always_inline)) -> bool {
+    (void)l;
+    floatx4 acc[2][NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[0][nt] = acc[1][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const float *bx = &Wx_s[i16 * LDX + xcol + 4 * g4];
+#pragma unroll
+    for (int b = 0; b < NBX; ++b) {
+      const float4 av = as_float4(t.xv[b]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        acc[b & 1][nt] = mfma_k16(av, *(const float4 *)(bx + nt * 16 * LDX + 16 * b), acc[b & 1][nt]);
+    }
+    CORTEX_TRACE_POINT(l, 1);
+    if (!gave_up && !ready(t)) {
+      const uint64_t t0 = wall_clock64();
+      for (;;) {
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int b = 0; b < NBR; ++b) {
+          if (!t.hv[b].ready(tag)) {
+            const uint32_t so = (uint32_t)(t.cr * H + rcol + 16 * b + 4 * g4) * 8u;
+            t.hv[b].lo = hs.load2_at(so);
+            t.hv[b].hi = hs.load2_at(so + 16u);
+          }
+        }
+        const int stv = load_status(a.status);
+        if (ready(t)) break;
+        if (stv != 0) {
+          gave_up = 1;
+          break;
+        }
+        if (wall_clock64() - t0 > a.timeout) {
+          raise_status(a.status, CORTEX_ST_BARRIER_TIMEOUT);
+          gave_up = 1;
+          break;
+        }
+      }
+    }
+    CORTEX_TRACE_POINT(l, 2);
+    if (ncd) issue(ncd, nrow, nrend, tn);      // in flight during the recurrent part
+#pragma unroll
+    for (int b = 0; b < NBR; ++b) {
+      const float4 av = t.hv[b].value(true);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[b & 1][nt] = mfma_k16(av, wr[b][nt], acc[b & 1][nt]);
+    }
+    CORTEX_TRACE_WAVE(l);
+    // the next tile's loads stay in flight through this tile's epilogue
+    // (vector memory operations retire in order, so its first use waits
+    // for them alone)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        C_s[(wave * kTileM + 4 * g4 + v) * LDC + nt * 16 + i16] = acc[0][nt][v] + acc[1][nt][v];
+    __syncthreads();
+    CORTEX_TRACE_POINT(l, 3);
+#pragma unroll
+    for (int e = 0; e < EPI; ++e) {
+      const int p = tid + e * kFwdThreads, i = p / J, j = p % J;
+      const int row = rowbase + i;
+      float sum = bias_s[j];
+#pragma unroll
+      for (int w = 0; w < kFwdWaves; ++w) sum += C_s[(w * kTileM + i) * LDC + j];
+      if (row < rend) {
+        const uint32_t el = (uint32_t)(row * H + hbase + j);
+        const float hv = tanh_f(sum);
+        hs.store1(el, hv, tag);
+        a.h[el] = hv;
+      }
+    }
+    CORTEX_TRACE_POINT(l, 4);
+    return __syncthreads_or(gave_up) != 0;
+  };
+
+  Ops ta, tb;
+  if (listed) {
+    // one flat pass over this group's tiles, level after level
+    auto tile = [&](int e) __attribute__((always_inline)) -> const int * { return &list[e * TI]; };
+    if (total > 0) issue(tile(0) + 4, tile(0)[2], tile(0)[3], ta);
+    for (int e = 0; e < total;) {
+#pragma unroll
+      for (int ph = 0; ph < 2; ++ph) {
+        const int *t = tile(e);
+        const bool more = e + 1 < total;
+        const int *tn = more ? tile(e + 1) : nullptr;
+        if (e == 0 || tile(e - 1)[0] != t[0]) CORTEX_TRACE_POINT(t[0], 0);
+        const bool stop = process(t[0], t[2], t[3], ph ? tb : ta, more ? tn + 4 : nullptr, more ? tn[2] : 0,
+                                  more ? tn[3] : 0, ph ? ta : tb);
+        if (!more || tn[0] != t[0]) CORTEX_TRACE_POINT(t[0], 5);
+        if (stop) return;
+        if (++e >= total) break;
+      }
+    }
+  } else {
+    // the list does not fit: walk the levels, staging each chunk of tiles' sources
+    const int *off = a.level_offsets;
+    for (int l = 0; l < L; ++l) {
+      CORTEX_TRACE_POINT(l, 0);
+      const int r0 = off[l], r1 = off[l + 1];
+      const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
+      for (int u0 = ((group - l) % Q + Q) % Q; u0 < ntile; u0 += Q * kChunkTiles) {
+        const int u_last = min(ntile - 1, u0 + Q * (kChunkTiles - 1));
+        __syncthreads();                // the previous chunk's codes are no longer read
+        stage_chunk_codes<CELL_DAG>(a, chunk, u0, (u_last - u0) / Q + 1, Q, r0, r1, 0);
+        __syncthreads();
+        issue(&chunk.code[0][0][0], r0 + u0 * kTileM, r1, ta);
+        for (int u = u0, k = 0;; ++k) {
+          const bool more = u + Q <= u_last;
+          const int *ncd = more ? &chunk.code[k + 1][0][0] : nullptr;
+          const bool stop = process(l, r0 + u * kTileM, r1, (k & 1) ? tb : ta, ncd, r0 + (u + Q) * kTileM, r1,
+                                    (k & 1) ? ta : tb);
+          if (stop) return;
+          u += Q;
+          if (!more) break;
+        }
+      }
+      CORTEX_TRACE_POINT(l, 5);
+    }
+  }
+  CORTEX_TRACE_KERNEL(3);
+}
+
+// ---------------------------------------------------------------------------
 // Child-sum TreeLSTM.  Per tile of 16 nodes: the node part x W^T (k split
 // over waves 0-3) and the edge part h_k U^T for the 16 x 4 child slots (edge
 // tile m = wave & 3, k half = wave >> 2).  The gates are then
@@ -1147,6 +1508,7 @@ struct Instance {
   KernelFn fn;
   int J;
   int threads;
+  size_t lds = SIZE_MAX;        // dynamic LDS the kernel sizes itself (SIZE_MAX: the structure cache)
 };
 
 constexpr size_t kStructCacheBudget = 40 * 1024;    // bytes of LDS for the cached linearization
@@ -1175,6 +1537,13 @@ static bool pick(int cell, int H, bool cached, Instance &out) {
   const int64_t units = knob(CORTEX_KNOB_FWD_SLICE_UNITS);
   if (cell == CORTEX_NARY_TREELSTM && H == 256 && units == 2) {
     pick_slice<CORTEX_NARY_TREELSTM, 256, 2>(cached, out);
+    return true;
+  }
+  if (cell == CELL_DAG && H == kDagH && units != 16) {    // 16: the narrow-slice kernel
+    out.fn = dag_slice64_kernel;
+    out.J = kDagJ;
+    out.threads = kFwdThreads;
+    out.lds = kDagListBytes;
     return true;
   }
 #define CORTEX_CASE(CELLID, HH)                                      \
@@ -1236,6 +1605,7 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   }
   Instance inst;
   if (!pick(cell, H, cached, inst)) return CORTEX_E_INVAL;
+  if (inst.lds != SIZE_MAX) dyn = inst.lds;
   const int per_cu = cached_occupancy((const void *)inst.fn, inst.threads, dyn);
   const int cus = num_cus();
   if (per_cu <= 0 || cus <= 0) return CORTEX_E_HIP;

@@ -109,6 +109,7 @@ def main():
     ap.add_argument("--warm", type=int, default=5)
     ap.add_argument("--json", default=None)
     ap.add_argument("--markdown", default=None)
+    ap.add_argument("--npy", default=None, help="also save the raw stamps, uint64 [256, 64, 16]")
     args = ap.parse_args()
 
     import torch
@@ -136,7 +137,10 @@ def main():
     if st != 0:
         raise RuntimeError("device status %d" % st)
     L = int(dw.lin_host()["num_levels"])
-    rep = summarize(read_timeline(dw), L, C.cortex_last_grid(1))
+    raw = read_timeline(dw)
+    if args.npy:
+        np.save(args.npy, raw)
+    rep = summarize(raw, L, C.cortex_last_grid(1))
     rep["workload"] = wl.name
     rep["grid"] = C.cortex_last_grid(1)
     rep["num_levels"] = L
