@@ -27,6 +27,7 @@ constexpr int kSubs = kTile / 64;            // 64-item sub-chunks per tile
 constexpr int kSubsPerWave = kSubs / kLinWaves;
 constexpr int kMaxChunk = 8192;              // heights per workgroup held in LDS
 constexpr int kTargetChunk = 1024;           // default chunk when the grid is free
+constexpr int kLinPer = kTargetChunk / kLinThreads;   // nodes per thread whose children sit in registers
 
 
 struct LinArgs {
@@ -99,10 +100,99 @@ __device__ int block_exclusive_scan(int *data, int n, int *wsum) {
   return total;
 }
 
+// ---------------------------------------------------------------------------
+// Height relaxation over a block of nodes whose heights live in LDS (hs).  A
+// thread owns the nodes i = tid + j*THREADS (j < PER) and holds their child
+// slots in registers: lc = the child's index inside the block (-1 when the
+// slot is empty or the child lies outside), ext = a fixed lower bound on the
+// height of a child outside the block (-1 otherwise).  A sweep raises h(i) to
+// 1 + max over its children.  Values only grow and never pass the true
+// height, so sweeps run without barriers, each wave reading whatever the
+// others last wrote.  After kSweepBatch such sweeps come a barrier and one
+// more sweep: if that sweep changes nothing anywhere, every h(i) equals
+// 1 + max over its children as they stand, which is the fixed point, i.e.
+// the height.  A value >= N proves a cycle.
+// ---------------------------------------------------------------------------
+constexpr int kSweepBatch = 4;
+
+template <int PER, int THREADS, int KS>
+__device__ __forceinline__ bool height_sweep(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER],
+                                             int *hs, int n, int N, bool &cyc) {
+  bool changed = false;
+  // A wave reads the child heights of its live nodes back to back, with one
+  // wait: whether round j holds live nodes is uniform over the wave, and an
+  // empty slot reads entry 0 of the block and is masked.  KS = slots read.
+  const int wave_first = (int)(threadIdx.x & ~63u);
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    if (wave_first + j * THREADS >= n) break;
+    int hv[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) hv[s] = lds_load(&hs[lc[j][s] >= 0 ? lc[j][s] : 0]);
+    const int i = (int)threadIdx.x + j * THREADS;
+    int m = -1;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) m = max(m, max(lc[j][s] >= 0 ? hv[s] : -1, ext[j][s]));
+    if (i < n && m + 1 > myh[j]) {
+      myh[j] = m + 1;
+      lds_store(&hs[i], m + 1);
+      changed = true;
+      if (m + 1 >= N) cyc = true;
+    }
+  }
+  return changed;
+}
+
+// Sweeps to the fixed point over child slots [0, KS).  Returns (uniformly
+// over the workgroup) whether any height changed; *cycle is set when a value
+// reached N.  Every thread of the workgroup calls it.
+template <int PER, int THREADS, int KS>
+__device__ bool relax_heights_k(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
+                                int N, bool *cycle, int *sweeps) {
+  bool any = false;
+  *cycle = false;
+  for (;;) {
+    bool cyc = false;
+#pragma unroll 1
+    for (int r = 0; r < kSweepBatch; ++r) any |= height_sweep<PER, THREADS, KS>(lc, ext, myh, hs, n, N, cyc);
+    __syncthreads();
+    const bool ch = height_sweep<PER, THREADS, KS>(lc, ext, myh, hs, n, N, cyc);
+    any |= ch;
+    *sweeps += kSweepBatch + 1;
+    if (__syncthreads_or(cyc)) {
+      *cycle = true;
+      break;
+    }
+    if (!__syncthreads_or(ch)) break;
+  }
+  return __syncthreads_or(any) != 0;
+}
+
+template <int PER, int THREADS>
+__device__ bool relax_heights(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
+                              int K, int N, bool *cycle, int *sweeps) {
+  if (K <= 2) return relax_heights_k<PER, THREADS, 2>(lc, ext, myh, hs, n, N, cycle, sweeps);
+  return relax_heights_k<PER, THREADS, 4>(lc, ext, myh, hs, n, N, cycle, sweeps);
+}
+
+// Trace builds only: workgroup 0 stamps phase boundaries into uint64 slots
+// 1..15 of the barrier header (the generation word uses slot 0 only).
+#ifdef CORTEX_TRACE
+#define CORTEX_BIG_STAMP(k, v)                                                        \
+  do {                                                                               \
+    if (blockIdx.x == 0 && threadIdx.x == 0) ((uint64_t *)a.sync)[(k)] = (v);          \
+  } while (0)
+#else
+#define CORTEX_BIG_STAMP(k, v) \
+  do {                         \
+  } while (0)
+#endif
+
 __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   __shared__ int hs[kMaxChunk];
   __shared__ int cnt[kSubs][256];
   __shared__ int hist[256];
+  __shared__ int base_s[256];
   __shared__ int scan_tmp[kLinThreads];
 
   const SyncWords sw{a.sync};
@@ -112,9 +202,42 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   const int lo = blockIdx.x * a.chunk;
   const int hi = min(N, lo + a.chunk);
   const int n = max(0, hi - lo);
-  bool ok = load_status(a.status) == 0;
+  CORTEX_BIG_STAMP(1, wall_clock64());
+  const int status0 = load_status(a.status);     // requested together with the children
+  int sweeps0 = 0;
 
   // ---------------- 1. heights ----------------
+  // The children of a chunk of at most kLinPer nodes per thread (the default
+  // chunk) go to registers once; a larger chunk reads them on every sweep.
+  const bool in_regs = n <= kLinPer * kLinThreads;
+  int cid[kLinPer][4], lc[kLinPer][4], ext[kLinPer][4], myh[kLinPer];
+  int bad = 0;
+  // all loads issued before any is used (absent slots read entry 0, masked)
+#pragma unroll
+  for (int j = 0; j < kLinPer; ++j)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int i = tid + j * kLinThreads;
+      cid[j][s] = a.children[(in_regs && i < n && s < K) ? (size_t)(lo + i) * K + s : 0];
+    }
+#pragma unroll
+  for (int j = 0; j < kLinPer; ++j) {
+    const int i = tid + j * kLinThreads;
+    myh[j] = 0;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      int c = (in_regs && i < n && s < K) ? cid[j][s] : -1;
+      if (c < -1 || c >= N) {
+        bad = 1;
+        c = -1;
+      }
+      cid[j][s] = c;
+      lc[j][s] = (c >= lo && c < hi) ? c - lo : -1;
+      ext[j][s] = -1;
+    }
+  }
+  bool ok = status0 == 0;
+  if (bad) raise_status(a.status, CORTEX_ST_CHILD_RANGE);
   for (int i = tid; i < n; i += kLinThreads) hs[i] = 0;
   __syncthreads();
   int round = 0;
@@ -122,7 +245,22 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   while (ok) {
     int block_changed = (round == 0);
     int local_max = 0;
-    for (;;) {
+    if (in_regs) {
+      // children outside the chunk keep one height per round: 0 in round 0
+      // (a lower bound), then what the previous round published
+#pragma unroll
+      for (int j = 0; j < kLinPer; ++j)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const int c = cid[j][s];
+          ext[j][s] = (c < 0 || lc[j][s] >= 0)
+                          ? -1
+                          : (round == 0 ? 0 : __hip_atomic_load(&a.height[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        }
+      bool cyc;
+      if (relax_heights<kLinPer, kLinThreads>(lc, ext, myh, hs, n, K, N, &cyc, &sweeps0)) block_changed = 1;
+      if (cyc && tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
+    } else for (;;) {
       int changed = 0, cyc = 0;
       for (int i = tid; i < n; i += kLinThreads) {
         const int v = lo + i;
@@ -153,6 +291,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       // uniform exit decision for the whole workgroup
       const int any = __syncthreads_or(changed);
       const int stop = __syncthreads_or(cyc);
+      if (round == 0) ++sweeps0;
       block_changed |= any;
       if (!any || stop) break;
     }
@@ -188,6 +327,9 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     }
   }
 
+  CORTEX_BIG_STAMP(2, wall_clock64());
+  CORTEX_BIG_STAMP(7, (uint64_t)round);
+  CORTEX_BIG_STAMP(8, (uint64_t)sweeps0);
   // ---------------- 2. stable counting sort on height ----------------
   int passes = 1;
   for (int v = (L - 1) >> 8; v > 0; v >>= 8) ++passes;
@@ -218,29 +360,27 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     }
     ok = grid_sync(sw, a.status, a.timeout);
     if (!ok) break;
-
-    // (b) exclusive scan of the 256*T counts, by workgroup 0, through LDS in
-    //     chunks of kSubs*256 (the cnt array), carrying the running total
-    if (blockIdx.x == 0) {
-      const int M = 256 * T;
-      int carry = 0;
-      int *buf = &cnt[0][0];
-      for (int c0 = 0; c0 < M; c0 += kSubs * 256) {
-        const int n = min(kSubs * 256, M - c0);
-        for (int i = tid; i < n; i += kLinThreads) buf[i] = a.tile_hist[c0 + i];
-        __syncthreads();
-        const int total = block_exclusive_scan<kLinThreads>(buf, n, scan_tmp);
-        for (int i = tid; i < n; i += kLinThreads) a.tile_hist[c0 + i] = buf[i] + carry;
-        carry += total;
-        __syncthreads();
-      }
-    }
-    ok = grid_sync(sw, a.status, a.timeout);
-    if (!ok) break;
+    if (p == 0) CORTEX_BIG_STAMP(3, wall_clock64());
 
     // (c) stable scatter: rank = (digit base of this tile) + (equal digits
     //     earlier in the tile).  Sub-chunk q of 64 items goes to wave q/4.
     for (int t = blockIdx.x; t < T; t += G) {
+      // digit bases of tile t, from every tile's histogram: the rows of all
+      // smaller digits, plus the rows of the same digit in earlier tiles
+      {
+        int tot = 0, before = 0;
+#pragma unroll 8
+        for (int t2 = 0; t2 < T; ++t2) {
+          const int x = a.tile_hist[(size_t)tid * T + t2];
+          tot += x;
+          before += t2 < t ? x : 0;
+        }
+        hist[tid] = tot;
+        __syncthreads();
+        block_exclusive_scan<kLinThreads>(hist, 256, scan_tmp);
+        base_s[tid] = hist[tid] + before;
+      }
+      if (p == 0 && t == (int)blockIdx.x) CORTEX_BIG_STAMP(4, wall_clock64());
       for (int i = tid; i < kSubs * 256; i += kLinThreads) (&cnt[0][0])[i] = 0;
       __syncthreads();
       int item[kSubsPerWave], dig[kSubsPerWave], rank[kSubsPerWave];
@@ -272,7 +412,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       for (int qq = 0; qq < kSubsPerWave; ++qq) {
         if (!valid[qq]) continue;
         const int q = wave * kSubsPerWave + qq;
-        const int pos = a.tile_hist[(size_t)dig[qq] * T + t] + cnt[q][dig[qq]] + rank[qq];
+        const int pos = base_s[dig[qq]] + cnt[q][dig[qq]] + rank[qq];
         if (pos < 0 || pos >= N) {              // cannot happen for consistent counts
           raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
           continue;
@@ -284,6 +424,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     }
     ok = grid_sync(sw, a.status, a.timeout);
   }
+  CORTEX_BIG_STAMP(5, wall_clock64());
 
   // ---------------- 3. level offsets and child rows ----------------
   if (ok) {
@@ -304,6 +445,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       *a.num_levels = L;
     }
   }
+  CORTEX_BIG_STAMP(6, wall_clock64());
 }
 
 
@@ -354,62 +496,54 @@ __global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs 
   int *flags = cursor + 256;          // [64] scratch
 
   CORTEX_LIN_STAMP(0);
-  if (load_status(a.status) != 0) return;
+  const int status0 = load_status(a.status);     // requested together with the children
   // 1. children: into registers for the sweeps (node v = tid + j*threads) and
   //    into LDS for the output phase; range check
   int myc[kSmallPer][4], myh[kSmallPer];
   int bad = 0;
+  // every load is issued before any result is used (an absent slot reads
+  // entry 0 and is masked), so they cost one memory round trip together
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int v = tid + j * kSmallThreads;
+      myc[j][s] = a.children[(v < N && s < K) ? (size_t)v * K + s : 0];
+    }
 #pragma unroll
   for (int j = 0; j < kSmallPer; ++j) {
     const int v = tid + j * kSmallThreads;
     myh[j] = 0;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      int c = (v < N && s < K) ? a.children[(size_t)v * K + s] : -1;
+      int c = (v < N && s < K) ? myc[j][s] : -1;
       if (c < -1 || c >= N) { bad = 1; c = -1; }
       myc[j][s] = c;
       if (v < N && s < K) ch[v * K + s] = c;
     }
     if (v < N) hgt[v] = 0;
   }
-  if (tid < 3) flags[tid] = 0;      // sweep change flags (3, rotating)
-  if (tid == 0) flags[3] = 0;       // cycle flag
+  if (__syncthreads_or(status0 != 0)) return;
   if (__syncthreads_or(bad)) {
     if (tid == 0) raise_status(a.status, CORTEX_ST_CHILD_RANGE);
     return;
   }
   CORTEX_LIN_STAMP(1);
-  // 2. heights: monotone sweeps to the fixed point, one barrier per sweep.
-  //    Sweep k raises flags[k % 3]; flags[(k+2) % 3] is cleared for sweep k+2
-  //    while no thread can still be reading it.
-  for (int k = 0;; ++k) {
-    if (tid == 0) flags[(k + 2) % 3] = 0;
-    int changed = 0, cyc = 0;
+  // 2. heights: barrier-free sweeps to the fixed point (every child is in LDS)
+  {
+    int ext[kSmallPer][4];
 #pragma unroll
-    for (int j = 0; j < kSmallPer; ++j) {
-      const int v = tid + j * kSmallThreads;
-      if (v >= N) continue;
-      int m = -1;
+    for (int j = 0; j < kSmallPer; ++j)
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-        if (myc[j][s] >= 0) m = max(m, lds_load(&hgt[myc[j][s]]));
-      if (m + 1 > myh[j]) {
-        myh[j] = m + 1;
-        lds_store(&hgt[v], m + 1);
-        changed = 1;
-        if (m + 1 >= N) cyc = 1;
-      }
-    }
-    if (changed) lds_store(&flags[k % 3], 1);
-    if (cyc) lds_store(&flags[3], 1);
-    __syncthreads();
-    if (lds_load(&flags[3])) {
+      for (int s = 0; s < 4; ++s) ext[j][s] = -1;
+    bool cyc;
+    int sweeps = 0;
+    relax_heights<kSmallPer, kSmallThreads>(myc, ext, myh, hgt, N, K, N, &cyc, &sweeps);
+    if (cyc) {
       if (tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
       return;
     }
-    if (!lds_load(&flags[k % 3])) break;
   }
-  __syncthreads();                  // every exit decision has read flags before they are reused
   CORTEX_LIN_STAMP(2);
   // L = 1 + max height, level counts
   int mx = 0;

@@ -144,6 +144,15 @@ def main():
     rep["workload"] = wl.name
     rep["grid"] = C.cortex_last_grid(1)
     rep["num_levels"] = L
+    lin_big = dw.ws_lin[:128].cpu().numpy().view(np.uint64).astype(np.int64)
+    if C.cortex_last_grid(0) > 1 and lin_big[1] > 0:
+        # multi-workgroup linearizer (workgroup 0's view): entry, heights,
+        # histograms, scan, sort, offsets and child rows; height rounds and
+        # the local sweeps of round 0
+        t = lin_big[1:7]
+        rep["linearize_big_phases_us"] = [float(x - t[0]) / TICKS_PER_US for x in t]
+        rep["linearize_big_rounds"] = int(lin_big[7])
+        rep["linearize_big_sweeps0"] = int(lin_big[8])
     if C.cortex_last_grid(0) == 1 and lin_stamps[0] > 0:
         # single-workgroup linearizer: entry, children loaded, heights done,
         # level counts, sort done, outputs written, offsets written
@@ -152,6 +161,11 @@ def main():
     if "linearize_phases_us" in rep:
         md += ("\n\nLinearizer (one workgroup), from its entry: children loaded %.2f, heights %.2f, "
                "level counts %.2f, sort %.2f, outputs %.2f, offsets %.2f us." % tuple(rep["linearize_phases_us"][1:]))
+    if "linearize_big_phases_us" in rep:
+        md += ("\n\nLinearizer (%d workgroups), workgroup 0 from its entry: heights %.2f (%d global rounds, "
+               "%d local sweeps in round 0), histograms %.2f, scan %.2f, sort %.2f, offsets and child rows %.2f us."
+               % (C.cortex_last_grid(0), rep["linearize_big_phases_us"][1], rep["linearize_big_rounds"],
+                  rep["linearize_big_sweeps0"], *rep["linearize_big_phases_us"][2:]))
     print(md)
     sys.stdout.flush()
     if args.json:
