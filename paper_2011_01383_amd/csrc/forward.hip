@@ -549,8 +549,9 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   const int cross_b = (H - o0) / 16 < NB ? (H - o0) / 16 : NB;
 
   CORTEX_TRACE_KERNEL(0);
-  if (load_status(a.status) != 0) return;
+  const int status0 = load_status(a.status);    // one round trip with the weight loads
   load_weight_slice<CELL, H, J>(a, hbase, W_s, bias_s);
+  if (status0 != 0) return;
   CORTEX_TRACE_KERNEL(1);
   int L;
   const int *off, *codes, *xrow;
@@ -763,6 +764,102 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
     }
     CORTEX_TRACE_POINT(l, 5);
     if (__syncthreads_or(gave_up)) return;
+  }
+  CORTEX_TRACE_KERNEL(3);
+}
+
+// ---------------------------------------------------------------------------
+// TreeRNN at H = 64 in one workgroup with every state in LDS.
+//   h = tanh(W [h(slot 0); h(slot 1)] + b),  leaf h = its input row.
+// The whole cell fits one CU: wave w holds W[16 (w & 3) .., (w >> 2) * 64 ..]
+// (its 16 output units x the 64 columns of child slot w >> 2) in registers,
+// and the h row of every node stays in LDS, so a level reads its children
+// from LDS and one barrier orders consecutive levels; nothing goes through
+// global memory between levels, and the states are written out once at the
+// end.  Used while the rows fit the LDS budget.
+// ---------------------------------------------------------------------------
+constexpr int kLdsH = 64;
+constexpr int kLdsHStride = kLdsH + 4;        // h row stride in LDS
+constexpr int kLdsMaxRows = 320;              // rows kept in LDS
+
+__global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
+  constexpr int H = kLdsH, LDH = kLdsHStride, NB = H / 16;
+  constexpr int EPI = kTileM * H / kFwdThreads;
+  __shared__ __attribute__((aligned(16))) float C_s[2][kTileM][H + 4];
+  __shared__ float bias_s[H];
+  extern __shared__ __attribute__((aligned(16))) float dyn_s[];   // h rows, then the structure cache
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int nt = wave & 3, kh = wave >> 2;     // this wave's output units and child slot
+  const int N = a.N;
+  float *h_s = dyn_s;
+  int *cache = (int *)(dyn_s + (size_t)N * LDH);
+
+  CORTEX_TRACE_KERNEL(0);
+  const int status0 = load_status(a.status);  // one round trip with the weight loads
+  // wr[b] = W[16 nt + i16][64 kh + 16 b + 4 g4 .. +3]
+  float4 wr[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    wr[b] = *(const float4 *)(a.W + (size_t)(16 * nt + i16) * 2 * H + kh * H + 16 * b + 4 * g4);
+  if (tid < H) bias_s[tid] = a.b[tid];
+  if (status0 != 0) return;
+  CORTEX_TRACE_KERNEL(1);
+  Structure<true> st;
+  int L;
+  if (!setup_structure<true, true, false>(a, cache, st, L)) return;
+  CORTEX_TRACE_KERNEL(2);
+
+  // level 0: the leaves are their input rows (zeros without one)
+  const int off1 = st.offset(1 < L ? 1 : L);
+  CORTEX_TRACE_POINT(0, 0);
+  for (int e = tid; e < off1 * (H / 4); e += kFwdThreads) {
+    const int r = e / (H / 4), c4 = e % (H / 4);
+    const int xr = st.input_row(r);
+    const float4 v = xr >= 0 ? *(const float4 *)&a.x_table[(size_t)xr * H + 4 * c4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    *(float4 *)&h_s[r * LDH + 4 * c4] = v;
+  }
+  __syncthreads();
+  CORTEX_TRACE_POINT(0, 5);
+
+  for (int l = 1; l < L; ++l) {
+    CORTEX_TRACE_POINT(l, 0);
+    const int r0 = st.offset(l), r1 = st.offset(l + 1);
+    for (int rowbase = r0; rowbase < r1; rowbase += kTileM) {
+      const int row = rowbase + i16;
+      const int cr = row < r1 ? st.child(row, kh) : -1;
+      float4 av[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        av[b] = cr >= 0 ? *(const float4 *)&h_s[cr * LDH + 16 * b + 4 * g4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      CORTEX_TRACE_POINT(l, 2);
+      floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if (b & 1) acc1 = mfma_k16(av[b], wr[b], acc1);
+        else acc0 = mfma_k16(av[b], wr[b], acc0);
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) C_s[kh][4 * g4 + v][16 * nt + i16] = acc0[v] + acc1[v];
+      __syncthreads();
+      CORTEX_TRACE_POINT(l, 3);
+#pragma unroll
+      for (int e = 0; e < EPI; ++e) {
+        const int p = tid + e * kFwdThreads, i = p / H, j = p % H;
+        const int r = rowbase + i;
+        if (r < r1) h_s[r * LDH + j] = tanh_f(bias_s[j] + C_s[0][i][j] + C_s[1][i][j]);
+      }
+      __syncthreads();
+      CORTEX_TRACE_POINT(l, 4);
+    }
+    CORTEX_TRACE_POINT(l, 5);
+  }
+  // every state leaves LDS once, coalesced (no global store inside the
+  // level loop, whose barriers would otherwise wait for them)
+  for (int e = tid; e < N * (H / 4); e += kFwdThreads) {
+    const int r = e / (H / 4), c4 = e % (H / 4);
+    *(float4 *)&a.h[(size_t)r * H + 4 * c4] = *(const float4 *)&h_s[r * LDH + 4 * c4];
   }
   CORTEX_TRACE_KERNEL(3);
 }
@@ -1170,8 +1267,9 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
   const int zi = tid / ZW, zk = (tid % ZW) / J, zj = tid % J;
 
   CORTEX_TRACE_KERNEL(0);
-  if (load_status(a.status) != 0) return;
+  const int status0 = load_status(a.status);    // one round trip with the weight loads
   load_weight_slice<CORTEX_CHILDSUM_TREELSTM, H, J>(a, hbase, W_s, bias_s);
+  if (status0 != 0) return;
   CORTEX_TRACE_KERNEL(1);
   Structure<kCached> st;
   int L;
@@ -1533,8 +1631,15 @@ static void pick_slice(bool cached, Instance &out) {
 }
 
 // units per slice: the knob's value where an instance exists, else the default
-static bool pick(int cell, int H, bool cached, Instance &out) {
+static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   const int64_t units = knob(CORTEX_KNOB_FWD_SLICE_UNITS);
+  if (cell == CORTEX_TREE_RNN && H == kLdsH && N <= kLdsMaxRows && knob(CORTEX_KNOB_FWD_NODE_GROUPS) <= 1) {
+    out.fn = tree_rnn_lds_kernel;        // one workgroup, every state in LDS
+    out.J = kLdsH;
+    out.threads = kFwdThreads;
+    out.lds = (size_t)N * kLdsHStride * sizeof(float) + (4 * (size_t)N + 2) * sizeof(int);
+    return true;
+  }
   if (cell == CORTEX_NARY_TREELSTM && H == 256 && units == 2) {
     pick_slice<CORTEX_NARY_TREELSTM, 256, 2>(cached, out);
     return true;
@@ -1604,7 +1709,7 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
     if (!cached) dyn = 0;
   }
   Instance inst;
-  if (!pick(cell, H, cached, inst)) return CORTEX_E_INVAL;
+  if (!pick(cell, H, lin->num_nodes, cached, inst)) return CORTEX_E_INVAL;
   if (inst.lds != SIZE_MAX) dyn = inst.lds;
   const int per_cu = cached_occupancy((const void *)inst.fn, inst.threads, dyn);
   const int cus = num_cus();

@@ -529,8 +529,80 @@ __global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs 
     return;
   }
   CORTEX_LIN_STAMP(1);
-  // 2. heights: barrier-free sweeps to the fixed point (every child is in LDS)
-  {
+  // 2. heights.  Forest (every node fills at most one child slot in the
+  //    whole batch): a last-arriver walk.  Each node counts its pending
+  //    children; the thread of a leaf climbs towards the root: at each
+  //    parent it raises the parent's height to its own + 1, then takes one
+  //    off the parent's count, and the thread that empties the count holds
+  //    the parent's final height and climbs on.  A node still pending
+  //    afterwards lies on or above a cycle.  Any other DAG: barrier-free
+  //    sweeps to the fixed point.  (perm0, nrow and lcount serve as the
+  //    parent-count, parent and pending arrays here; all are rewritten later.)
+  //    The walk's LDS operations stay in program order (compiler fences) and
+  //    the LDS unit performs one wave's operations in that order, so the
+  //    raise lands before the decrement and the last decrement sees every
+  //    sibling's raise.
+  int *npar = perm0, *parent = nrow, *pend = lcount;
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    const int v = tid + j * kSmallThreads;
+    if (v < N) {
+      npar[v] = 0;
+      parent[v] = -1;
+      pend[v] = (myc[j][0] >= 0) + (myc[j][1] >= 0) + (myc[j][2] >= 0) + (myc[j][3] >= 0);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    const int v = tid + j * kSmallThreads;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int c = myc[j][s];
+      if (c >= 0) {
+        __hip_atomic_fetch_add(&npar[c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        parent[c] = v;
+      }
+    }
+  }
+  __syncthreads();
+  int multi = 0;
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    const int v = tid + j * kSmallThreads;
+    if (v < N && npar[v] > 1) multi = 1;
+  }
+  if (!__syncthreads_or(multi)) {
+#pragma unroll 1
+    for (int j = 0; j < kSmallPer; ++j) {
+      const int v = tid + j * kSmallThreads;
+      if (v >= N || (myc[j][0] >= 0) + (myc[j][1] >= 0) + (myc[j][2] >= 0) + (myc[j][3] >= 0) != 0) continue;
+      int hu = 0, p = parent[v];
+      while (p >= 0) {
+        __hip_atomic_fetch_max(&hgt[p], hu + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        const int left = __hip_atomic_fetch_sub(&pend[p], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (left != 1) break;
+        hu = lds_load(&hgt[p]);
+        p = lds_load(&parent[p]);
+      }
+    }
+    __syncthreads();
+    int stuck = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallPer; ++j) {
+      const int v = tid + j * kSmallThreads;
+      if (v < N) {
+        if (pend[v] != 0) stuck = 1;
+        myh[j] = hgt[v];
+      }
+    }
+    if (__syncthreads_or(stuck)) {
+      if (tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
+      return;
+    }
+  } else {
     int ext[kSmallPer][4];
 #pragma unroll
     for (int j = 0; j < kSmallPer; ++j)
@@ -558,23 +630,38 @@ __global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs 
   L += 1;
   for (int v = tid; v < N; v += kSmallThreads) atomicAdd(&lcount[hgt[v]], 1);
   __syncthreads();
+  // level offsets = exclusive scan of the level counts (kept in lcount)
+  const int total = block_exclusive_scan<kSmallThreads>(lcount, L, flags);
+  for (int l = tid; l < L; l += kSmallThreads) a.level_offsets[l] = lcount[l];
+  if (tid == 0) {
+    a.level_offsets[L] = total;
+    *a.num_levels = L;
+  }
   CORTEX_LIN_STAMP(3);
-  // 3. stable LSD counting sort on height, 8-bit digits
+  // 3. stable LSD counting sort on height, 8-bit digits.  With one pass
+  //    (L <= 256) the digit is the height itself: its starts are the level
+  //    offsets, and only bits(L-1) ballots and L digit columns are needed.
   int passes = 1;
   for (int v = (L - 1) >> 8; v > 0; v >>= 8) ++passes;
+  const int nbits = passes == 1 ? 32 - __clz(L - 1) : 8;      // __clz(0) = 32: L = 1 needs none
+  const int ndig = passes == 1 ? L : 256;
   const unsigned long long lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
   for (int p = 0; p < passes; ++p) {
     const int shift = 8 * p;
     const int *in = (p & 1) ? perm0 : perm1;    // pass 0 reads ids directly
     int *out = (p & 1) ? perm1 : perm0;
-    if (tid < 256) dstart[tid] = 0;
-    __syncthreads();
-    for (int i = tid; i < N; i += kSmallThreads) {
-      const int v = p == 0 ? i : in[i];
-      atomicAdd(&dstart[(hgt[v] >> shift) & 255], 1);
+    if (passes == 1) {
+      if (tid < L) dstart[tid] = lcount[tid];
+    } else {
+      if (tid < 256) dstart[tid] = 0;
+      __syncthreads();
+      for (int i = tid; i < N; i += kSmallThreads) {
+        const int v = p == 0 ? i : in[i];
+        atomicAdd(&dstart[(hgt[v] >> shift) & 255], 1);
+      }
+      __syncthreads();
+      block_exclusive_scan<kSmallThreads>(dstart, 256, flags);
     }
-    __syncthreads();
-    block_exclusive_scan<kSmallThreads>(dstart, 256, flags);
     if (tid < 256) cursor[tid] = 0;
     __syncthreads();
     for (int base = 0; base < N; base += kSmallThreads) {
@@ -583,18 +670,17 @@ __global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs 
       const int item = valid ? (p == 0 ? idx : in[idx]) : 0;
       const int dig = valid ? ((hgt[item] >> shift) & 255) : 0;
       unsigned long long peers = __ballot(valid);
-#pragma unroll
-      for (int b = 0; b < 8; ++b) {
+      for (int b = 0; b < nbits; ++b) {
         const bool bit = (dig >> b) & 1;
         const unsigned long long m = __ballot(bit);
         peers &= bit ? m : ~m;
       }
       const int rank = __popcll(peers & lt_mask);
-      for (int i = tid; i < kSmallWaves * 256; i += kSmallThreads) wcnt[i] = 0;
+      for (int i = tid; i < kSmallWaves * ndig; i += kSmallThreads) wcnt[(i / ndig) * 256 + i % ndig] = 0;
       __syncthreads();
       if (valid && rank == 0) wcnt[wave * 256 + dig] = __popcll(peers);
       __syncthreads();
-      if (tid < 256) {             // per digit: wave offsets within the chunk, then advance the cursor
+      if (tid < ndig) {            // per digit: wave offsets within the chunk, then advance the cursor
         int run = cursor[tid];
         for (int w = 0; w < kSmallWaves; ++w) { const int x = wcnt[w * 256 + tid]; wcnt[w * 256 + tid] = run; run += x; }
         cursor[tid] = run;
@@ -620,12 +706,6 @@ __global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs 
     }
   }
   CORTEX_LIN_STAMP(5);
-  const int total = block_exclusive_scan<kSmallThreads>(lcount, L, flags);
-  for (int l = tid; l < L; l += kSmallThreads) a.level_offsets[l] = lcount[l];
-  if (tid == 0) {
-    a.level_offsets[L] = total;
-    *a.num_levels = L;
-  }
   CORTEX_LIN_STAMP(6);
 }
 

@@ -160,7 +160,7 @@ def main():
     md = as_markdown(rep, "%s (grid %d, %d levels)" % (wl.name, rep["grid"], L))
     if "linearize_phases_us" in rep:
         md += ("\n\nLinearizer (one workgroup), from its entry: children loaded %.2f, heights %.2f, "
-               "level counts %.2f, sort %.2f, outputs %.2f, offsets %.2f us." % tuple(rep["linearize_phases_us"][1:]))
+               "level counts and offsets %.2f, sort %.2f, outputs %.2f (end %.2f) us." % tuple(rep["linearize_phases_us"][1:]))
     if "linearize_big_phases_us" in rep:
         md += ("\n\nLinearizer (%d workgroups), workgroup 0 from its entry: heights %.2f (%d global rounds, "
                "%d local sweeps in round 0), histograms %.2f, scan %.2f, sort %.2f, offsets and child rows %.2f us."

@@ -224,3 +224,15 @@ def test_dag_tile_list_overflow():
     dw = run(wl, 1)
     assert C.cortex_last_grid(1) == 4
     compare_states(dw.states_by_node(), O.forward_workload(wl), "dag overflow")
+
+
+@pytest.mark.parametrize("n_leaves", [1, 2, 7, 160, 161, 230])
+def test_tree_rnn_h64_lds_limit(n_leaves):
+    """TreeRNN at H = 64 runs in one workgroup with every state in LDS up to
+    320 rows (160 leaves: 319 rows) and in the slice kernel beyond; both
+    sides of the limit against the oracle."""
+    wl = I.tree_rnn_workload(600 + n_leaves, n_leaves=n_leaves, H=64)
+    announce("tree_rnn h64 %d leaves N=%d" % (n_leaves, wl.N))
+    dw = run(wl)
+    assert C.cortex_last_grid(1) == 1
+    compare_states(dw.states_by_node(), O.forward_workload(wl), "tree_rnn %d leaves" % n_leaves)
