@@ -15,13 +15,13 @@
  *                           whose dependence is carried by the batch loop,
  *                           Appendix A.4), run as ONE persistent kernel with
  *                           the cell weights resident on chip (kernel fusion
- *                           and model persistence, Sec. 7.2 and 7.3).  The
- *                           tree, child-sum and DAG kernels order levels per
- *                           datum: each state element is also published as a
- *                           (value, launch tag) pair in the workspace and a
- *                           consumer waits for exactly the elements it reads;
- *                           the MV-RNN kernel uses one device-wide barrier
- *                           per level.
+ *                           and model persistence, Sec. 7.2 and 7.3).  Levels
+ *                           are ordered per datum: each state element is
+ *                           also published as a (value, launch tag) pair in
+ *                           the workspace and a consumer waits for exactly
+ *                           the elements it reads (a TreeRNN batch small
+ *                           enough for one workgroup keeps its states in
+ *                           LDS and orders levels with workgroup barriers).
  *
  * Conventions shared by every entry point
  * ---------------------------------------

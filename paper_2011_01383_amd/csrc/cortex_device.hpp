@@ -133,6 +133,9 @@ struct InBuf {
   __device__ __forceinline__ u32x4 load4(uint32_t off) const {
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
   }
+  __device__ __forceinline__ unsigned int load1(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+  }
 };
 
 __device__ __forceinline__ float4 as_float4(u32x4 v) {

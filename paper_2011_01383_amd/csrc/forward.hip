@@ -1481,94 +1481,210 @@ __device__ __forceinline__ bool level_bounds(const FwdArgs &a, int l, int &r0, i
 // Node-parallel: workgroup b owns output rows [16*(b%4), 16*(b%4)+16) of every
 // node it processes (its 16 rows of W and W_M stay in LDS), and node group
 // b/4 takes nodes q, q + G/4, ... of each level.  P = W_M[A;B] runs on MFMA
-// with [A;B] staged in LDS; the matrix-vector products use VALU.
+// with [A;B] staged in LDS; the matrix-vector products use VALU.  Levels are
+// ordered per datum, as in the slice kernels: every element of p and P is
+// also published as a (value, launch tag) pair, a workgroup waits for
+// exactly the child vectors and matrices it stages, and a leaf child is read
+// from the inputs (its state is the given (a, A)), so nothing waits on the
+// leaf level.  Child rows and the input rows of the leaves are cached in LDS
+// for batches of up to kMvCacheRows rows.
 // ---------------------------------------------------------------------------
 constexpr int kMvThreads = 256;
 constexpr int kMvD = 64;
 constexpr int kMvLd = 2 * kMvD + 4;        // W / W_M slice row stride
 constexpr int kMvAb = kMvD + 1;            // [A;B] row stride (odd: row-wise reads spread banks)
+constexpr int kMvGroups = 2 * kMvD * kMvD / 4 / kMvThreads;   // float4 groups of [A;B] per thread
+constexpr int kMvCacheRows = 3072;
 
 __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
   constexpr int D = kMvD;
+  constexpr int WPER = 16 * 2 * D / kMvThreads;
   __shared__ float WM_s[16 * kMvLd];
   __shared__ float Wv_s[16 * kMvLd];
   __shared__ float AB_s[2 * D * kMvAb];
   __shared__ float vec_s[2 * D];          // a (left vector), b (right vector)
   __shared__ float bab_s[2 * D];          // [B a; A b]
-  __shared__ int cr_s[2];
+  __shared__ int src_s[2][2];             // per child slot: staged row or -1, input row or -1
+  extern __shared__ int mv_cache[];       // cached: child rows [N*2], then leaf input rows [off1]
 
-  const SyncWords sw{a.sync};
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
   const int rblk = blockIdx.x & 3, ngroup = blockIdx.x >> 2, ngroups = gridDim.x >> 2;
-  const DevBuf hb(a.h, (uint32_t)a.N * D * 4);
-  const DevBuf pb(a.c, (uint32_t)a.N * D * D * 4);
+  const int N = a.N;
+  const bool cached = N <= kMvCacheRows;
+  const uint32_t tag = a.tag;
+  const TagBuf hs(a.hs, (uint32_t)N * D * 8);
+  const TagBuf ps(a.cs, (uint32_t)N * D * D * 8);
+  const InBuf xv(a.x_table, a.x_table ? (uint32_t)a.x_rows * D * 4 : 0u);
+  const InBuf xm(a.leaf_mat, a.leaf_mat ? (uint32_t)a.x_rows * D * D * 4 : 0u);
 
-  bool ok = load_status(a.status) == 0;
-  if (!ok) return;
-  for (int idx = tid; idx < 16 * 2 * D; idx += kMvThreads) {
-    const int r = idx / (2 * D), k = idx % (2 * D);
-    WM_s[r * kMvLd + k] = a.W_M[(size_t)(rblk * 16 + r) * 2 * D + k];
-    Wv_s[r * kMvLd + k] = a.W[(size_t)(rblk * 16 + r) * 2 * D + k];
-  }
+  // status, level count and weights requested together
+  const int status0 = load_status(a.status);
   const int L = *a.num_levels;
-  if (L < 1 || L > a.N) {
+  {
+    float wm[WPER], wv[WPER];
+#pragma unroll
+    for (int k = 0; k < WPER; ++k) {
+      const int idx = tid + k * kMvThreads, r = idx / (2 * D), c = idx % (2 * D);
+      wm[k] = a.W_M[(size_t)(rblk * 16 + r) * 2 * D + c];
+      wv[k] = a.W[(size_t)(rblk * 16 + r) * 2 * D + c];
+    }
+#pragma unroll
+    for (int k = 0; k < WPER; ++k) {
+      const int idx = tid + k * kMvThreads, r = idx / (2 * D), c = idx % (2 * D);
+      WM_s[r * kMvLd + c] = wm[k];
+      Wv_s[r * kMvLd + c] = wv[k];
+    }
+  }
+  if (status0 != 0) return;
+  if (L < 1 || L > N) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
     return;
   }
-  // leaves: (p, P) = (x_table[x], leaf_mat[x]) or zeros; rows spread over all workgroups
-  {
-    int r0, r1;
-    if (!level_bounds(a, 0, r0, r1)) ok = false;
-    for (int r = blockIdx.x; ok && r < r1; r += gridDim.x) {
-      const int v = a.level_nodes[r];
-      int xi = (v >= 0 && v < a.N) ? a.x_index[v] : -1;
-      if (xi < -1 || xi >= a.x_rows) { raise_status(a.status, CORTEX_ST_INPUT_RANGE); xi = -1; }
-      if (tid < D / 4) {
-        float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (xi >= 0) val = *(const float4 *)(a.x_table + (size_t)xi * D + tid * 4);
-        hb.store4((uint32_t)((r * D + tid * 4) * 4), val);
-      }
-      for (int e = tid; e < D * D / 4; e += kMvThreads) {
-        float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (xi >= 0) val = *(const float4 *)(a.leaf_mat + (size_t)xi * D * D + e * 4);
-        pb.store4((uint32_t)((r * D * D + e * 4) * 4), val);
-      }
+  int r0, r1;
+  if (!level_bounds(a, 0, r0, r1)) return;
+  const int off1 = r1;
+
+  // input row of leaf row r (validated), -1 = none
+  auto leaf_input = [&](int r) -> int {
+    const int v = a.level_nodes[r];
+    if (v < 0 || v >= N) {
+      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      return -1;
     }
-    if (L > 1) ok = grid_sync<false>(sw, a.status, a.timeout) && ok;
+    const int xi = a.x_index[v];
+    if (xi < -1 || xi >= a.x_rows) {
+      raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+      return -1;
+    }
+    return xi;
+  };
+  int *crow_c = mv_cache, *leafx_c = mv_cache + 2 * N;
+  if (cached) {
+    for (int i = tid; i < 2 * N; i += kMvThreads) {
+      int c = a.child_rows[i];
+      if (c < -1 || c >= N) {
+        raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+        c = -1;
+      }
+      crow_c[i] = c;
+    }
+    for (int r = tid; r < off1; r += kMvThreads) leafx_c[r] = leaf_input(r);
+    __syncthreads();
   }
-  for (int l = 1; ok && l < L; ++l) {
-    int r0, r1;
-    if (!level_bounds(a, l, r0, r1)) { ok = false; break; }
+
+  // leaves: (p, P) = (x_table[x], leaf_mat[x]) or zeros; rows spread over all
+  // workgroups, plain stores (no workgroup reads them back)
+  for (int r = blockIdx.x; r < off1; r += gridDim.x) {
+    const int xi = cached ? leafx_c[r] : leaf_input(r);
+    if (tid < D / 4) {
+      const float4 val = as_float4(xv.load4(xi >= 0 ? (uint32_t)((xi * D + tid * 4) * 4) : kNoSource));
+      *(float4 *)&a.h[(size_t)r * D + tid * 4] = val;
+    }
+    for (int e = tid; e < D * D / 4; e += kMvThreads) {
+      const float4 val = as_float4(xm.load4(xi >= 0 ? (uint32_t)((xi * D * D + e * 4) * 4) : kNoSource));
+      *(float4 *)&a.c[(size_t)r * D * D + e * 4] = val;
+    }
+  }
+
+  int gave_up = 0;
+  for (int l = 1; l < L && !gave_up; ++l) {
+    if (!level_bounds(a, l, r0, r1)) return;
     for (int r = r0 + ngroup; r < r1; r += ngroups) {
       if (tid < 2) {
-        int cr = a.child_rows[(size_t)r * a.K + tid];
-        if (cr < -1 || cr >= r0) { raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION); cr = -1; }
-        cr_s[tid] = cr;
+        int cr = cached ? crow_c[r * 2 + tid] : a.child_rows[(size_t)r * 2 + tid];
+        if (cr < -1 || cr >= r0) {              // a child must sit in a lower level
+          raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+          cr = -1;
+        }
+        src_s[tid][0] = cr >= off1 ? cr : -1;
+        src_s[tid][1] = (cr >= 0 && cr < off1) ? (cached ? leafx_c[cr] : leaf_input(cr)) : -1;
       }
       __syncthreads();
-      // stage [A; B] (rows 0..63 = A from slot 0, 64..127 = B from slot 1) and a, b
-      for (int e = tid; e < 2 * D * D / 4; e += kMvThreads) {
-        const int side = e / (D * D / 4), rem = e % (D * D / 4);
-        const int rr = rem / (D / 4), c4 = rem % (D / 4);
-        const int cr = cr_s[side];
-        float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (cr >= 0) val = pb.load4((uint32_t)((cr * D * D + rr * D + c4 * 4) * 4));
-        float *dst = &AB_s[(side * D + rr) * kMvAb + c4 * 4];
-        dst[0] = val.x; dst[1] = val.y; dst[2] = val.z; dst[3] = val.w;
+      // [A; B]: float4 group f = tid + k*256 is side f / 1024 (0 = A from
+      // slot 0, 1 = B from slot 1), element 4 (f mod 1024) of that matrix
+      u32x4 lo[kMvGroups], hi[kMvGroups];
+#pragma unroll
+      for (int k = 0; k < kMvGroups; ++k) {
+        const int f = tid + k * kMvThreads, side = f >> 10, e4 = (f & 1023) * 4;
+        const int st = src_s[side][0], xi = src_s[side][1];
+        if (st >= 0) {
+          const uint32_t so = (uint32_t)(st * D * D + e4) * 8u;
+          lo[k] = ps.load2_at(so);
+          hi[k] = ps.load2_at(so + 16u);
+        } else {
+          lo[k] = xm.load4(xi >= 0 ? (uint32_t)((xi * D * D + e4) * 4) : kNoSource);
+          hi[k] = u32x4{0u, 0u, 0u, 0u};
+        }
       }
+      // vectors: thread t < 128 takes element t mod 64 of side t / 64
+      const int vside = (tid >> 6) & 1, vk = tid & 63;
+      const int vst = src_s[vside][0], vxi = src_s[vside][1];
+      u32x2 vv = {0u, 0u};
       if (tid < 2 * D) {
-        const int cr = cr_s[tid / D];
-        vec_s[tid] = cr >= 0 ? hb.load1((uint32_t)((cr * D + (tid % D)) * 4)) : 0.f;
+        if (vst >= 0) vv = hs.load1_at((uint32_t)(vst * D + vk) * 8u);
+        else vv.x = xv.load1(vxi >= 0 ? (uint32_t)((vxi * D + vk) * 4) : kNoSource);
       }
-      __syncthreads();
+      auto ready = [&]() -> bool {
+        bool ok = !(tid < 2 * D && vst >= 0) || vv.y == tag;
+#pragma unroll
+        for (int k = 0; k < kMvGroups; ++k) {
+          const int side = (tid + k * kMvThreads) >> 10;
+          if (src_s[side][0] >= 0) ok = ok && lo[k].y == tag && lo[k].w == tag && hi[k].y == tag && hi[k].w == tag;
+        }
+        return ok;
+      };
+      if (!ready()) {
+        const uint64_t t0 = wall_clock64();
+        for (;;) {
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int k = 0; k < kMvGroups; ++k) {
+            const int f = tid + k * kMvThreads, side = f >> 10, st = src_s[side][0];
+            if (st >= 0 && !(lo[k].y == tag && lo[k].w == tag && hi[k].y == tag && hi[k].w == tag)) {
+              const uint32_t so = (uint32_t)(st * D * D + (f & 1023) * 4) * 8u;
+              lo[k] = ps.load2_at(so);
+              hi[k] = ps.load2_at(so + 16u);
+            }
+          }
+          if (tid < 2 * D && vst >= 0 && vv.y != tag) vv = hs.load1_at((uint32_t)(vst * D + vk) * 8u);
+          const int stv = load_status(a.status);
+          if (ready()) break;
+          if (stv != 0) {
+            gave_up = 1;
+            break;
+          }
+          if (wall_clock64() - t0 > a.timeout) {
+            raise_status(a.status, CORTEX_ST_BARRIER_TIMEOUT);
+            gave_up = 1;
+            break;
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kMvGroups; ++k) {
+        const int f = tid + k * kMvThreads, side = f >> 10, e4 = (f & 1023) * 4;
+        const bool staged = src_s[side][0] >= 0;
+        const float4 val = make_float4(as_float(lo[k].x), as_float(staged ? lo[k].z : lo[k].y),
+                                       as_float(staged ? hi[k].x : lo[k].z), as_float(staged ? hi[k].z : lo[k].w));
+        float *dst = &AB_s[(side * D + e4 / D) * kMvAb + e4 % D];
+        dst[0] = val.x;
+        dst[1] = val.y;
+        dst[2] = val.z;
+        dst[3] = val.w;
+      }
+      if (tid < 2 * D) vec_s[tid] = as_float(vv.x);
+      if (__syncthreads_or(gave_up)) {
+        gave_up = 1;
+        break;
+      }
       // [B a; A b]: thread k<64 -> (B a)[k] = sum_n B[k][n] a[n];  k>=64 -> (A b)[k-64]
       if (tid < 2 * D) {
         const int k = tid % D;
         const float *mrow = (tid < D) ? &AB_s[(D + k) * kMvAb] : &AB_s[k * kMvAb];
-        const float *vv = (tid < D) ? &vec_s[0] : &vec_s[D];
+        const float *vw = (tid < D) ? &vec_s[0] : &vec_s[D];
         float s = 0.f;
-        for (int n2 = 0; n2 < D; ++n2) s += mrow[n2] * vv[n2];
+        for (int n2 = 0; n2 < D; ++n2) s += mrow[n2] * vw[n2];
         bab_s[tid] = s;
       }
       // P rows [16*rblk, +16) = W_M[rows] [A;B]: wave w -> output columns 16w..16w+15
@@ -1578,9 +1694,12 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
         acc1 = mfma16x16x4(WM_s[i16 * kMvLd + k0 + 4 + g4], AB_s[(k0 + 4 + g4) * kMvAb + wave * 16 + i16], acc1);
       }
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        pb.store1((uint32_t)((r * D * D + (rblk * 16 + 4 * g4 + v) * D + wave * 16 + i16) * 4),
-                  acc0[v] + acc1[v]);
+      for (int v = 0; v < 4; ++v) {
+        const uint32_t el = (uint32_t)(r * D * D + (rblk * 16 + 4 * g4 + v) * D + wave * 16 + i16);
+        const float pv = acc0[v] + acc1[v];
+        ps.store1(el, pv, tag);
+        a.c[el] = pv;
+      }
       __syncthreads();
       // p rows: 16 outputs x 16 partial sums of 8 terms, reduced over 16 lanes
       {
@@ -1588,12 +1707,16 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
         float s = 0.f;
 #pragma unroll
         for (int kk = 0; kk < 8; ++kk) s += Wv_s[o * kMvLd + part * 8 + kk] * bab_s[part * 8 + kk];
-        for (int off = 8; off > 0; off >>= 1) s += __shfl_xor(s, off, 16);
-        if (part == 0) hb.store1((uint32_t)((r * D + rblk * 16 + o) * 4), tanh_f(s));
+        for (int sh = 8; sh > 0; sh >>= 1) s += __shfl_xor(s, sh, 16);
+        if (part == 0) {
+          const uint32_t el = (uint32_t)(r * D + rblk * 16 + o);
+          const float pv = tanh_f(s);
+          hs.store1(el, pv, tag);
+          a.h[el] = pv;
+        }
       }
       __syncthreads();
     }
-    if (l + 1 < L) ok = grid_sync<false>(sw, a.status, a.timeout);
   }
 }
 
@@ -1669,20 +1792,26 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
     out.fn = mvrnn_forward_kernel;
     out.J = kMvD;
     out.threads = kMvThreads;
+    out.lds = N <= kMvCacheRows ? 3 * (size_t)N * sizeof(int) : 0;
     return true;
   }
   return false;
 }
 
 // Workspace of a forward launch: barrier words, the trace area, then the
-// tagged staging of h (and of c for the LSTM cells), 8 bytes per element.
+// tagged staging of h (and of c for the LSTM cells, of P for MV-RNN), 8 bytes
+// per element.
 static size_t staging_bytes(int32_t N, int32_t H) { return align_up((size_t)N * H * 8, 256); }
 static size_t staging_offset() { return align_up(kSyncBytes + kTraceBytes, 256); }
 size_t trace_offset() { return kSyncBytes; }
 static int staged_tensors(int32_t cell) {
-  if (cell == CORTEX_NARY_TREELSTM || cell == CORTEX_CHILDSUM_TREELSTM) return 2;
+  if (cell == CORTEX_NARY_TREELSTM || cell == CORTEX_CHILDSUM_TREELSTM || cell == CORTEX_MVRNN) return 2;
   if (cell == CORTEX_TREE_RNN || cell == -1) return 1;
   return 0;
+}
+// bytes of the second staged tensor: c [N, H], or P [N, H, H] for MV-RNN
+static size_t second_staging_bytes(int32_t cell, int32_t N, int32_t H) {
+  return cell == CORTEX_MVRNN ? align_up((size_t)N * H * H * 8, 256) : staging_bytes(N, H);
 }
 static std::atomic<uint32_t> g_tag{0};
 
@@ -1735,7 +1864,7 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   const int staged = staged_tensors(cell == CELL_DAG ? -1 : cell);
   char *stage = (char *)d_ws + staging_offset();
   a.hs = staged >= 1 ? stage : nullptr;
-  a.cs = staged >= 2 ? stage + staging_bytes(lin->num_nodes, H) : nullptr;
+  a.cs = staged >= 2 ? stage + staging_bytes(lin->num_nodes, H) : nullptr;   // c, or P for MV-RNN
   a.tag = next_tag();
   set_last_grid(1, (int32_t)G);
   return launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
@@ -1763,7 +1892,9 @@ using namespace cortex;
 extern "C" size_t cortex_forward_workspace_bytes(int32_t cell, int32_t N, int32_t H) {
   if (N < 0 || H <= 0) return 0;
   if (cell < -1 || cell > CORTEX_MVRNN) return 0;
-  return cortex::staging_offset() + cortex::staged_tensors(cell) * cortex::staging_bytes(N, H);
+  const int staged = cortex::staged_tensors(cell);
+  return cortex::staging_offset() + (staged >= 1 ? cortex::staging_bytes(N, H) : 0) +
+         (staged >= 2 ? cortex::second_staging_bytes(cell, N, H) : 0);
 }
 
 extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,
