@@ -254,15 +254,6 @@ __device__ bool setup_structure(const FwdArgs &a, int *cache, Structure<kCached>
   return true;
 }
 
-// Input row of row r (cached, or through level_nodes and x_index).
-template <bool kCached>
-__device__ __forceinline__ int input_row_of(const FwdArgs &a, const Structure<kCached> &st, int r) {
-  if (kCached) return st.input_row(r);
-  const int v = a.level_nodes[r];
-  const int xi = a.x_index[v];
-  return (xi < -1 || xi >= a.x_rows) ? -1 : xi;
-}
-
 // Child rows and input rows of up to kChunkTiles of a workgroup's tiles in one
 // level (child-sum kernel), staged into LDS in one pass when the whole
 // linearization is not cached: operand addresses then never wait on a global
@@ -687,10 +678,9 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
         }
       }
       CORTEX_TRACE_WAVE(l);
-      // The next tile's loads complete here, before this tile's stores: no
-      // load is then pending behind a store, and the next tile starts with
-      // its operands in registers.
-      __builtin_amdgcn_s_waitcnt(kWaitVmcntZero);
+      // The next tile's loads stay in flight through this tile's epilogue
+      // (vector memory operations retire in order, so their first use
+      // waits for them alone).
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -1285,7 +1275,90 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
     int ce;
   };
 
-  for (int l = 0; l < L; ++l) {
+  // ---- level 0: a leaf has no child, so its cell is the node-input part
+  //      alone: c = i*u, h = o*tanh(c).  Each of LW waves takes H / LW input
+  //      columns, and the input rows of up to kLeafBatch of this group's leaf
+  //      tiles (u = group, group + Q, ...) are requested at once, so the
+  //      gathers from the input table share one memory round trip ----
+  {
+    constexpr int LW = (H / 16 < kFwdWaves) ? H / 16 : kFwdWaves;   // waves with input columns
+    constexpr int NBL = H / 16 / LW;                                 // 16-blocks per wave
+    constexpr int kLeafBatch = 8;
+    CORTEX_TRACE_POINT(0, 0);
+    const int lr1 = st.offset(L > 1 ? 1 : L);
+    if (lr1 < 0 || lr1 > N) {
+      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      return;
+    }
+    const int nt0 = (lr1 + kTileM - 1) / kTileM;
+    const int kcol = wave * 16 * NBL + 4 * g4;           // this lane's first input column
+    for (int ub = group; ub < nt0; ub += Q * kLeafBatch) {
+      u32x4 xl[kLeafBatch][NBL];
+#pragma unroll
+      for (int k = 0; k < kLeafBatch; ++k) {
+        const int row = (ub + k * Q) * kTileM + i16;
+        int xr = -1;
+        if (wave < LW && ub + k * Q < nt0 && row < lr1) {
+          if (kCached) {
+            xr = st.input_row(row);
+          } else {
+            const int v = a.level_nodes[row];
+            if (v < 0 || v >= N) {
+              raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+            } else {
+              xr = a.x_index[v];
+              if (xr < -1 || xr >= a.x_rows) {
+                raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+                xr = -1;
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < NBL; ++b)
+          xl[k][b] = xin.load4(xr >= 0 ? (uint32_t)((xr * H + kcol + 16 * b) * 4) : kNoSource);
+      }
+#pragma unroll
+      for (int k = 0; k < kLeafBatch; ++k) {
+        const int rowbase = (ub + k * Q) * kTileM;
+        if (rowbase >= lr1) break;
+        if (wave < LW) {
+          floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int b = 0; b < NBL; ++b)
+            acc = mfma_k16(as_float4(xl[k][b]), *(const float4 *)&W_s[i16 * LDW + kcol + 16 * b], acc);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) Ce[(wave * 16 + 4 * g4 + v) * 16 + i16] = acc[v];
+        }
+        __syncthreads();
+        if (tid < kTileM * 16) {           // gate row m = (gate i, o, u or f; unit)
+          const int i = tid >> 4, m = tid & 15;
+          float sum = bias_s[m];
+#pragma unroll
+          for (int w = 0; w < LW; ++w) sum += Ce[(w * 16 + i) * 16 + m];
+          Z_s[tid] = m / J == 2 ? tanh_f(sum) : sigmoidf(sum);
+        }
+        __syncthreads();
+        if (tid < kTileM * J) {
+          const int i = tid / J, j = tid % J, row = rowbase + i;
+          if (row < lr1) {
+            const float *z = &Z_s[i * 16];
+            const float cn = z[j] * z[2 * J + j];
+            const float hv = z[J + j] * tanh_f(cn);
+            const uint32_t el = (uint32_t)(row * H + hbase + j);
+            cs.store1(el, cn, tag);
+            hs.store1(el, hv, tag);
+            a.c[el] = cn;
+            a.h[el] = hv;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    CORTEX_TRACE_POINT(0, 5);
+  }
+
+  for (int l = 1; l < L; ++l) {
     CORTEX_TRACE_POINT(l, 0);
     const int r0 = st.offset(l), r1 = st.offset(l + 1);
     if (!kCached && (r1 < r0 || r1 > N || (l == 0 && r0 != 0))) {
@@ -1340,6 +1413,17 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
     };
 
     auto process = [&](int u, TileOps &t, bool more, TileOps &tn) __attribute__((always_inline)) {
+      // node-input part first: it needs no child
+      floatx4 xacc0 = {0.f, 0.f, 0.f, 0.f}, xacc1 = {0.f, 0.f, 0.f, 0.f};
+      if (wave < 4) {
+        const float *brow = &W_s[i16 * LDW + wave * KWX + 4 * g4];
+#pragma unroll
+        for (int b = 0; b < NBX; ++b) {
+          const float4 bv = *(const float4 *)(brow + 16 * b);
+          if (b & 1) xacc1 = mfma_k16(as_float4(t.xv[b]), bv, xacc1);
+          else xacc0 = mfma_k16(as_float4(t.xv[b]), bv, xacc0);
+        }
+      }
       CORTEX_TRACE_POINT(l, 1);
       if (!gave_up && !all_ready(t)) {
         const uint64_t t0 = wall_clock64();
@@ -1370,16 +1454,6 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
       }
       CORTEX_TRACE_POINT(l, 2);
       if (more) issue(u + Q, tn);
-      floatx4 xacc0 = {0.f, 0.f, 0.f, 0.f}, xacc1 = {0.f, 0.f, 0.f, 0.f};
-      if (wave < 4) {
-        const float *brow = &W_s[i16 * LDW + wave * KWX + 4 * g4];
-#pragma unroll
-        for (int b = 0; b < NBX; ++b) {
-          const float4 bv = *(const float4 *)(brow + 16 * b);
-          if (b & 1) xacc1 = mfma_k16(as_float4(t.xv[b]), bv, xacc1);
-          else xacc0 = mfma_k16(as_float4(t.xv[b]), bv, xacc0);
-        }
-      }
       floatx4 eacc0 = {0.f, 0.f, 0.f, 0.f}, eacc1 = {0.f, 0.f, 0.f, 0.f};
       if (__ballot(t.ecr >= 0) != 0) {      // skip edge tiles with no child at all (leaves)
         const float *brow = &W_s[i16 * LDW + H + ek];
@@ -1391,8 +1465,7 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
         }
       }
       CORTEX_TRACE_WAVE(l);
-      // the next tile's loads complete before this tile's stores
-      __builtin_amdgcn_s_waitcnt(kWaitVmcntZero);
+      // the next tile's loads stay in flight through this tile's epilogue
       if (wave < 4) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) Cx[(wave * 16 + 4 * g4 + v) * 16 + i16] = xacc0[v] + xacc1[v];
