@@ -134,6 +134,75 @@ def cpu_baseline(wl, seconds):
                       % (runs, wl.N, el)}
 
 
+# Cortex's own latencies on the paper's V100 GPU, in ms (the GPU rows of the
+# latency table comparing Cortex with DyNet, Sec. 7), keyed by (model,
+# hidden size h_s / h_l, batch).  Context for the grid below, never a target:
+# other hardware, and SST trees where this build uses SST-sized random ones.
+PAPER_V100_CORTEX_MS = {
+    ("treefc", "s", 1): 0.08, ("treefc", "s", 10): 0.17, ("treefc", "l", 1): 0.12, ("treefc", "l", 10): 0.37,
+    ("dagrnn", "s", 1): 0.22, ("dagrnn", "s", 10): 0.39, ("dagrnn", "l", 1): 0.26, ("dagrnn", "l", 10): 0.54,
+    ("treelstm", "s", 1): 0.24, ("treelstm", "s", 10): 0.39, ("treelstm", "l", 1): 0.29, ("treelstm", "l", 10): 0.70,
+    ("mvrnn", "s", 1): 0.34, ("mvrnn", "s", 10): 0.78, ("mvrnn", "l", 1): 0.39, ("mvrnn", "l", 10): 1.11,
+}
+
+
+def paper_grid(args):
+    """The paper's workload grid (models x batch {1, 10} x hidden {h_s, h_l});
+    one JSON line per cell: step latency on this GPU (same protocol as the
+    main bench), the forward kernel's roofline fraction, and the paper's V100
+    latency as context.  Cells whose hidden size the library does not
+    implement are reported as unsupported."""
+    import torch
+    from paper_2011_01383_amd import cortex as C
+    from paper_2011_01383_amd import inputs as I
+    from paper_2011_01383_amd.runner import DeviceWorkload
+    stream = torch.cuda.current_stream()
+    for cell in I.PAPER_GRID_CELLS:
+        for hidden in ("s", "l"):
+            for batch in (1, 10):
+                wl = I.paper_grid_workload(cell, batch, hidden)
+                line = {"grid_cell": cell, "hidden": wl.H, "hidden_class": "h_" + hidden, "batch": batch,
+                        "workload": wl.name, "nodes": wl.N,
+                        "paper_v100_cortex_ms": PAPER_V100_CORTEX_MS[(cell, hidden, batch)]}
+                try:
+                    dw = DeviceWorkload(wl)
+                    dw.step()
+                except RuntimeError as e:
+                    line.update({"supported": False, "reason": str(e)})
+                    print(json.dumps(line))
+                    continue
+                for _ in range(args.warmup):
+                    dw.step()
+                torch.cuda.synchronize()
+                assert dw.status_code() == 0
+                g0 = torch.cuda.Event(enable_timing=True)
+                g1 = torch.cuda.Event(enable_timing=True)
+                g0.record(stream)
+                for _ in range(args.steps):
+                    dw.step()
+                g1.record(stream)
+                torch.cuda.synchronize()
+                assert dw.status_code() == 0
+                ms = g0.elapsed_time(g1) / args.steps
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for _ in range(args.steps):
+                    dw.forward()
+                b.record(stream)
+                torch.cuda.synchronize()
+                fwd_ms = a.elapsed_time(b) / args.steps
+                flops, byts = algorithmic_work(wl)
+                bound = bound_of(flops, byts)
+                frac = (flops / (fwd_ms / 1e3) / 1e12 / PEAK_FP32_TFLOPS if bound == "mfma"
+                        else byts / (fwd_ms / 1e3) / 1e9 / PEAK_HBM_GBS)
+                line.update({"supported": True, "levels": int(dw.lin_host()["num_levels"]), "ms_per_step": ms,
+                             "nodes_per_s": wl.N / (ms / 1e3), "forward_ms": fwd_ms, "bound": bound,
+                             "roofline_frac": frac})
+                print(json.dumps(line))
+                sys.stdout.flush()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,6 +216,8 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB mebibytes (reads MIB, writes MIB) "
                          "five times, to scale HBM byte counters; prints one JSON line")
+    ap.add_argument("--paper-grid", action="store_true",
+                    help="run the paper's model x batch x hidden-size grid; one JSON line per cell")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -173,6 +244,9 @@ def main():
         from paper_2011_01383_amd import build
         build.build()
     torch.cuda.set_device(0)
+    if args.paper_grid:
+        paper_grid(args)
+        return
     wl = I.make_workload(args.workload)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, args.node_groups)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, args.slice_units)

@@ -202,8 +202,10 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *                                   forward (0 = the default of the cell;
  *                                   other values are used where the library
  *                                   has a kernel for them: 2 for the N-ary
- *                                   TreeLSTM at H = 256; 16 for the DAG-RNN
- *                                   at H = 256, whose default is 64)
+ *                                   TreeLSTM at H = 256; 16 or 64 for the
+ *                                   DAG-RNN at H = 256, whose default is 64
+ *                                   for batches of at least 12288 nodes and
+ *                                   16 below)
  * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value.
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0

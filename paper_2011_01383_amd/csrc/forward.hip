@@ -877,6 +877,7 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
 // budget walks the levels instead, staging each chunk of tiles' sources.
 // ---------------------------------------------------------------------------
 constexpr int kDagH = 256, kDagJ = 64, kDagS = kDagH / kDagJ;
+constexpr int kDagWideMinRows = 12288;             // default choice of this kernel (measured crossover)
 constexpr int kDagTileInts = 4 + kTileM * 3;        // level, level start, first row, level end, codes[16][3]
 constexpr int kDagTileCap = 240;                    // tiles per workgroup list (dynamic LDS)
 constexpr size_t kDagListBytes = (size_t)kDagTileCap * kDagTileInts * sizeof(int);
@@ -1840,7 +1841,11 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
     pick_slice<CORTEX_NARY_TREELSTM, 256, 2>(cached, out);
     return true;
   }
-  if (cell == CELL_DAG && H == kDagH && units != 16) {    // 16: the narrow-slice kernel
+  // DAG-RNN at H = 256: four 64-unit slices for large batches (operand
+  // re-reads dominate there), sixteen 16-unit slices for small ones (a
+  // tile's contraction is 4x shorter, and small levels are latency-bound);
+  // the knob forces either (16 or 64)
+  if (cell == CELL_DAG && H == kDagH && (units == 64 || (units != 16 && N >= kDagWideMinRows))) {
     out.fn = dag_slice64_kernel;
     out.J = kDagJ;
     out.threads = kFwdThreads;
@@ -1858,8 +1863,10 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   CORTEX_CASE(CORTEX_NARY_TREELSTM, 256)
   CORTEX_CASE(CORTEX_CHILDSUM_TREELSTM, 64)
   CORTEX_CASE(CORTEX_CHILDSUM_TREELSTM, 256)
+  CORTEX_CASE(CORTEX_TREE_RNN, 512)
   CORTEX_CASE(CELL_DAG, 64)
   CORTEX_CASE(CELL_DAG, 256)
+  CORTEX_CASE(CELL_DAG, 512)
 #undef CORTEX_CASE
   if (cell == CORTEX_MVRNN && H == kMvD) {
     out.fn = mvrnn_forward_kernel;

@@ -282,6 +282,46 @@ def dagrnn_workload(seed: int, n_grids: int = 64, rows: int = 32, cols: int = 32
                     children, x=x, W=W, U=U, b=b)
 
 
+def treefc_workload(seed: int, batch: int = 10, height: int = 7, H: int = 256) -> Workload:
+    """TreeFC (the paper's TF-Fold benchmarking model, Table "Models and
+    datasets"): ``batch`` perfect binary trees of height ``height`` (edges),
+    read as the TreeRNN cell h = tanh(W[h_l; h_r] + b) with leaf h = N(0,1)
+    rows; W, b ~ U(-0.05, 0.05)."""
+    rng = np.random.default_rng(seed)
+    children, is_leaf = forest_to_children([perfect_tree(height) for _ in range(batch)], 2)
+    N = is_leaf.size
+    n_leaf = int(is_leaf.sum())
+    x_index = np.full(N, -1, dtype=np.int32)
+    x_index[is_leaf] = np.arange(n_leaf, dtype=np.int32)
+    leaves = _n(rng, (n_leaf, H))
+    W = _u(rng, -0.05, 0.05, (H, 2 * H))
+    b = _u(rng, -0.05, 0.05, (H,))
+    return Workload("treefc_h%d_b%d" % (H, batch), CELL_TREE_RNN, H, 2, children,
+                    x_index=x_index, x_table=leaves, W=W, b=b)
+
+
+# The paper's evaluation grid (Sec. 7.1, Table "Models and datasets"; its
+# latency table lists batch sizes 1 and 10 and hidden sizes h_s / h_l =
+# 256 / 512, 64 / 128 for MV-RNN).  TreeGRU is not built.  SST-based models
+# use the SST-sized random trees of the five workloads above.
+PAPER_GRID_CELLS = ("treefc", "dagrnn", "treelstm", "mvrnn")
+
+
+def paper_grid_workload(cell: str, batch: int, hidden: str) -> Workload:
+    """One cell of the paper's grid; ``hidden`` is "s" or "l"."""
+    idx = PAPER_GRID_CELLS.index(cell) * 4 + (0 if batch == 1 else 1) * 2 + (0 if hidden == "s" else 1)
+    seed = BASE_SEED + 1000 + idx
+    if cell == "treefc":
+        return treefc_workload(seed, batch=batch, H=256 if hidden == "s" else 512)
+    if cell == "dagrnn":
+        return dagrnn_workload(seed, n_grids=batch, rows=10, cols=10, H=256 if hidden == "s" else 512)
+    if cell == "treelstm":
+        return childsum_treelstm_workload(seed, batch=batch, H=256 if hidden == "s" else 512)
+    if cell == "mvrnn":
+        return mvrnn_workload(seed, batch=batch, d=64 if hidden == "s" else 128)
+    raise ValueError(cell)
+
+
 # The five evaluation workloads, indexed 0..4.  Extra parity seeds for workload
 # k are BASE_SEED + 100*j + k + 1 (j = 1, 2, ...).
 WORKLOADS = {

@@ -201,16 +201,17 @@ def test_host_errors_enqueue_nothing():
     assert rc == C.CORTEX_E_TOO_LARGE
 
 
-@pytest.mark.parametrize("units,groups", [(0, 0), (0, 8), (0, 5), (16, 0), (16, 2)])
+@pytest.mark.parametrize("units,groups", [(64, 0), (64, 8), (64, 5), (16, 0), (16, 2), (0, 0)])
 def test_dag_slice_widths(units, groups):
-    """DAG-RNN at H = 256 under both slice widths (64 units, the default, and
-    16) and grids that do (multiples of 32 workgroups) and do not use the
-    XCD-grouped block order; each against the oracle."""
+    """DAG-RNN at H = 256 under both slice widths (64 and 16 units; 0 = the
+    size-based default, 16 units at this size) and grids that do (multiples
+    of 32 workgroups) and do not use the XCD-grouped block order; each
+    against the oracle."""
     wl = I.dagrnn_workload(77, n_grids=5, rows=13, cols=9, H=256)
     announce("dag slice units %d groups %d N=%d" % (units, groups, wl.N))
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
     dw = run(wl, groups)
-    S = 16 if units == 16 else 4
+    S = 4 if units == 64 else 16
     assert C.cortex_last_grid(1) == S * (groups if groups else 256 // S)
     compare_states(dw.states_by_node(), O.forward_workload(wl), "dag units %d" % units)
 
@@ -221,6 +222,7 @@ def test_dag_tile_list_overflow():
     chunk's sources instead; against the oracle."""
     wl = I.dagrnn_workload(78, n_grids=6, rows=32, cols=32, H=256)
     announce("dag tile-list overflow N=%d" % wl.N)
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 64)
     dw = run(wl, 1)
     assert C.cortex_last_grid(1) == 4
     compare_states(dw.states_by_node(), O.forward_workload(wl), "dag overflow")
