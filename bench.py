@@ -203,6 +203,57 @@ def paper_grid(args):
                 sys.stdout.flush()
 
 
+def ablation(args):
+    """How the forward orders its levels (CORTEX_KNOB_LEVEL_SYNC): per-datum
+    waits in one persistent launch (the default), plus a device-wide barrier
+    after every level, or one launch per level that reloads weights and
+    structure each time.  One JSON line per (workload, mode): the forward
+    kernel time (for mode 2, the whole per-level launch sequence, which also
+    synchronizes once to read L)."""
+    import torch
+    from paper_2011_01383_amd import cortex as C
+    from paper_2011_01383_amd import inputs as I
+    from paper_2011_01383_amd.runner import DeviceWorkload
+    stream = torch.cuda.current_stream()
+    names = {0: "per-datum waits, one launch", 1: "plus a device-wide barrier per level",
+             2: "one launch per level"}
+    for k, units in ((1, 0), (2, 0), (4, 64)):
+        wl = I.make_workload(k)
+        C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
+        for mode in (0, 1, 2):
+            C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)
+            line = {"workload": wl.name, "level_sync": mode, "mode": names[mode]}
+            dw = DeviceWorkload(wl)
+            dw.linearize()
+            try:
+                dw.forward()
+            except RuntimeError as e:
+                line.update({"supported": False, "reason": str(e)})
+                print(json.dumps(line))
+                continue
+            for _ in range(args.warmup):
+                dw.forward()
+            torch.cuda.synchronize()
+            assert dw.status_code() == 0
+            n = max(10, min(args.steps, 100))
+            t0 = time.perf_counter()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(n):
+                dw.forward()
+            b.record(stream)
+            torch.cuda.synchronize()
+            assert dw.status_code() == 0
+            line.update({"supported": True, "forward_ms": a.elapsed_time(b) / n,
+                         "host_wall_ms": (time.perf_counter() - t0) / n * 1e3,
+                         "levels": int(dw.lin_host()["num_levels"]), "grid": C.cortex_last_grid(1)})
+            print(json.dumps(line))
+            sys.stdout.flush()
+        C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 0)
+        C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -218,6 +269,8 @@ def main():
                          "five times, to scale HBM byte counters; prints one JSON line")
     ap.add_argument("--paper-grid", action="store_true",
                     help="run the paper's model x batch x hidden-size grid; one JSON line per cell")
+    ap.add_argument("--ablation", action="store_true",
+                    help="forward time under each level-ordering mode; one JSON line per (workload, mode)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -246,6 +299,9 @@ def main():
     torch.cuda.set_device(0)
     if args.paper_grid:
         paper_grid(args)
+        return
+    if args.ablation:
+        ablation(args)
         return
     wl = I.make_workload(args.workload)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, args.node_groups)

@@ -206,13 +206,26 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *                                   DAG-RNN at H = 256, whose default is 64
  *                                   for batches of at least 12288 nodes and
  *                                   16 below)
- * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value.
+ *   CORTEX_KNOB_LEVEL_SYNC          how the forward orders its levels, for
+ *                                   ablation studies (the results are the same):
+ *                                   0 = per-datum waits in one launch (default);
+ *                                   1 = also a device-wide barrier after every
+ *                                   level (slice and child-sum kernels);
+ *                                   2 = one launch per level, each reloading
+ *                                   weights and structure (slice, child-sum
+ *                                   and 64-unit DAG-RNN kernels; the call then
+ *                                   synchronizes the stream once to read L).
+ *                                   A forward whose kernel lacks the mode
+ *                                   returns CORTEX_E_INVAL.
+ * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value
+ * (or a LEVEL_SYNC value above 2).
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0
 #define CORTEX_KNOB_FWD_NODE_GROUPS 1
 #define CORTEX_KNOB_BARRIER_TIMEOUT_US 2
 #define CORTEX_KNOB_COOPERATIVE 3
 #define CORTEX_KNOB_FWD_SLICE_UNITS 4
+#define CORTEX_KNOB_LEVEL_SYNC 5
 int cortex_set_knob(int32_t knob, int64_t value);
 int64_t cortex_get_knob(int32_t knob);
 

@@ -85,6 +85,8 @@ struct FwdArgs {
   uint64_t *trace;
   uint32_t tag;                 // this launch's staging tag
   void *hs, *cs;                // tagged staging of h and c (workspace)
+  int32_t level_lo, level_hi;   // levels this launch runs (all of them unless one launch per level)
+  int32_t level_barrier;        // 1: a device-wide barrier closes every level (instead of per-datum waits alone)
 };
 
 // ---------------------------------------------------------------------------
@@ -551,7 +553,7 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   const int off1 = off[1];
   int gave_up = 0;
 
-  for (int l = 0; l < L; ++l) {
+  for (int l = a.level_lo; l < L && l < a.level_hi; ++l) {
     CORTEX_TRACE_POINT(l, 0);
     const int r0 = off[l], r1 = off[l + 1];
     if (!kCached && (r1 < r0 || r1 > N || (l == 0 && r0 != 0))) {
@@ -754,6 +756,7 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
     }
     CORTEX_TRACE_POINT(l, 5);
     if (__syncthreads_or(gave_up)) return;
+    if (a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
   }
   CORTEX_TRACE_KERNEL(3);
 }
@@ -989,7 +992,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       r1 = a.level_offsets[l + 1];
       const bool ok = r0 >= 0 && r1 >= r0 && r1 <= N && (l != 0 || r0 == 0) && (l != L - 1 || r1 == N);
       if (!ok) bad = 1;
-      const int ntile = ok ? (r1 - r0 + kTileM - 1) / kTileM : 0;
+      const int ntile = (ok && l >= a.level_lo && l < a.level_hi) ? (r1 - r0 + kTileM - 1) / kTileM : 0;
       uf = ((group - l) % Q + Q) % Q;
       cnt = uf < ntile ? (ntile - 1 - uf) / Q + 1 : 0;
     }
@@ -1190,7 +1193,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   } else {
     // the list does not fit: walk the levels, staging each chunk of tiles' sources
     const int *off = a.level_offsets;
-    for (int l = 0; l < L; ++l) {
+    for (int l = a.level_lo; l < L && l < a.level_hi; ++l) {
       CORTEX_TRACE_POINT(l, 0);
       const int r0 = off[l], r1 = off[l + 1];
       const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
@@ -1281,7 +1284,7 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
   //      columns, and the input rows of up to kLeafBatch of this group's leaf
   //      tiles (u = group, group + Q, ...) are requested at once, so the
   //      gathers from the input table share one memory round trip ----
-  {
+  if (a.level_lo == 0) {
     constexpr int LW = (H / 16 < kFwdWaves) ? H / 16 : kFwdWaves;   // waves with input columns
     constexpr int NBL = H / 16 / LW;                                 // 16-blocks per wave
     constexpr int kLeafBatch = 8;
@@ -1357,9 +1360,11 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
       }
     }
     CORTEX_TRACE_POINT(0, 5);
+    if (L > 1 && a.level_hi > 1 && a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout))
+      return;
   }
 
-  for (int l = 1; l < L; ++l) {
+  for (int l = a.level_lo > 1 ? a.level_lo : 1; l < L && l < a.level_hi; ++l) {
     CORTEX_TRACE_POINT(l, 0);
     const int r0 = st.offset(l), r1 = st.offset(l + 1);
     if (!kCached && (r1 < r0 || r1 > N || (l == 0 && r0 != 0))) {
@@ -1535,6 +1540,7 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
     }
     CORTEX_TRACE_POINT(l, 5);
     if (__syncthreads_or(gave_up)) return;
+    if (a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
   }
   CORTEX_TRACE_KERNEL(3);
 }
@@ -1804,6 +1810,8 @@ struct Instance {
   int J;
   int threads;
   size_t lds = SIZE_MAX;        // dynamic LDS the kernel sizes itself (SIZE_MAX: the structure cache)
+  bool level_barrier_ok = false;   // honours FwdArgs.level_barrier
+  bool level_range_ok = false;     // honours FwdArgs.level_lo / level_hi
 };
 
 constexpr size_t kStructCacheBudget = 40 * 1024;    // bytes of LDS for the cached linearization
@@ -1821,6 +1829,7 @@ template <int CELL, int H, int J>
 static void pick_slice(bool cached, Instance &out) {
   out.J = J;
   out.threads = kFwdThreads;
+  out.level_barrier_ok = out.level_range_ok = true;
   if constexpr (CELL == CORTEX_CHILDSUM_TREELSTM)
     out.fn = cached ? childsum_forward_kernel<H, true> : childsum_forward_kernel<H, false>;
   else
@@ -1850,6 +1859,7 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
     out.J = kDagJ;
     out.threads = kFwdThreads;
     out.lds = kDagListBytes;
+    out.level_range_ok = true;
     return true;
   }
 #define CORTEX_CASE(CELLID, HH)                                      \
@@ -1946,8 +1956,29 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   a.hs = staged >= 1 ? stage : nullptr;
   a.cs = staged >= 2 ? stage + staging_bytes(lin->num_nodes, H) : nullptr;   // c, or P for MV-RNN
   a.tag = next_tag();
+  a.level_lo = 0;
+  a.level_hi = 0x7fffffff;
+  a.level_barrier = 0;
+  const int64_t sync_mode = knob(CORTEX_KNOB_LEVEL_SYNC);
+  if ((sync_mode == 1 && !inst.level_barrier_ok) || (sync_mode == 2 && !inst.level_range_ok)) return CORTEX_E_INVAL;
   set_last_grid(1, (int32_t)G);
-  return launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
+  if (sync_mode == 1) a.level_barrier = 1;
+  if (sync_mode != 2) return launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
+  // one launch per level (ablation): L is read back first; every launch
+  // reloads weights and structure and keeps the launch tag, so a level
+  // reads what the previous launches staged
+  int32_t L = 0;
+  if (hipMemcpyAsync(&L, lin->num_levels, sizeof(L), hipMemcpyDeviceToHost, (hipStream_t)stream) != hipSuccess ||
+      hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
+    return CORTEX_E_HIP;
+  if (L < 1 || L > lin->num_nodes) L = 1;          // the kernel itself reports a broken linearization
+  for (int32_t l = 0; l < L; ++l) {
+    a.level_lo = l;
+    a.level_hi = l + 1;
+    const int rc = launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
+    if (rc != CORTEX_OK) return rc;
+  }
+  return CORTEX_OK;
 }
 
 static void fill_lin(FwdArgs &a, const cortex_lin_t *lin) {

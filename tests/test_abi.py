@@ -76,3 +76,12 @@ def test_knobs(lib):
     assert C.cortex_set_knob(99, 1) == C.CORTEX_E_INVAL
     assert C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, -1) == C.CORTEX_E_INVAL
     assert C.cortex_get_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US) > 0
+
+
+def test_level_sync_knob_range(lib):
+    assert C.cortex_get_knob(C.CORTEX_KNOB_LEVEL_SYNC) == 0
+    assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 3) == C.CORTEX_E_INVAL
+    for v in (2, 1, 0):
+        assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, v) == C.CORTEX_OK
+        assert C.cortex_get_knob(C.CORTEX_KNOB_LEVEL_SYNC) == v
+    assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC + 1, 0) == C.CORTEX_E_INVAL

@@ -23,6 +23,7 @@ def _gpu():
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, 0)
     C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, 0)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
+    C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 0)
 
 
 def run(wl, groups=0):
@@ -238,3 +239,50 @@ def test_tree_rnn_h64_lds_limit(n_leaves):
     dw = run(wl)
     assert C.cortex_last_grid(1) == 1
     compare_states(dw.states_by_node(), O.forward_workload(wl), "tree_rnn %d leaves" % n_leaves)
+
+
+LEVEL_SYNC_CASES = {
+    "nary": (lambda: cached_workload(1, 0), 0),
+    "childsum": (lambda: cached_workload(2, 0), 0),
+    "tree_rnn_h256": (lambda: I.tree_rnn_workload(41, n_leaves=37, H=256), 0),
+    "dag_h256_units16": (lambda: I.dagrnn_workload(42, n_grids=3, rows=9, cols=7, H=256), 16),
+    "dag_h256_units64": (lambda: I.dagrnn_workload(43, n_grids=3, rows=9, cols=7, H=256), 64),
+}
+
+
+@pytest.mark.parametrize("name", sorted(LEVEL_SYNC_CASES))
+@pytest.mark.parametrize("mode", [1, 2])
+def test_level_sync_modes_change_only_the_schedule(name, mode):
+    """The ablation modes (a device-wide barrier after every level; one
+    launch per level) run the same arithmetic in the same order as the
+    default per-datum waits, so the states are bitwise identical; a kernel
+    without the mode rejects it on the host."""
+    make, units = LEVEL_SYNC_CASES[name]
+    wl = make()
+    announce("level sync mode %d %s N=%d" % (mode, name, wl.N))
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
+    ref = run(wl).states_by_node()
+    C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)
+    if name == "dag_h256_units64" and mode == 1:
+        dw = DeviceWorkload(wl)
+        dw.linearize()
+        with pytest.raises(RuntimeError, match="host code %d" % C.CORTEX_E_INVAL):
+            dw.forward()
+        return
+    got = run(wl).states_by_node()
+    for key in ref:
+        assert np.array_equal(ref[key], got[key]), key
+
+
+@pytest.mark.parametrize("k", [0, 3])
+@pytest.mark.parametrize("mode", [1, 2])
+def test_level_sync_modes_unsupported(k, mode):
+    """TreeRNN H = 64 (states in LDS) and MV-RNN have no ablation modes."""
+    wl = cached_workload(k, 0)
+    announce("level sync mode %d unsupported on workload %d" % (mode, k))
+    C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)
+    dw = DeviceWorkload(wl)
+    dw.linearize()
+    with pytest.raises(RuntimeError, match="host code %d" % C.CORTEX_E_INVAL):
+        dw.forward()
+    assert dw.status_code() == 0
