@@ -39,6 +39,12 @@ published forms are used, see the readings listed with the design notes):
                      c = i*u + sum_k f_k*c_k, h = o*tanh(c); x at every node
 * mvrnn              p = tanh(W [B a; A b]), P = W_M [A; B]; leaf (a, A)
 * dagrnn             h = tanh(W x + U_up h_up + U_left h_left + b)
+* childsum_treegru   h~ = sum_k h_k; z = sig(W_z x + U_z h~ + b_z); one reset
+                     gate per child r_k = sig(W_r x + U_r h_k + b_r);
+                     h' = tanh(W_h x + U_h sum_k r_k*h_k + b_h);
+                     h = z*h~ + (1-z)*h'; x at every node
+* simple_treegru     the same with h = (1-z)*h' (the simplification the
+                     paper describes for its refactoring study, Sec. 7.3)
 
 Every function here is pinned by ``tests/test_oracle_*.py`` against hand
 values, library cells (torch RNNCell/LSTMCell in fp64), closed forms and the
@@ -286,6 +292,22 @@ def cell_apply(p: _Params, v: int, kids: Sequence[Optional[tuple]]):
         x = p.input_row(v)
         hu, hl = full[0][0], full[1][0]
         return (np.tanh(p.W @ x + p.U[0] @ hu + p.U[1] @ hl + p.b),)
+
+    if p.cell in ("childsum_treegru", "simple_treegru"):
+        x = p.input_row(v)
+        Wz, Wr, Wh = p.W
+        Uz, Ur, Uh = p.U
+        bz, br, bh = p.b
+        hsum = np.zeros(H)
+        reset_sum = np.zeros(H)                  # sum over children of r_k * h_k
+        for (hk,) in present:
+            hsum = hsum + hk
+            reset_sum = reset_sum + sigmoid(Wr @ x + Ur @ hk + br) * hk
+        z = sigmoid(Wz @ x + Uz @ hsum + bz)
+        cand = np.tanh(Wh @ x + Uh @ reset_sum + bh)
+        if p.cell == "simple_treegru":
+            return ((1.0 - z) * cand,)
+        return (z * hsum + (1.0 - z) * cand,)
 
     raise ValueError("unknown cell %r" % p.cell)
 

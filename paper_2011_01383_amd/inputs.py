@@ -38,6 +38,8 @@ CELL_NARY_TREELSTM = "nary_treelstm"
 CELL_CHILDSUM_TREELSTM = "childsum_treelstm"
 CELL_MVRNN = "mvrnn"
 CELL_DAGRNN = "dagrnn"
+CELL_CHILDSUM_TREEGRU = "childsum_treegru"
+CELL_SIMPLE_TREEGRU = "simple_treegru"
 
 
 @dataclass
@@ -251,6 +253,27 @@ def childsum_treelstm_workload(seed: int, batch: int = 10, H: int = 256, vocab: 
                     max_arity, children, x_index=x_index, x_table=emb, W=W, U=U, b=b)
 
 
+def childsum_treegru_workload(seed: int, batch: int = 10, H: int = 256, vocab: int = 1000,
+                              node_lo: int = 20, node_hi: int = 80, max_arity: int = 4,
+                              simple: bool = False) -> Workload:
+    """Child-sum TreeGRU (or SimpleTreeGRU) over random-arity trees, the same
+    shapes as the child-sum TreeLSTM; every node reads Emb[id]; weights
+    W, U [3, H, H] and b [3, H] (gates z, r, h) ~ U(-0.05, 0.05)."""
+    rng = np.random.default_rng(seed)
+    sizes = [int(rng.integers(node_lo, node_hi + 1)) for _ in range(batch)]
+    trees = [random_arity_tree(rng, s, max_arity) for s in sizes]
+    children, is_leaf = forest_to_children(trees, max_arity)
+    N = is_leaf.size
+    x_index = rng.integers(0, vocab, size=N).astype(np.int32)
+    emb = _n(rng, (vocab, H))
+    W = _u(rng, -0.05, 0.05, (3, H, H))
+    U = _u(rng, -0.05, 0.05, (3, H, H))
+    b = _u(rng, -0.05, 0.05, (3, H))
+    cell = CELL_SIMPLE_TREEGRU if simple else CELL_CHILDSUM_TREEGRU
+    name = ("simple_treegru_h%d_b%d" if simple else "childsum_treegru_h%d_b%d") % (H, batch)
+    return Workload(name, cell, H, max_arity, children, x_index=x_index, x_table=emb, W=W, U=U, b=b)
+
+
 def mvrnn_workload(seed: int, batch: int = 10, d: int = 64, leaf_lo: int = 10,
                    leaf_hi: int = 40, wm_scale: float = 0.1) -> Workload:
     """MV-RNN: leaf (a, A) = (N(0,1), I + 0.01 N(0,1)); p = tanh(W[Ba; Ab]), P = W_M[A; B]."""
@@ -302,9 +325,9 @@ def treefc_workload(seed: int, batch: int = 10, height: int = 7, H: int = 256) -
 
 # The paper's evaluation grid (Sec. 7.1, Table "Models and datasets"; its
 # latency table lists batch sizes 1 and 10 and hidden sizes h_s / h_l =
-# 256 / 512, 64 / 128 for MV-RNN).  TreeGRU is not built.  SST-based models
-# use the SST-sized random trees of the five workloads above.
-PAPER_GRID_CELLS = ("treefc", "dagrnn", "treelstm", "mvrnn")
+# 256 / 512, 64 / 128 for MV-RNN).  SST-based models (TreeGRU, TreeLSTM,
+# MV-RNN) use the SST-sized random trees of the five workloads above.
+PAPER_GRID_CELLS = ("treefc", "dagrnn", "treegru", "treelstm", "mvrnn")
 
 
 def paper_grid_workload(cell: str, batch: int, hidden: str) -> Workload:
@@ -317,6 +340,8 @@ def paper_grid_workload(cell: str, batch: int, hidden: str) -> Workload:
         return dagrnn_workload(seed, n_grids=batch, rows=10, cols=10, H=256 if hidden == "s" else 512)
     if cell == "treelstm":
         return childsum_treelstm_workload(seed, batch=batch, H=256 if hidden == "s" else 512)
+    if cell == "treegru":
+        return childsum_treegru_workload(seed, batch=batch, H=256 if hidden == "s" else 512)
     if cell == "mvrnn":
         return mvrnn_workload(seed, batch=batch, d=64 if hidden == "s" else 128)
     raise ValueError(cell)

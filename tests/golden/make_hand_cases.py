@@ -93,6 +93,50 @@ cases["dagrnn_2x2_h1"] = {
     "expect": {"h": {"0": h00, "1": h01, "2": h10, "3": h11}},
 }
 
+# child-sum TreeGRU and SimpleTreeGRU, two leaves under a root, H = 1.
+# W = (W_z, W_r, W_h) = (0, .25, 1), U = (U_z, U_r, U_h) = (.5, 1, .5), b = 0.
+# Emb = [1, 2, -1]; leaves x = 2, -1; root x = 1.
+# leaf k (no child): z = sig(0) = 1/2, h' = tanh(x_k), h_k = tanh(x_k)/2 (both variants)
+# root: z = sig(.5 (h1 + h2)); r_k = sig(.25 + h_k); m = r_1 h1 + r_2 h2;
+#       h' = tanh(1 + .5 m); TreeGRU h = z (h1 + h2) + (1 - z) h';  Simple h = (1 - z) h'
+g1, g2 = 0.5 * math.tanh(2.0), 0.5 * math.tanh(-1.0)
+gz = sig(0.5 * (g1 + g2))
+gm = sig(0.25 + g1) * g1 + sig(0.25 + g2) * g2
+gcand = math.tanh(1.0 + 0.5 * gm)
+gru_inputs = {"x_index": [1, 2, 0], "x_table": [[1.0], [2.0], [-1.0]],
+              "W": [[[0.0]], [[0.25]], [[1.0]]], "U": [[[0.5]], [[1.0]], [[0.5]]], "b": [[0.0]] * 3}
+gru_children = [-1, -1, -1, -1, -1, -1, -1, -1, 0, 1, -1, -1]
+cases["childsum_treegru_two_children_h1"] = {
+    "cell": "childsum_treegru", "K": 4, "H": 1, "children": gru_children, "inputs": gru_inputs,
+    "derivation": "h = z(h1+h2) + (1-z) tanh(1 + .5(r1 h1 + r2 h2)), r_k = sig(.25 + h_k); "
+                  "one reset gate on h~ would give sig(.25 + h~) h~ inside the tanh",
+    "expect": {"h": {"0": g1, "1": g2, "2": gz * (g1 + g2) + (1.0 - gz) * gcand}},
+}
+cases["simple_treegru_two_children_h1"] = {
+    "cell": "simple_treegru", "K": 4, "H": 1, "children": gru_children, "inputs": gru_inputs,
+    "derivation": "h = (1-z) tanh(1 + .5(r1 h1 + r2 h2)); leaves as in the TreeGRU case",
+    "expect": {"h": {"0": g1, "1": g2, "2": (1.0 - gz) * gcand}},
+}
+
+# child-sum TreeGRU, H = 2, one leaf under a root: where the reset gate sits.
+# W = (W_z, W_r, W_h) = (0, 0, I), U = (U_z, U_r, U_h) = (0, 0, [[0, 1], [1, 0]]),
+# b = (0, (1, -2), 0).  Leaf x = (1, -.5): z = 1/2, h_c = tanh(x)/2.  Root x = 0:
+# h~ = h_c, z = 1/2, r = (sig(1), sig(-2)), m = r * h_c, h' = tanh(U_h m) =
+# (tanh(r_1 h_c1), tanh(r_0 h_c0)); h = h_c/2 + h'/2.  A reset applied after U_h
+# (r * (U_h h_c)) would give (tanh(r_0 h_c1), tanh(r_1 h_c0)) instead.
+hc0, hc1 = 0.5 * math.tanh(1.0), 0.5 * math.tanh(-0.5)
+r0, r1 = sig(1.0), sig(-2.0)
+cases["childsum_treegru_reset_placement_h2"] = {
+    "cell": "childsum_treegru", "K": 4, "H": 2, "children": [-1, -1, -1, -1, 0, -1, -1, -1],
+    "inputs": {"x_index": [1, 0], "x_table": [[0.0, 0.0], [1.0, -0.5]],
+               "W": [[[0.0, 0.0], [0.0, 0.0]], [[0.0, 0.0], [0.0, 0.0]], [[1.0, 0.0], [0.0, 1.0]]],
+               "U": [[[0.0, 0.0], [0.0, 0.0]], [[0.0, 0.0], [0.0, 0.0]], [[0.0, 1.0], [1.0, 0.0]]],
+               "b": [[0.0, 0.0], [1.0, -2.0], [0.0, 0.0]]},
+    "derivation": "h' = tanh(U_h (r * h_c)) with U_h the swap: (tanh(r1 hc1), tanh(r0 hc0)); h = hc/2 + h'/2",
+    "expect": {"h": {"0": [hc0, hc1],
+                     "1": [0.5 * hc0 + 0.5 * math.tanh(r1 * hc1), 0.5 * hc1 + 0.5 * math.tanh(r0 * hc0)]}},
+}
+
 out = os.path.join(os.path.dirname(os.path.abspath(__file__)), "hand_cases.json")
 with open(out, "w") as f:
     json.dump(cases, f, indent=1, sort_keys=True)

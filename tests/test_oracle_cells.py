@@ -145,7 +145,9 @@ def _case_arrays(case):
 
 
 @pytest.mark.parametrize("name", ["tree_rnn_h1", "nary_treelstm_h1", "childsum_leaf_h1",
-                                  "childsum_two_children_h1", "mvrnn_h1", "dagrnn_2x2_h1"])
+                                  "childsum_two_children_h1", "mvrnn_h1", "dagrnn_2x2_h1",
+                                  "childsum_treegru_two_children_h1", "simple_treegru_two_children_h1",
+                                  "childsum_treegru_reset_placement_h2"])
 def test_hand_cases(name):
     case = load_hand()[name]
     children, arrays = _case_arrays(case)
@@ -380,6 +382,105 @@ def test_dagrnn_zero_input_is_zero():
 
 
 # ---------------------------------------------------------------------------
+# Child-sum TreeGRU and SimpleTreeGRU
+# ---------------------------------------------------------------------------
+
+def _gru_params(rng, H, reset_one=False, update_zero=False):
+    """W, U [3, H, H], b [3, H] for gates (z, r, h).  reset_one: W_r = U_r = 0
+    and b_r = 40, so r = 1 exactly in float64; update_zero: W_z = U_z = 0 and
+    b_z = -40, so 1 - z = 1 exactly."""
+    W = rng.uniform(-0.5, 0.5, (3, H, H)).astype(np.float32)
+    U = rng.uniform(-0.5, 0.5, (3, H, H)).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, (3, H)).astype(np.float32)
+    if reset_one:
+        W[1] = 0
+        U[1] = 0
+        b[1] = 40.0
+    if update_zero:
+        W[0] = 0
+        U[0] = 0
+        b[0] = -40.0
+    return W, U, b
+
+
+def _chain4(rng, N):
+    children = np.full(N * 4, -1, dtype=np.int32)
+    for v in range(1, N):
+        children[v * 4 + int(rng.integers(0, 4))] = v - 1     # any slot
+    return children
+
+
+def test_childsum_treegru_arity1_chain_is_grucell():
+    """With r = 1 the candidate is tanh(W_h x + U_h h + b_h) whichever side of
+    U_h the reset sits, so an arity-1 chain is torch.nn.GRUCell (gate order r,
+    z, n; bias_hh = 0) run from h = 0."""
+    rng = np.random.default_rng(21)
+    H, N = 5, 9
+    children = _chain4(rng, N)
+    emb = rng.standard_normal((20, H)).astype(np.float32)
+    x_index = rng.integers(0, 20, N).astype(np.int32)
+    W, U, b = _gru_params(rng, H, reset_one=True)
+    out = O.forward("childsum_treegru", children, 4, H, x_index=x_index, x_table=emb, W=W, U=U, b=b)
+    cell = torch.nn.GRUCell(H, H).to(F64)
+    with torch.no_grad():
+        cell.weight_ih.copy_(torch.from_numpy(np.concatenate([W[1], W[0], W[2]])).to(F64))
+        cell.weight_hh.copy_(torch.from_numpy(np.concatenate([U[1], U[0], U[2]])).to(F64))
+        cell.bias_ih.copy_(torch.from_numpy(np.concatenate([b[1], b[0], b[2]])).to(F64))
+        cell.bias_hh.zero_()
+    h = torch.zeros(1, H, dtype=F64)
+    for v in range(N):
+        h = cell(torch.from_numpy(emb[x_index[v]]).to(F64)[None], h)
+        np.testing.assert_allclose(out["h"][v], h[0].detach().numpy(), rtol=0, atol=1e-13)
+
+
+def test_simple_treegru_arity1_chain_is_rnncell():
+    """With r = 1 and 1 - z = 1, SimpleTreeGRU's h = (1 - z) h' is
+    tanh(W_h x + U_h h + b_h): an Elman chain, torch.nn.RNNCell(tanh)."""
+    rng = np.random.default_rng(22)
+    H, N = 5, 9
+    children = _chain4(rng, N)
+    emb = rng.standard_normal((20, H)).astype(np.float32)
+    x_index = rng.integers(0, 20, N).astype(np.int32)
+    W, U, b = _gru_params(rng, H, reset_one=True, update_zero=True)
+    out = O.forward("simple_treegru", children, 4, H, x_index=x_index, x_table=emb, W=W, U=U, b=b)
+    cell = torch.nn.RNNCell(H, H, nonlinearity="tanh").to(F64)
+    with torch.no_grad():
+        cell.weight_ih.copy_(torch.from_numpy(W[2]).to(F64))
+        cell.weight_hh.copy_(torch.from_numpy(U[2]).to(F64))
+        cell.bias_ih.copy_(torch.from_numpy(b[2]).to(F64))
+        cell.bias_hh.zero_()
+    h = torch.zeros(1, H, dtype=F64)
+    for v in range(N):
+        h = cell(torch.from_numpy(emb[x_index[v]]).to(F64)[None], h)
+        np.testing.assert_allclose(out["h"][v], h[0].detach().numpy(), rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("k", [2, 3, 4])
+def test_childsum_treegru_duplicate_children_is_grucell_from_summed_state(k):
+    """k copies of one child h (with r = 1): h~ = k h and sum_k r h_k = k h,
+    so the node is one GRUCell step from the state k h.  This pins h~ as the
+    plain sum of the children in both the update gate and z * h~."""
+    rng = np.random.default_rng(30 + k)
+    H = 4
+    children = np.full(3 * 4, -1, dtype=np.int32)
+    children[1 * 4 + 0] = 0
+    for s in range(k):
+        children[2 * 4 + s] = 1
+    emb = rng.standard_normal((3, H)).astype(np.float32)
+    x_index = np.array([0, 1, 2], dtype=np.int32)
+    W, U, b = _gru_params(rng, H, reset_one=True)
+    out = O.forward("childsum_treegru", children, 4, H, x_index=x_index, x_table=emb, W=W, U=U, b=b)
+    cell = torch.nn.GRUCell(H, H).to(F64)
+    with torch.no_grad():
+        cell.weight_ih.copy_(torch.from_numpy(np.concatenate([W[1], W[0], W[2]])).to(F64))
+        cell.weight_hh.copy_(torch.from_numpy(np.concatenate([U[1], U[0], U[2]])).to(F64))
+        cell.bias_ih.copy_(torch.from_numpy(np.concatenate([b[1], b[0], b[2]])).to(F64))
+        cell.bias_hh.zero_()
+    h = cell(torch.from_numpy(emb[2]).to(F64)[None], k * torch.from_numpy(out["h"][1])[None])
+    np.testing.assert_allclose(out["h"][2], h[0].detach().numpy(), rtol=0, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
 # Order invariance and brute force
 # ---------------------------------------------------------------------------
 
@@ -407,6 +508,10 @@ def _random_topo_order(children, K, rng):
 
 
 def _small(k):
+    if k == 5:
+        return I.childsum_treegru_workload(1005, batch=3, H=8, vocab=20, node_lo=3, node_hi=12)
+    if k == 6:
+        return I.childsum_treegru_workload(1006, batch=3, H=8, vocab=20, node_lo=3, node_hi=12, simple=True)
     if k == 0:
         return I.tree_rnn_workload(1000, n_leaves=9, H=8)
     if k == 1:
@@ -418,7 +523,7 @@ def _small(k):
     return I.dagrnn_workload(1004, n_grids=2, rows=4, cols=5, H=8)
 
 
-@pytest.mark.parametrize("k", range(5))
+@pytest.mark.parametrize("k", range(7))
 def test_order_invariance_bitwise(k):
     wl = _small(k)
     rng = np.random.default_rng(9)
@@ -434,7 +539,7 @@ def test_order_invariance_bitwise(k):
             np.testing.assert_array_equal(out[key], ref[key])
 
 
-@pytest.mark.parametrize("k", range(5))
+@pytest.mark.parametrize("k", range(7))
 def test_relabel_invariance_bitwise(k):
     wl = _small(k)
     rng = np.random.default_rng(10)
