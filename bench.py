@@ -57,6 +57,11 @@ def algorithmic_work(wl):
     elif wl.cell == "childsum_treelstm":
         flops = N * (2 * H * 4 * H + 4 * H) + n_int * 2 * H * 3 * H + E * 2 * H * H
         byts = (8 * H * H + 4 * H) * f4 + N * H * f4 + 2 * N * H * f4 + struct_bytes
+    elif wl.cell in ("childsum_treegru", "simple_treegru"):
+        # per node: W x for 3 gates + bias; per internal node: U_z h~, U_h m;
+        # per child edge: U_r h_k
+        flops = N * (2 * H * 3 * H + 3 * H) + n_int * 2 * (2 * H * H) + E * 2 * H * H
+        byts = (6 * H * H + 3 * H) * f4 + N * H * f4 + N * H * f4 + struct_bytes
     elif wl.cell == "mvrnn":
         flops = n_int * (2 * H * 2 * H * H + 2 * 2 * H * H + 2 * H * 2 * H)
         byts = (2 * H * 2 * H) * f4 + n_leaf * (H * H + H) * f4 + N * (H * H + H) * f4 + struct_bytes
@@ -141,6 +146,7 @@ def cpu_baseline(wl, seconds):
 PAPER_V100_CORTEX_MS = {
     ("treefc", "s", 1): 0.08, ("treefc", "s", 10): 0.17, ("treefc", "l", 1): 0.12, ("treefc", "l", 10): 0.37,
     ("dagrnn", "s", 1): 0.22, ("dagrnn", "s", 10): 0.39, ("dagrnn", "l", 1): 0.26, ("dagrnn", "l", 10): 0.54,
+    ("treegru", "s", 1): 0.18, ("treegru", "s", 10): 0.35, ("treegru", "l", 1): 0.25, ("treegru", "l", 10): 0.75,
     ("treelstm", "s", 1): 0.24, ("treelstm", "s", 10): 0.39, ("treelstm", "l", 1): 0.29, ("treelstm", "l", 10): 0.70,
     ("mvrnn", "s", 1): 0.34, ("mvrnn", "s", 10): 0.78, ("mvrnn", "l", 1): 0.39, ("mvrnn", "l", 10): 1.11,
 }
@@ -217,8 +223,11 @@ def ablation(args):
     stream = torch.cuda.current_stream()
     names = {0: "per-datum waits, one launch", 1: "plus a device-wide barrier per level",
              2: "one launch per level"}
-    for k, units in ((1, 0), (2, 0), (4, 64)):
-        wl = I.make_workload(k)
+    cases = [(I.make_workload(1), 0), (I.make_workload(2), 0),
+             (I.childsum_treegru_workload(I.BASE_SEED + 60, batch=10, H=256), 0),
+             (I.childsum_treegru_workload(I.BASE_SEED + 60, batch=10, H=256, simple=True), 0),
+             (I.make_workload(4), 64)]
+    for wl, units in cases:
         C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
         for mode in (0, 1, 2):
             C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)

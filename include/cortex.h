@@ -86,6 +86,8 @@ extern "C" {
 #define CORTEX_NARY_TREELSTM 1       /* binary N-ary TreeLSTM; leaf (h, c) = (x, 0) */
 #define CORTEX_CHILDSUM_TREELSTM 2   /* child-sum TreeLSTM; input x at every node */
 #define CORTEX_MVRNN 3               /* MV-RNN; leaf (p, P) = (a, A) */
+#define CORTEX_CHILDSUM_TREEGRU 4    /* child-sum TreeGRU: h = z*h~ + (1-z)*h'; input x at every node */
+#define CORTEX_SIMPLE_TREEGRU 5      /* SimpleTreeGRU: h = (1-z)*h' (Sec. 7.3 refactoring study) */
 
 /*
  * Linearization (Sec. 4.2, Appendix B).  Every pointer is device memory
@@ -116,6 +118,10 @@ typedef struct {
  *   NARY_TREELSTM      U [2, 5, H, H] = (U_l, U_r), gates (i, f_l, f_r, o, u); b [5, H]
  *   CHILDSUM_TREELSTM  W [4, H, H], U [4, H, H], gates (i, f, o, u); b [4, H]
  *   MVRNN              W [H, 2H], W_M [H, 2H]
+ *   CHILDSUM_TREEGRU,  W [3, H, H], U [3, H, H], b [3, H], gates (z, r, h):
+ *   SIMPLE_TREEGRU       h~ = sum_k h_k, z = s(W_z x + U_z h~ + b_z),
+ *                        r_k = s(W_r x + U_r h_k + b_r) per child,
+ *                        h' = tanh(W_h x + U_h sum_k r_k*h_k + b_h)
  */
 typedef struct {
   const float *W;
@@ -150,18 +156,21 @@ size_t cortex_forward_workspace_bytes(int32_t cell, int32_t N, int32_t H);
 /*
  * Forward pass of a tree cell over a linearized batch (the loop nest of
  * Sec. 4.1: a specialized leaf loop, then one fused step per level).
- *   cell        CORTEX_TREE_RNN / NARY_TREELSTM / CHILDSUM_TREELSTM / MVRNN
- *   H           hidden size: 64 or 256 for TREE_RNN, NARY and CHILDSUM; 64 for MVRNN
- *   lin         the output of cortex_linearize (K must be 2, or 1..4 for CHILDSUM)
+ *   cell        CORTEX_TREE_RNN / NARY_TREELSTM / CHILDSUM_TREELSTM / MVRNN /
+ *               CHILDSUM_TREEGRU / SIMPLE_TREEGRU
+ *   H           hidden size: 64, 256 or 512 for TREE_RNN; 64 or 256 for NARY, the
+ *               CHILDSUM cells and the TREEGRU cells; 64 for MVRNN
+ *   lin         the output of cortex_linearize (K must be 2, or 1..4 for the
+ *               child-sum TreeLSTM and TreeGRU cells)
  *   d_x_table   [x_rows, H] float32: leaf vectors or an embedding table
  *   d_x_index   [N] int32 by NODE ID: the input row of each node, -1 = none
  *               (zero input).  TREE_RNN, NARY and MVRNN read it at leaves only;
- *               CHILDSUM reads it at every node.
+ *               the child-sum TreeLSTM and TreeGRU cells read it at every node.
  *   d_leaf_mat  MVRNN only: [x_rows, H, H] leaf matrices (row-major)
  *   w           weights (layouts above)
  *   d_h         [N, H] output, in ROW order (row r = node lin->level_nodes[r])
  *   d_c_or_P    NARY/CHILDSUM: [N, H] memory cells; MVRNN: [N, H, H] matrices;
- *               TREE_RNN: unused (may be NULL).  Row order.
+ *               TREE_RNN and the TreeGRU cells: unused (may be NULL).  Row order.
  * An absent child slot contributes a zero state (Sec. 4.3).
  */
 int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,

@@ -35,6 +35,8 @@ CORTEX_TREE_RNN = 0
 CORTEX_NARY_TREELSTM = 1
 CORTEX_CHILDSUM_TREELSTM = 2
 CORTEX_MVRNN = 3
+CORTEX_CHILDSUM_TREEGRU = 4
+CORTEX_SIMPLE_TREEGRU = 5
 
 CORTEX_KNOB_LIN_BLOCKS = 0
 CORTEX_KNOB_FWD_NODE_GROUPS = 1
@@ -44,7 +46,8 @@ CORTEX_KNOB_FWD_SLICE_UNITS = 4
 CORTEX_KNOB_LEVEL_SYNC = 5
 
 CELL_IDS = {"tree_rnn": CORTEX_TREE_RNN, "nary_treelstm": CORTEX_NARY_TREELSTM,
-            "childsum_treelstm": CORTEX_CHILDSUM_TREELSTM, "mvrnn": CORTEX_MVRNN}
+            "childsum_treelstm": CORTEX_CHILDSUM_TREELSTM, "mvrnn": CORTEX_MVRNN,
+            "childsum_treegru": CORTEX_CHILDSUM_TREEGRU, "simple_treegru": CORTEX_SIMPLE_TREEGRU}
 
 EXPORTED = [
     "cortex_linearize_workspace_bytes", "cortex_linearize", "cortex_forward_workspace_bytes",

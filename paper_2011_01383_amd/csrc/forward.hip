@@ -1545,6 +1545,381 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
   CORTEX_TRACE_KERNEL(3);
 }
 
+// ---------------------------------------------------------------------------
+// Child-sum TreeGRU and SimpleTreeGRU.
+//   h~ = sum_k h_k,  z = s(W_z x + U_z h~ + b_z),  r_k = s(W_r x + U_r h_k + b_r),
+//   h' = tanh(W_h x + U_h m + b_h) with m = sum_k r_k * h_k,
+//   TreeGRU h = z*h~ + (1-z)*h';  SimpleTreeGRU h = (1-z)*h'.
+// The candidate needs the whole vector m, and each slice forms m only for its
+// own units, so a level has two exchanges: phase A (as in the child-sum
+// TreeLSTM kernel: node inputs on waves 0-3, the 16 x 4 child-slot rows on
+// all waves) gives z, r_k, m and h~ for the slice's units and publishes m as
+// (value, launch tag) pairs; phase B waits for the tile's m rows from every
+// slice and contracts them with U_h.  Weight-slice rows are (z, r, h, zero)
+// x 4 units; the edge contraction uses the U_z and U_r rows, phase B the U_h
+// rows (the other rows' results are unused).  Leaves (no child) have m = 0
+// and h~ = 0: a leaf phase evaluates them from their inputs alone.
+// ---------------------------------------------------------------------------
+template <int H, bool kSimple, bool kCached>
+__global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a) {
+  constexpr int J = 4;
+  constexpr int LDW = 2 * H + 4;
+  constexpr int KWX = H / 4, NBX = KWX / 16;      // node input part: waves 0-3
+  constexpr int KWE = H / 2, NBE = KWE / 16;      // edge part: two k halves
+  constexpr int BW = (H / 16 < kFwdWaves) ? H / 16 : kFwdWaves;   // phase B waves
+  constexpr int KWB = H / BW, NBB = KWB / 16;
+  constexpr int ZW = 6 * J;                       // per row: z, W_h x + b_h, then r_k * h_k and h_k per slot
+  static_assert(KWB % 16 == 0 && KWX % 16 == 0 && KWE % 16 == 0 && kTileM * ZW <= kFwdThreads, "tiling");
+
+  __shared__ __attribute__((aligned(16))) float W_s[16 * LDW];
+  __shared__ __attribute__((aligned(16))) float Cx[4 * 16 * 16];     // [4 waves][16 nodes][16]
+  __shared__ __attribute__((aligned(16))) float Ce[2 * 64 * 16];     // [2 halves][64 edges][16]; phase B: [8][16][16]
+  __shared__ float Z_s[kTileM * ZW];
+  __shared__ float R_s[kTileM * 4 * J][2];        // per (node, slot, unit): r_k * h_k, h_k
+  __shared__ float keep_s[kTileM * J][3];         // per (node, unit): z, W_h x + b_h, h~
+  __shared__ float bias_s[16];
+  __shared__ ChunkRows chunk;
+  extern __shared__ int cache[];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int slice = blockIdx.x % a.S, group = blockIdx.x / a.S, Q = a.Q;
+  const int hbase = slice * J;
+  const int N = a.N, K = a.K;
+  const uint32_t tag = a.tag;
+  const TagBuf hs(a.hs, (uint32_t)N * H * 8);
+  const TagBuf ms(a.cs, (uint32_t)N * H * 8);
+  const InBuf xin(a.x_table, (uint32_t)a.x_rows * H * 4);
+  const int em = wave & 3, ehalf = wave >> 2;
+  const int e_node = (16 * em + i16) >> 2, e_slot = (16 * em + i16) & 3;
+  const int ek = ehalf * KWE + 4 * g4;
+  const int zi = tid / ZW, zk = (tid % ZW) / J, zj = tid % J;   // epilogue item: row, kind, unit
+
+  CORTEX_TRACE_KERNEL(0);
+  const int status0 = load_status(a.status);
+  {
+    // weight slice: row m = g*J + j (g = z, r, h, zero); columns [W | U]
+    constexpr int ROW4 = (LDW - 4) / 4, ITEMS = 16 * ROW4, PER = (ITEMS + kFwdThreads - 1) / kFwdThreads;
+    float4 v[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads, m = idx / ROW4, c4 = idx % ROW4;
+      const int g = m / J, hj = hbase + m % J, sg = c4 / (H / 4), o4 = c4 % (H / 4);
+      v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (idx < ITEMS && g < 3) v[k] = *(const float4 *)((sg == 0 ? a.W : a.U) + ((size_t)g * H + hj) * H + o4 * 4);
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      if (idx < ITEMS) *(float4 *)&W_s[(idx / ROW4) * LDW + (idx % ROW4) * 4] = v[k];
+    }
+    if (tid < 16) bias_s[tid] = tid / J < 3 ? a.b[(tid / J) * H + hbase + tid % J] : 0.f;
+  }
+  if (status0 != 0) return;
+  CORTEX_TRACE_KERNEL(1);
+  Structure<kCached> st;
+  int L;
+  if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
+  CORTEX_TRACE_KERNEL(2);
+  int gave_up = 0;
+
+  // ---- level 0: leaves (m = 0, h~ = 0): h = (1 - z) tanh(W_h x + b_h) ----
+  if (a.level_lo == 0) {
+    constexpr int LW = (H / 16 < kFwdWaves) ? H / 16 : kFwdWaves;
+    constexpr int NBL = H / 16 / LW;
+    constexpr int kLeafBatch = 8;
+    CORTEX_TRACE_POINT(0, 0);
+    const int lr1 = st.offset(L > 1 ? 1 : L);
+    if (lr1 < 0 || lr1 > N) {
+      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      return;
+    }
+    const int nt0 = (lr1 + kTileM - 1) / kTileM;
+    const int kcol = wave * 16 * NBL + 4 * g4;
+    for (int ub = group; ub < nt0; ub += Q * kLeafBatch) {
+      u32x4 xl[kLeafBatch][NBL];
+#pragma unroll
+      for (int k = 0; k < kLeafBatch; ++k) {
+        const int row = (ub + k * Q) * kTileM + i16;
+        int xr = -1;
+        if (wave < LW && ub + k * Q < nt0 && row < lr1) {
+          if (kCached) {
+            xr = st.input_row(row);
+          } else {
+            const int v = a.level_nodes[row];
+            if (v < 0 || v >= N) {
+              raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+            } else {
+              xr = a.x_index[v];
+              if (xr < -1 || xr >= a.x_rows) {
+                raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+                xr = -1;
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < NBL; ++b)
+          xl[k][b] = xin.load4(xr >= 0 ? (uint32_t)((xr * H + kcol + 16 * b) * 4) : kNoSource);
+      }
+#pragma unroll
+      for (int k = 0; k < kLeafBatch; ++k) {
+        const int rowbase = (ub + k * Q) * kTileM;
+        if (rowbase >= lr1) break;
+        if (wave < LW) {
+          floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int b = 0; b < NBL; ++b)
+            acc = mfma_k16(as_float4(xl[k][b]), *(const float4 *)&W_s[i16 * LDW + kcol + 16 * b], acc);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) Ce[(wave * 16 + 4 * g4 + v) * 16 + i16] = acc[v];
+        }
+        __syncthreads();
+        if (tid < kTileM * J) {
+          const int i = tid / J, j = tid % J, row = rowbase + i;
+          float sz = bias_s[j], sh = bias_s[2 * J + j];
+#pragma unroll
+          for (int w = 0; w < LW; ++w) {
+            sz += Ce[(w * 16 + i) * 16 + j];
+            sh += Ce[(w * 16 + i) * 16 + 2 * J + j];
+          }
+          if (row < lr1) {
+            const float hv = (1.f - sigmoidf(sz)) * tanh_f(sh);
+            const uint32_t el = (uint32_t)(row * H + hbase + j);
+            hs.store1(el, hv, tag);
+            a.h[el] = hv;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    CORTEX_TRACE_POINT(0, 5);
+    if (L > 1 && a.level_hi > 1 && a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout))
+      return;
+  }
+
+  for (int l = a.level_lo > 1 ? a.level_lo : 1; l < L && l < a.level_hi; ++l) {
+    CORTEX_TRACE_POINT(l, 0);
+    const int r0 = st.offset(l), r1 = st.offset(l + 1);
+    if (!kCached && (r1 < r0 || r1 > N)) {
+      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      return;
+    }
+    const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
+    for (int u0 = ((group - l) % Q + Q) % Q; u0 < ntile; u0 += Q * kChunkTiles) {
+      const int u_last = min(ntile - 1, u0 + Q * (kChunkTiles - 1));
+      if (!kCached) {
+        __syncthreads();
+        stage_chunk(a, chunk, u0, (u_last - u0) / Q + 1, Q, r0, r1);
+        __syncthreads();
+      }
+      auto child = [&](int u, int i, int s) __attribute__((always_inline)) -> int {
+        const int row = r0 + u * kTileM + i;
+        if (row >= r1 || s >= K) return -1;
+        if (kCached) return st.child(row, s);
+        return chunk.crow[(u - u0) / Q][i][s];
+      };
+      for (int u = u0; u <= u_last; u += Q) {
+        const int rowbase = r0 + u * kTileM;
+        // ---- phase A operands: node inputs (waves 0-3), child-slot rows, and
+        //      this item's child state h_k[unit] ----
+        u32x4 xv[NBX];
+        {
+          int xr = -1;
+          if (wave < 4 && rowbase + i16 < r1) xr = kCached ? st.input_row(rowbase + i16) : chunk.xrow[(u - u0) / Q][i16];
+#pragma unroll
+          for (int b = 0; b < NBX; ++b)
+            xv[b] = xin.load4(xr >= 0 ? (uint32_t)((xr * H + wave * KWX + 16 * b + 4 * g4) * 4) : kNoSource);
+        }
+        const int ecr = child(u, e_node, e_slot);
+        Frag ev[NBE];
+#pragma unroll
+        for (int b = 0; b < NBE; ++b) {
+          const uint32_t so = ecr >= 0 ? (uint32_t)(ecr * H + ek + 16 * b) * 8u : kNoSource;
+          ev[b].lo = hs.load2_at(so);
+          ev[b].hi = hs.load2_at(so + 16u);
+        }
+        const int icr = (tid < kTileM * ZW && zk >= 2) ? child(u, zi, zk - 2) : -1;
+        const int ie = icr >= 0 ? icr * H + hbase + zj : -1;
+        u32x2 ih = hs.load1_at(ie >= 0 ? (uint32_t)ie * 8u : kNoSource);
+        // node-input part first: it needs no child
+        floatx4 xacc0 = {0.f, 0.f, 0.f, 0.f}, xacc1 = {0.f, 0.f, 0.f, 0.f};
+        if (wave < 4) {
+          const float *brow = &W_s[i16 * LDW + wave * KWX + 4 * g4];
+#pragma unroll
+          for (int b = 0; b < NBX; ++b) {
+            const float4 bv = *(const float4 *)(brow + 16 * b);
+            if (b & 1) xacc1 = mfma_k16(as_float4(xv[b]), bv, xacc1);
+            else xacc0 = mfma_k16(as_float4(xv[b]), bv, xacc0);
+          }
+        }
+        CORTEX_TRACE_POINT(l, 1);
+        auto ready_a = [&]() __attribute__((always_inline)) -> bool {
+          bool r = ie < 0 || ih.y == tag;
+          if (ecr >= 0) {
+#pragma unroll
+            for (int b = 0; b < NBE; ++b) r = r && ev[b].ready(tag);
+          }
+          return r;
+        };
+        if (!gave_up && !ready_a()) {
+          const uint64_t t0 = wall_clock64();
+          for (;;) {
+            __builtin_amdgcn_s_sleep(1);
+            if (ecr >= 0) {
+#pragma unroll
+              for (int b = 0; b < NBE; ++b)
+                if (!ev[b].ready(tag)) {
+                  const uint32_t so = (uint32_t)(ecr * H + ek + 16 * b) * 8u;
+                  ev[b].lo = hs.load2_at(so);
+                  ev[b].hi = hs.load2_at(so + 16u);
+                }
+            }
+            if (ie >= 0 && ih.y != tag) ih = hs.load1_at((uint32_t)ie * 8u);
+            const int stv = load_status(a.status);
+            if (ready_a()) break;
+            if (stv != 0) {
+              gave_up = 1;
+              break;
+            }
+            if (wall_clock64() - t0 > a.timeout) {
+              raise_status(a.status, CORTEX_ST_BARRIER_TIMEOUT);
+              gave_up = 1;
+              break;
+            }
+          }
+        }
+        CORTEX_TRACE_POINT(l, 2);
+        floatx4 eacc0 = {0.f, 0.f, 0.f, 0.f}, eacc1 = {0.f, 0.f, 0.f, 0.f};
+        if (__ballot(ecr >= 0) != 0) {
+          const float *brow = &W_s[i16 * LDW + H + ek];
+#pragma unroll
+          for (int b = 0; b < NBE; ++b) {
+            const float4 bv = *(const float4 *)(brow + 16 * b);
+            if (b & 1) eacc1 = mfma_k16(ev[b].value(true), bv, eacc1);
+            else eacc0 = mfma_k16(ev[b].value(true), bv, eacc0);
+          }
+        }
+        if (wave < 4) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) Cx[(wave * 16 + 4 * g4 + v) * 16 + i16] = xacc0[v] + xacc1[v];
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) Ce[(ehalf * 64 + 16 * em + 4 * g4 + v) * 16 + i16] = eacc0[v] + eacc1[v];
+        __syncthreads();
+        // ---- phase A epilogue: z, W_h x + b_h per (node, unit); r_k * h_k
+        //      and h_k per (node, slot, unit) ----
+        if (tid < kTileM * ZW) {
+          const int gz = zk == 0 ? 0 : (zk == 1 ? 2 : 1);      // gate row: z, h or r
+          const int m = gz * J + zj;
+          float sum = bias_s[m] + Cx[(0 * 16 + zi) * 16 + m] + Cx[(1 * 16 + zi) * 16 + m] +
+                      Cx[(2 * 16 + zi) * 16 + m] + Cx[(3 * 16 + zi) * 16 + m];
+          if (zk == 0) {                 // z: U_z h~ = sum over the child slots of U_z h_k
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+              sum += Ce[(0 * 64 + zi * 4 + s) * 16 + m] + Ce[(1 * 64 + zi * 4 + s) * 16 + m];
+            Z_s[tid] = sigmoidf(sum);
+          } else if (zk == 1) {
+            Z_s[tid] = sum;
+          } else {
+            const int s = zk - 2;
+            sum += Ce[(0 * 64 + zi * 4 + s) * 16 + m] + Ce[(1 * 64 + zi * 4 + s) * 16 + m];
+            const float hk = ie >= 0 ? as_float(ih.x) : 0.f;
+            R_s[(zi * 4 + s) * J + zj][0] = ie >= 0 ? sigmoidf(sum) * hk : 0.f;
+            R_s[(zi * 4 + s) * J + zj][1] = hk;
+          }
+        }
+        __syncthreads();
+        if (tid < kTileM * J) {
+          const int i = tid / J, j = tid % J, row = rowbase + i;
+          float mv = 0.f, hsum = 0.f;
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            mv += R_s[(i * 4 + s) * J + j][0];
+            hsum += R_s[(i * 4 + s) * J + j][1];
+          }
+          keep_s[tid][0] = Z_s[i * ZW + j];
+          keep_s[tid][1] = Z_s[i * ZW + J + j];
+          keep_s[tid][2] = hsum;
+          if (row < r1) ms.store1((uint32_t)(row * H + hbase + j), mv, tag);
+        }
+        // ---- phase B: the tile's m rows from every slice, contracted with U_h ----
+        Frag mf[NBB];
+        const int mrow = (wave < BW) ? rowbase + i16 : r1;       // waves past BW have no columns
+#pragma unroll
+        for (int b = 0; b < NBB; ++b) {
+          const uint32_t so = mrow < r1 ? (uint32_t)(mrow * H + wave * KWB + 16 * b + 4 * g4) * 8u : kNoSource;
+          mf[b].lo = ms.load2_at(so);
+          mf[b].hi = ms.load2_at(so + 16u);
+        }
+        auto ready_b = [&]() __attribute__((always_inline)) -> bool {
+          bool r = true;
+#pragma unroll
+          for (int b = 0; b < NBB; ++b) r = r && mf[b].ready(tag);
+          return mrow >= r1 || r;
+        };
+        if (!gave_up && !ready_b()) {
+          const uint64_t t0 = wall_clock64();
+          for (;;) {
+            __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+            for (int b = 0; b < NBB; ++b)
+              if (!mf[b].ready(tag)) {
+                const uint32_t so = (uint32_t)(mrow * H + wave * KWB + 16 * b + 4 * g4) * 8u;
+                mf[b].lo = ms.load2_at(so);
+                mf[b].hi = ms.load2_at(so + 16u);
+              }
+            const int stv = load_status(a.status);
+            if (ready_b()) break;
+            if (stv != 0) {
+              gave_up = 1;
+              break;
+            }
+            if (wall_clock64() - t0 > a.timeout) {
+              raise_status(a.status, CORTEX_ST_BARRIER_TIMEOUT);
+              gave_up = 1;
+              break;
+            }
+          }
+        }
+        floatx4 bacc = {0.f, 0.f, 0.f, 0.f};
+        if (wave < BW) {
+          const float *brow = &W_s[i16 * LDW + H + wave * KWB + 4 * g4];
+#pragma unroll
+          for (int b = 0; b < NBB; ++b) bacc = mfma_k16(mf[b].value(true), *(const float4 *)(brow + 16 * b), bacc);
+        }
+        __syncthreads();                  // every wave is past its reads of Ce (phase A)
+        if (wave < BW) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) Ce[(wave * 16 + 4 * g4 + v) * 16 + i16] = bacc[v];
+        }
+        __syncthreads();
+        CORTEX_TRACE_POINT(l, 3);
+        if (tid < kTileM * J) {
+          const int i = tid / J, j = tid % J, row = rowbase + i;
+          float sh = keep_s[tid][1];
+#pragma unroll
+          for (int w = 0; w < BW; ++w) sh += Ce[(w * 16 + i) * 16 + 2 * J + j];
+          const float zv = keep_s[tid][0];
+          const float cand = tanh_f(sh);
+          const float hv = kSimple ? (1.f - zv) * cand : zv * keep_s[tid][2] + (1.f - zv) * cand;
+          if (row < r1) {
+            const uint32_t el = (uint32_t)(row * H + hbase + j);
+            hs.store1(el, hv, tag);
+            a.h[el] = hv;
+          }
+        }
+        __syncthreads();
+        CORTEX_TRACE_POINT(l, 4);
+      }
+    }
+    CORTEX_TRACE_POINT(l, 5);
+    if (__syncthreads_or(gave_up)) return;
+    if (a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
+  }
+  CORTEX_TRACE_KERNEL(3);
+}
+
 // Validated level bounds; false (and a status) when the linearization is broken.
 __device__ __forceinline__ bool level_bounds(const FwdArgs &a, int l, int &r0, int &r1) {
   r0 = a.level_offsets[l];
@@ -1820,7 +2195,8 @@ constexpr size_t kStructCacheBudget = 40 * 1024;    // bytes of LDS for the cach
 // (child-sum: offsets, child rows, input rows; the slice kernels: offsets,
 // source codes, input rows of the leaf-input cells)
 static size_t cache_ints(int cell, int32_t N, int32_t K) {
-  if (cell == CORTEX_CHILDSUM_TREELSTM) return (size_t)N + 1 + (size_t)N * K + N;
+  if (cell == CORTEX_CHILDSUM_TREELSTM || cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU)
+    return (size_t)N + 1 + (size_t)N * K + N;
   const size_t segs = cell == CELL_DAG ? 3 : 2;
   return (size_t)N + 1 + (size_t)N * segs + (cell == CELL_DAG ? 0 : N);
 }
@@ -1878,6 +2254,19 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   CORTEX_CASE(CELL_DAG, 256)
   CORTEX_CASE(CELL_DAG, 512)
 #undef CORTEX_CASE
+  if ((cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) && (H == 64 || H == 256)) {
+    const bool simple = cell == CORTEX_SIMPLE_TREEGRU;
+    if (H == 64)
+      out.fn = simple ? (cached ? treegru_forward_kernel<64, true, true> : treegru_forward_kernel<64, true, false>)
+                      : (cached ? treegru_forward_kernel<64, false, true> : treegru_forward_kernel<64, false, false>);
+    else
+      out.fn = simple ? (cached ? treegru_forward_kernel<256, true, true> : treegru_forward_kernel<256, true, false>)
+                      : (cached ? treegru_forward_kernel<256, false, true> : treegru_forward_kernel<256, false, false>);
+    out.J = 4;
+    out.threads = kFwdThreads;
+    out.level_barrier_ok = out.level_range_ok = true;
+    return true;
+  }
   if (cell == CORTEX_MVRNN && H == kMvD) {
     out.fn = mvrnn_forward_kernel;
     out.J = kMvD;
@@ -1895,7 +2284,9 @@ static size_t staging_bytes(int32_t N, int32_t H) { return align_up((size_t)N * 
 static size_t staging_offset() { return align_up(kSyncBytes + kTraceBytes, 256); }
 size_t trace_offset() { return kSyncBytes; }
 static int staged_tensors(int32_t cell) {
-  if (cell == CORTEX_NARY_TREELSTM || cell == CORTEX_CHILDSUM_TREELSTM || cell == CORTEX_MVRNN) return 2;
+  if (cell == CORTEX_NARY_TREELSTM || cell == CORTEX_CHILDSUM_TREELSTM || cell == CORTEX_MVRNN ||
+      cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU)
+    return 2;                                   // h, and c / P / the TreeGRU reset sum m
   if (cell == CORTEX_TREE_RNN || cell == -1) return 1;
   return 0;
 }
@@ -1924,7 +2315,9 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   bool cached = false;
   if (cell != CORTEX_MVRNN) {
     dyn = cache_ints(cell, lin->num_nodes, lin->max_arity) * sizeof(int);
-    cached = dyn <= kStructCacheBudget && (cell == CORTEX_CHILDSUM_TREELSTM || lin->num_nodes <= kMaxCachedRows);
+    const bool childsum_like =
+        cell == CORTEX_CHILDSUM_TREELSTM || cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU;
+    cached = dyn <= kStructCacheBudget && (childsum_like || lin->num_nodes <= kMaxCachedRows);
     if (!cached) dyn = 0;
   }
   Instance inst;
@@ -2002,7 +2395,7 @@ using namespace cortex;
 
 extern "C" size_t cortex_forward_workspace_bytes(int32_t cell, int32_t N, int32_t H) {
   if (N < 0 || H <= 0) return 0;
-  if (cell < -1 || cell > CORTEX_MVRNN) return 0;
+  if (cell < -1 || cell > CORTEX_SIMPLE_TREEGRU) return 0;
   const int staged = cortex::staged_tensors(cell);
   return cortex::staging_offset() + (staged >= 1 ? cortex::staging_bytes(N, H) : 0) +
          (staged >= 2 ? cortex::second_staging_bytes(cell, N, H) : 0);
@@ -2013,12 +2406,14 @@ extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *
                                    const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status,
                                    void *d_ws, size_t ws_bytes, void *stream) {
   if (!lin_ok(lin) || !w || !d_status || x_rows < 0) return CORTEX_E_INVAL;
-  if (cell < CORTEX_TREE_RNN || cell > CORTEX_MVRNN) return CORTEX_E_INVAL;
+  if (cell < CORTEX_TREE_RNN || cell > CORTEX_SIMPLE_TREEGRU) return CORTEX_E_INVAL;
   if (lin->num_nodes == 0) return CORTEX_OK;
   if (!d_ws || !d_h || !d_x_index || (x_rows > 0 && !d_x_table)) return CORTEX_E_INVAL;
   const int K = lin->max_arity;
   if (cell == CORTEX_CHILDSUM_TREELSTM) {
     if (!w->W || !w->U || !w->b || !d_c_or_P) return CORTEX_E_INVAL;
+  } else if (cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) {
+    if (!w->W || !w->U || !w->b) return CORTEX_E_INVAL;
   } else {
     if (K != 2) return CORTEX_E_INVAL;
     if (cell == CORTEX_TREE_RNN && (!w->W || !w->b)) return CORTEX_E_INVAL;

@@ -57,6 +57,10 @@ SMALL = {
     "childsum_h256": lambda s: I.childsum_treelstm_workload(s, batch=3, H=256, vocab=50, node_lo=1, node_hi=40),
     "mvrnn": lambda s: I.mvrnn_workload(s, batch=4, d=64, leaf_lo=1, leaf_hi=30),
     "mvrnn_gain1": lambda s: I.mvrnn_workload(s, batch=3, d=64, leaf_lo=10, leaf_hi=40, wm_scale=0.153),
+    "treegru_h64": lambda s: I.childsum_treegru_workload(s, batch=4, H=64, vocab=50, node_lo=1, node_hi=60),
+    "treegru_h256": lambda s: I.childsum_treegru_workload(s, batch=3, H=256, vocab=50, node_lo=1, node_hi=40),
+    "simple_treegru_h256": lambda s: I.childsum_treegru_workload(s, batch=3, H=256, vocab=50, node_lo=1,
+                                                                 node_hi=40, simple=True),
     "dag_h64": lambda s: I.dagrnn_workload(s, n_grids=3, rows=7, cols=5, H=64),
     "dag_h256": lambda s: I.dagrnn_workload(s, n_grids=2, rows=9, cols=11, H=256),
 }
@@ -242,6 +246,7 @@ def test_tree_rnn_h64_lds_limit(n_leaves):
 
 
 LEVEL_SYNC_CASES = {
+    "treegru": (lambda: I.childsum_treegru_workload(44, batch=4, H=256), 0),
     "nary": (lambda: cached_workload(1, 0), 0),
     "childsum": (lambda: cached_workload(2, 0), 0),
     "tree_rnn_h256": (lambda: I.tree_rnn_workload(41, n_leaves=37, H=256), 0),
@@ -286,3 +291,24 @@ def test_level_sync_modes_unsupported(k, mode):
     with pytest.raises(RuntimeError, match="host code %d" % C.CORTEX_E_INVAL):
         dw.forward()
     assert dw.status_code() == 0
+
+
+@pytest.mark.parametrize("simple", [False, True])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_treegru_batch10_parity(simple, seed):
+    """Child-sum TreeGRU and SimpleTreeGRU, H = 256, a batch of 10 SST-sized
+    random trees (arity 1-4), against the oracle."""
+    wl = I.childsum_treegru_workload(I.BASE_SEED + 50 + seed, batch=10, H=256, simple=simple)
+    announce("%s seed %d N=%d" % (wl.name, seed, wl.N))
+    dw = run(wl)
+    compare_lin(dw.lin_host(), O.linearize(wl.children, wl.K), wl.K)
+    compare_states(dw.states_by_node(), O.forward_workload(wl), wl.name)
+
+
+def test_treegru_uncached_structure():
+    """A TreeGRU batch too large for the LDS structure cache."""
+    wl = I.childsum_treegru_workload(34, batch=110, H=256)
+    assert wl.N > 2600
+    announce("treegru uncached N=%d" % wl.N)
+    dw = run(wl)
+    compare_states(dw.states_by_node(), O.forward_workload(wl), wl.name)

@@ -14,9 +14,9 @@ from tests.gpu_helpers import announce, compare_lin, compare_states, need_gpu
 
 pytestmark = pytest.mark.gpu
 
-SUPPORTED = [(c, b, "s") for c in I.PAPER_GRID_CELLS if c != "treegru" for b in (1, 10)] + \
+SUPPORTED = [(c, b, "s") for c in I.PAPER_GRID_CELLS for b in (1, 10)] + \
             [(c, b, "l") for c in ("treefc", "dagrnn") for b in (1, 10)]
-UNSUPPORTED = [("treelstm", 1, "l"), ("mvrnn", 1, "l")]
+UNSUPPORTED = [("treegru", 1, "l"), ("treelstm", 1, "l"), ("mvrnn", 1, "l")]
 
 
 @pytest.fixture(autouse=True)
