@@ -213,7 +213,9 @@ def ablation(args):
     """How the forward orders its levels (CORTEX_KNOB_LEVEL_SYNC): per-datum
     waits in one persistent launch (the default), plus a device-wide barrier
     after every level, or one launch per level that reloads weights and
-    structure each time.  One JSON line per (workload, mode): the forward
+    structure each time; for the TreeGRU cells also a barrier after each of
+    the level's two exchanges (the schedule without recursive refactoring,
+    Secs. 3.1 and 7.4).  One JSON line per (workload, mode): the forward
     kernel time (for mode 2, the whole per-level launch sequence, which also
     synchronizes once to read L)."""
     import torch
@@ -222,14 +224,15 @@ def ablation(args):
     from paper_2011_01383_amd.runner import DeviceWorkload
     stream = torch.cuda.current_stream()
     names = {0: "per-datum waits, one launch", 1: "plus a device-wide barrier per level",
-             2: "one launch per level"}
+             2: "one launch per level",
+             3: "a device-wide barrier after each of the two exchanges per level"}
     cases = [(I.make_workload(1), 0), (I.make_workload(2), 0),
              (I.childsum_treegru_workload(I.BASE_SEED + 60, batch=10, H=256), 0),
              (I.childsum_treegru_workload(I.BASE_SEED + 60, batch=10, H=256, simple=True), 0),
              (I.make_workload(4), 64)]
     for wl, units in cases:
         C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
-        for mode in (0, 1, 2):
+        for mode in ((0, 1, 3, 2) if wl.cell in (I.CELL_CHILDSUM_TREEGRU, I.CELL_SIMPLE_TREEGRU) else (0, 1, 2)):
             C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)
             line = {"workload": wl.name, "level_sync": mode, "mode": names[mode]}
             dw = DeviceWorkload(wl)

@@ -87,7 +87,7 @@ extern "C" {
 #define CORTEX_CHILDSUM_TREELSTM 2   /* child-sum TreeLSTM; input x at every node */
 #define CORTEX_MVRNN 3               /* MV-RNN; leaf (p, P) = (a, A) */
 #define CORTEX_CHILDSUM_TREEGRU 4    /* child-sum TreeGRU: h = z*h~ + (1-z)*h'; input x at every node */
-#define CORTEX_SIMPLE_TREEGRU 5      /* SimpleTreeGRU: h = (1-z)*h' (Sec. 7.3 refactoring study) */
+#define CORTEX_SIMPLE_TREEGRU 5      /* SimpleTreeGRU: h = (1-z)*h' (Sec. 7.4 refactoring study) */
 
 /*
  * Linearization (Sec. 4.2, Appendix B).  Every pointer is device memory
@@ -223,11 +223,17 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *                                   2 = one launch per level, each reloading
  *                                   weights and structure (slice, child-sum
  *                                   and 64-unit DAG-RNN kernels; the call then
- *                                   synchronizes the stream once to read L).
+ *                                   synchronizes the stream once to read L);
+ *                                   3 = the TreeGRU cells only: a device-wide
+ *                                   barrier after each of a level's two
+ *                                   exchanges (the reset sums, then the
+ *                                   states): the TreeGRU schedule without
+ *                                   recursive refactoring (Secs. 3.1, 7.4), where
+ *                                   1 is the refactored one.
  *                                   A forward whose kernel lacks the mode
  *                                   returns CORTEX_E_INVAL.
  * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value
- * (or a LEVEL_SYNC value above 2).
+ * (or a LEVEL_SYNC value above 3).
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0
 #define CORTEX_KNOB_FWD_NODE_GROUPS 1

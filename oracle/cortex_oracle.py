@@ -44,7 +44,7 @@ published forms are used, see the readings listed with the design notes):
                      h' = tanh(W_h x + U_h sum_k r_k*h_k + b_h);
                      h = z*h~ + (1-z)*h'; x at every node
 * simple_treegru     the same with h = (1-z)*h' (the simplification the
-                     paper describes for its refactoring study, Sec. 7.3)
+                     paper describes for its refactoring study, Sec. 7.4)
 
 Every function here is pinned by ``tests/test_oracle_*.py`` against hand
 values, library cells (torch RNNCell/LSTMCell in fp64), closed forms and the

@@ -86,7 +86,9 @@ struct FwdArgs {
   uint32_t tag;                 // this launch's staging tag
   void *hs, *cs;                // tagged staging of h and c (workspace)
   int32_t level_lo, level_hi;   // levels this launch runs (all of them unless one launch per level)
-  int32_t level_barrier;        // 1: a device-wide barrier closes every level (instead of per-datum waits alone)
+  int32_t level_barrier;        // 1: a device-wide barrier closes every level (instead of per-datum waits alone);
+                                // 2 (TreeGRU): also one between the level's two exchanges
+  float *keep;                  // TreeGRU, level_barrier 2: z, W_h x + b_h and h~ per (row, unit), [3][N][H]
 };
 
 // ---------------------------------------------------------------------------
@@ -1706,6 +1708,15 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
       return;
     }
     const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
+    // one pass per level; two (phase A of every tile, a device-wide barrier,
+    // then phase B) under level_barrier 2
+    const int npass = a.level_barrier == 2 ? 2 : 1;
+    for (int pass = 0; pass < npass; ++pass) {
+    const bool doA = pass == 0, doB = pass == npass - 1;
+    if (pass == 1) {
+      if (__syncthreads_or(gave_up)) return;
+      if (!grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
+    }
     for (int u0 = ((group - l) % Q + Q) % Q; u0 < ntile; u0 += Q * kChunkTiles) {
       const int u_last = min(ntile - 1, u0 + Q * (kChunkTiles - 1));
       if (!kCached) {
@@ -1721,6 +1732,8 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
       };
       for (int u = u0; u <= u_last; u += Q) {
         const int rowbase = r0 + u * kTileM;
+        const size_t plane = (size_t)N * H;
+        if (doA) {
         // ---- phase A operands: node inputs (waves 0-3), child-slot rows, and
         //      this item's child state h_k[unit] ----
         u32x4 xv[NBX];
@@ -1841,7 +1854,26 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
           keep_s[tid][0] = Z_s[i * ZW + j];
           keep_s[tid][1] = Z_s[i * ZW + J + j];
           keep_s[tid][2] = hsum;
-          if (row < r1) ms.store1((uint32_t)(row * H + hbase + j), mv, tag);
+          if (row < r1) {
+            const uint32_t el = (uint32_t)(row * H + hbase + j);
+            ms.store1(el, mv, tag);
+            if (!doB) {                  // phase B runs after the barrier: keep z, W_h x + b_h, h~
+              a.keep[el] = keep_s[tid][0];
+              a.keep[plane + el] = keep_s[tid][1];
+              a.keep[2 * plane + el] = hsum;
+            }
+          }
+        }
+        }                                // doA
+        if (!doB) continue;
+        if (!doA && tid < kTileM * J) {  // the same thread wrote them before the barrier
+          const int row = rowbase + tid / J;
+          if (row < r1) {
+            const size_t el = (size_t)row * H + hbase + tid % J;
+            keep_s[tid][0] = a.keep[el];
+            keep_s[tid][1] = a.keep[plane + el];
+            keep_s[tid][2] = a.keep[2 * plane + el];
+          }
         }
         // ---- phase B: the tile's m rows from every slice, contracted with U_h ----
         Frag mf[NBB];
@@ -1913,6 +1945,7 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
         CORTEX_TRACE_POINT(l, 4);
       }
     }
+    }                                    // pass
     CORTEX_TRACE_POINT(l, 5);
     if (__syncthreads_or(gave_up)) return;
     if (a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
@@ -2187,6 +2220,7 @@ struct Instance {
   size_t lds = SIZE_MAX;        // dynamic LDS the kernel sizes itself (SIZE_MAX: the structure cache)
   bool level_barrier_ok = false;   // honours FwdArgs.level_barrier
   bool level_range_ok = false;     // honours FwdArgs.level_lo / level_hi
+  bool phase_barrier_ok = false;   // has two exchanges per level and honours level_barrier 2
 };
 
 constexpr size_t kStructCacheBudget = 40 * 1024;    // bytes of LDS for the cached linearization
@@ -2264,7 +2298,7 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
                       : (cached ? treegru_forward_kernel<256, false, true> : treegru_forward_kernel<256, false, false>);
     out.J = 4;
     out.threads = kFwdThreads;
-    out.level_barrier_ok = out.level_range_ok = true;
+    out.level_barrier_ok = out.level_range_ok = out.phase_barrier_ok = true;
     return true;
   }
   if (cell == CORTEX_MVRNN && H == kMvD) {
@@ -2290,9 +2324,13 @@ static int staged_tensors(int32_t cell) {
   if (cell == CORTEX_TREE_RNN || cell == -1) return 1;
   return 0;
 }
-// bytes of the second staged tensor: c [N, H], or P [N, H, H] for MV-RNN
+// bytes of the second staged tensor: c [N, H], P [N, H, H] for MV-RNN, or the
+// TreeGRU reset sums m [N, H] followed by the kept phase-A values [3, N, H]
+static size_t keep_bytes(int32_t N, int32_t H) { return align_up((size_t)N * H * 3 * sizeof(float), 256); }
 static size_t second_staging_bytes(int32_t cell, int32_t N, int32_t H) {
-  return cell == CORTEX_MVRNN ? align_up((size_t)N * H * H * 8, 256) : staging_bytes(N, H);
+  if (cell == CORTEX_MVRNN) return align_up((size_t)N * H * H * 8, 256);
+  if (cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) return staging_bytes(N, H) + keep_bytes(N, H);
+  return staging_bytes(N, H);
 }
 static std::atomic<uint32_t> g_tag{0};
 
@@ -2348,14 +2386,18 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   char *stage = (char *)d_ws + staging_offset();
   a.hs = staged >= 1 ? stage : nullptr;
   a.cs = staged >= 2 ? stage + staging_bytes(lin->num_nodes, H) : nullptr;   // c, or P for MV-RNN
+  a.keep = inst.phase_barrier_ok ? (float *)(stage + 2 * staging_bytes(lin->num_nodes, H)) : nullptr;
   a.tag = next_tag();
   a.level_lo = 0;
   a.level_hi = 0x7fffffff;
   a.level_barrier = 0;
   const int64_t sync_mode = knob(CORTEX_KNOB_LEVEL_SYNC);
-  if ((sync_mode == 1 && !inst.level_barrier_ok) || (sync_mode == 2 && !inst.level_range_ok)) return CORTEX_E_INVAL;
+  if ((sync_mode == 1 && !inst.level_barrier_ok) || (sync_mode == 2 && !inst.level_range_ok) ||
+      (sync_mode == 3 && !inst.phase_barrier_ok))
+    return CORTEX_E_INVAL;
   set_last_grid(1, (int32_t)G);
   if (sync_mode == 1) a.level_barrier = 1;
+  if (sync_mode == 3) a.level_barrier = 2;
   if (sync_mode != 2) return launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
   // one launch per level (ablation): L is read back first; every launch
   // reloads weights and structure and keeps the launch tag, so a level

@@ -80,8 +80,8 @@ def test_knobs(lib):
 
 def test_level_sync_knob_range(lib):
     assert C.cortex_get_knob(C.CORTEX_KNOB_LEVEL_SYNC) == 0
-    assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 3) == C.CORTEX_E_INVAL
-    for v in (2, 1, 0):
+    assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 4) == C.CORTEX_E_INVAL
+    for v in (3, 2, 1, 0):
         assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, v) == C.CORTEX_OK
         assert C.cortex_get_knob(C.CORTEX_KNOB_LEVEL_SYNC) == v
     assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC + 1, 0) == C.CORTEX_E_INVAL

@@ -293,6 +293,43 @@ def test_level_sync_modes_unsupported(k, mode):
     assert dw.status_code() == 0
 
 
+TREEGRU_SPLIT_CASES = {
+    "treegru_h256_b4": lambda: I.childsum_treegru_workload(44, batch=4, H=256),
+    "simple_treegru_h256_b10": lambda: I.childsum_treegru_workload(45, batch=10, H=256, simple=True),
+    "treegru_h64_b10": lambda: I.childsum_treegru_workload(46, batch=10, H=64),
+    "treegru_h256_uncached": lambda: I.childsum_treegru_workload(47, batch=110, H=256),
+}
+
+
+@pytest.mark.parametrize("name", sorted(TREEGRU_SPLIT_CASES))
+def test_treegru_phase_barrier_mode(name):
+    """LEVEL_SYNC 3 (a device-wide barrier between the reset sums and the
+    candidate, and another closing the level) keeps phase-A values in the
+    workspace across the barrier; the states are bitwise those of the
+    default schedule."""
+    wl = TREEGRU_SPLIT_CASES[name]()
+    announce("treegru phase barrier %s N=%d" % (name, wl.N))
+    ref = run(wl).states_by_node()
+    C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 3)
+    got = run(wl).states_by_node()
+    for key in ref:
+        assert np.array_equal(ref[key], got[key]), key
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4])
+def test_phase_barrier_mode_needs_two_exchanges(k):
+    """Only the TreeGRU kernels have a second exchange per level; the other
+    forwards reject LEVEL_SYNC 3 on the host and enqueue nothing."""
+    wl = cached_workload(k, 0)
+    announce("level sync mode 3 unsupported on workload %d" % k)
+    C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 3)
+    dw = DeviceWorkload(wl)
+    dw.linearize()
+    with pytest.raises(RuntimeError, match="host code %d" % C.CORTEX_E_INVAL):
+        dw.forward()
+    assert dw.status_code() == 0
+
+
 @pytest.mark.parametrize("simple", [False, True])
 @pytest.mark.parametrize("seed", [0, 1])
 def test_treegru_batch10_parity(simple, seed):
