@@ -266,6 +266,57 @@ def ablation(args):
         C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
 
 
+def unroll_study(args):
+    """Unrolled recursion for TreeRNN at H = 64 (Secs. 3.1, 7.4;
+    CORTEX_KNOB_TREE_UNROLL): the whole batch in one workgroup (up to 320
+    nodes), one workgroup per tree, and level-parallel hidden slices that
+    exchange states between workgroups at every level.  One JSON line per
+    (batch, schedule): the forward kernel time and the step (linearize +
+    forward), both averaged over back-to-back launches between two events."""
+    import torch
+    from paper_2011_01383_amd import cortex as C
+    from paper_2011_01383_amd import inputs as I
+    from paper_2011_01383_amd.runner import DeviceWorkload
+    stream = torch.cuda.current_stream()
+    names = {0: "whole batch in one workgroup", 1: "level-parallel hidden slices", 2: "one workgroup per tree"}
+    cases = [I.make_workload(0), I.tree_rnn_forest_workload(I.BASE_SEED + 80, batch=5),
+             I.tree_rnn_forest_workload(I.BASE_SEED + 81, batch=10),
+             I.tree_rnn_forest_workload(I.BASE_SEED + 82, batch=32, leaf_lo=10, leaf_hi=40),
+             I.tree_rnn_forest_workload(I.BASE_SEED + 83, batch=100, leaf_lo=2, leaf_hi=18)]
+    n = max(10, min(args.steps, 100))
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    for wl in cases:
+        for mode in (0, 2, 1):
+            if mode == 0 and wl.N > 320:
+                continue
+            C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL, mode)
+            dw = DeviceWorkload(wl)
+            dw.step()
+            torch.cuda.synchronize()
+            assert dw.status_code() == 0
+            fwd = timed(dw.forward)
+            step = timed(dw.step)
+            assert dw.status_code() == 0
+            print(json.dumps({"workload": wl.name, "nodes": wl.N, "levels": int(dw.lin_host()["num_levels"]),
+                              "schedule": names[mode], "tree_unroll": mode, "grid": C.cortex_last_grid(1),
+                              "forward_ms": fwd, "step_ms": step}))
+            sys.stdout.flush()
+        C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL, 0)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -283,6 +334,8 @@ def main():
                     help="run the paper's model x batch x hidden-size grid; one JSON line per cell")
     ap.add_argument("--ablation", action="store_true",
                     help="forward time under each level-ordering mode; one JSON line per (workload, mode)")
+    ap.add_argument("--unroll", action="store_true",
+                    help="TreeRNN H = 64 batches under each unrolling schedule; one JSON line per (batch, schedule)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -314,6 +367,9 @@ def main():
         return
     if args.ablation:
         ablation(args)
+        return
+    if args.unroll:
+        unroll_study(args)
         return
     wl = I.make_workload(args.workload)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, args.node_groups)

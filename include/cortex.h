@@ -200,7 +200,10 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  * never the results.
  *   CORTEX_KNOB_LIN_BLOCKS          workgroups of the linearizer (0 = chosen from N)
  *   CORTEX_KNOB_FWD_NODE_GROUPS     node groups of the forward; workgroups =
- *                                   hidden slices x node groups (0 = fill the GPU)
+ *                                   hidden slices x node groups (0 = fill the
+ *                                   GPU; a kernel with one slice, TreeRNN at
+ *                                   H = 64, takes one group per 16 nodes, at
+ *                                   most one per compute unit)
  *   CORTEX_KNOB_BARRIER_TIMEOUT_US  spin limit of one barrier or per-datum wait in
  *                                   microseconds (default 5,000,000; 0 makes every
  *                                   wait time out at once, for tests of that path)
@@ -232,8 +235,20 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *                                   1 is the refactored one.
  *                                   A forward whose kernel lacks the mode
  *                                   returns CORTEX_E_INVAL.
+ *   CORTEX_KNOB_TREE_UNROLL         TreeRNN at H = 64 (Secs. 3.1, 7.4, unrolled
+ *                                   recursion): 0 = the default choice (the
+ *                                   whole batch in one workgroup up to 320
+ *                                   nodes, one workgroup per tree up to 2048,
+ *                                   hidden slices beyond); 1 = level-parallel
+ *                                   hidden slices, states exchanged between
+ *                                   workgroups at every level; 2 = one
+ *                                   workgroup per tree, each tree evaluated
+ *                                   leaves to root on one compute unit (up to
+ *                                   2048 nodes, else CORTEX_E_INVAL; with
+ *                                   FWD_NODE_GROUPS > 0 that many workgroups
+ *                                   share the trees).
  * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value
- * (or a LEVEL_SYNC value above 3).
+ * (or a LEVEL_SYNC value above 3, a TREE_UNROLL value above 2).
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0
 #define CORTEX_KNOB_FWD_NODE_GROUPS 1
@@ -241,6 +256,7 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
 #define CORTEX_KNOB_COOPERATIVE 3
 #define CORTEX_KNOB_FWD_SLICE_UNITS 4
 #define CORTEX_KNOB_LEVEL_SYNC 5
+#define CORTEX_KNOB_TREE_UNROLL 6
 int cortex_set_knob(int32_t knob, int64_t value);
 int64_t cortex_get_knob(int32_t knob);
 

@@ -21,6 +21,7 @@
 // are the inputs themselves (specialization, Sec. 3.1; zero initial memory
 // cell, Sec. 4.3): a level reading a leaf child takes the row from the input
 // table directly, so nothing ever waits on the leaf level.
+#include <algorithm>
 #include <atomic>
 
 #include "cortex_device.hpp"
@@ -1548,6 +1549,270 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
 }
 
 // ---------------------------------------------------------------------------
+// TreeRNN at H = 64, unrolled recursion (Secs. 3.1, 7.4): every tree of the
+// batch is evaluated by one workgroup from its leaves to its root, so a node
+// is computed right after its children on the same compute unit and reads
+// their states from LDS; no state crosses workgroups and no workgroup waits
+// on another.  Every workgroup derives the same assignment from the
+// linearization: parents from the child rows, the root of every row by
+// pointer jumping (a child row lies in a strictly lower level, so parent
+// rows strictly increase and the jumps end), and the tree of root row t to
+// workgroup floor(G * hash(t) / 2^32).  A node with several parents joins
+// trees, so such a batch goes whole to workgroup 0.  A workgroup groups its
+// own rows by level (a slot per row from a per-level counter; the order
+// inside a level does not matter, rows being independent) and walks them
+// level by level with one workgroup barrier between levels, as the
+// single-workgroup kernel does; weights, tiles and epilogue are the same.
+// A workgroup that owns more than kForestStateRows rows keeps its states in
+// the output rows instead of LDS (its own stores, ordered by the barriers).
+// ---------------------------------------------------------------------------
+constexpr int kForestMaxRows = 2048;          // batch limit (per-row arrays in LDS)
+constexpr int kForestStateRows = 256;         // owned rows whose states stay in LDS
+constexpr int kForestRowsPerThread = kForestMaxRows / kFwdThreads;
+
+// LDS of the forest kernel: the states, then off [N + 1], crow [2N], loc, jp,
+// lrow, lx [N], loff [N + 1] and lc [2 kForestStateRows]: 8N + 2 + 512 ints.
+static size_t forest_lds_bytes(int32_t N) {
+  return (size_t)kForestStateRows * kLdsHStride * sizeof(float) +
+         ((size_t)(N + 1) + 2 * (size_t)N + 4 * (size_t)N + (N + 1) + 2 * kForestStateRows) * sizeof(int);
+}
+
+// The level walk over a workgroup's own rows lrow[0 .. n), grouped by level
+// (level l is lrow[loff[l] .. loff[l+1])); lx[k] is the input row of own
+// leaf k.  kLdsState: state k is h_s row k and lc holds the local indices of
+// its child slots; otherwise the states are the output rows and the child
+// slots are read as rows from crow.
+template <bool kLdsState>
+__device__ __forceinline__ void forest_levels(const FwdArgs &a, const int *crow, const int *lrow, const int *lc,
+                                              const int *lx, const int *loff, int L, float *h_s, const float4 *wr,
+                                              const float *bias_s, float (*C_s)[kTileM][kLdsH + 4]) {
+  constexpr int H = kLdsH, LDH = kLdsHStride, NB = H / 16;
+  constexpr int EPI = kTileM * H / kFwdThreads;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int nt = wave & 3, kh = wave >> 2;
+  auto state = [&](int k) __attribute__((always_inline)) -> float * {
+    return kLdsState ? h_s + (size_t)k * LDH : a.h + (size_t)lrow[k] * H;
+  };
+  auto child_state = [&](int c) __attribute__((always_inline)) -> const float * {
+    return kLdsState ? h_s + (size_t)c * LDH : a.h + (size_t)c * H;
+  };
+  // level 0: the leaves are their input rows (zeros without one)
+  CORTEX_TRACE_POINT(0, 0);
+  for (int e = tid; e < loff[1] * (H / 4); e += kFwdThreads) {
+    const int k = e / (H / 4), c4 = e % (H / 4);
+    const int xr = lx[k];
+    const float4 v = xr >= 0 ? *(const float4 *)&a.x_table[(size_t)xr * H + 4 * c4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    *(float4 *)(state(k) + 4 * c4) = v;
+  }
+  __syncthreads();
+  CORTEX_TRACE_POINT(0, 5);
+  for (int l = 1; l < L; ++l) {
+    CORTEX_TRACE_POINT(l, 0);
+    const int k0 = loff[l], k1 = loff[l + 1];
+    for (int kb = k0; kb < k1; kb += kTileM) {
+      const int k = kb + i16;
+      const int cr = k >= k1 ? -1 : (kLdsState ? lc[2 * k + kh] : crow[2 * lrow[k] + kh]);
+      float4 av[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        av[b] = cr >= 0 ? *(const float4 *)(child_state(cr) + 16 * b + 4 * g4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if (b & 1) acc1 = mfma_k16(av[b], wr[b], acc1);
+        else acc0 = mfma_k16(av[b], wr[b], acc0);
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) C_s[kh][4 * g4 + v][16 * nt + i16] = acc0[v] + acc1[v];
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < EPI; ++e) {
+        const int p = tid + e * kFwdThreads, i = p / H, j = p % H;
+        if (kb + i < k1) state(kb + i)[j] = tanh_f(bias_s[j] + C_s[0][i][j] + C_s[1][i][j]);
+      }
+      __syncthreads();
+    }
+    CORTEX_TRACE_POINT(l, 5);
+  }
+}
+
+__global__ void __launch_bounds__(kFwdThreads) tree_rnn_forest_kernel(FwdArgs a) {
+  constexpr int H = kLdsH, LDH = kLdsHStride, NB = H / 16, RPT = kForestRowsPerThread;
+  __shared__ __attribute__((aligned(16))) float C_s[2][kTileM][H + 4];
+  __shared__ float bias_s[H];
+  __shared__ int wsum[kFwdWaves + 1];
+  extern __shared__ __attribute__((aligned(16))) float dyn_s[];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int nt = wave & 3, kh = wave >> 2;
+  const int N = a.N, G = gridDim.x, me = blockIdx.x;
+  float *h_s = dyn_s;
+  int *off = (int *)(dyn_s + (size_t)kForestStateRows * LDH);
+  int *crow = off + N + 1, *loc = crow + 2 * N, *jp = loc + N, *lrow = jp + N, *lx = lrow + N;
+  int *loff = lx + N, *lc = loff + N + 1;
+
+  CORTEX_TRACE_KERNEL(0);
+  const int status0 = load_status(a.status);
+  float4 wr[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    wr[b] = *(const float4 *)(a.W + (size_t)(16 * nt + i16) * 2 * H + kh * H + 16 * b + 4 * g4);
+  if (tid < H) bias_s[tid] = a.b[tid];
+  const int L = *a.num_levels;
+  if (status0 != 0) return;
+  if (L < 1 || L > N || N > kForestMaxRows) {
+    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+    return;
+  }
+  // the structure, every load issued before the first LDS store (node ids
+  // of this thread's rows stay in registers)
+  int node[RPT], cv[2 * RPT], ov[RPT + 1];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) node[i] = tid + i * kFwdThreads < N ? a.level_nodes[tid + i * kFwdThreads] : -1;
+#pragma unroll
+  for (int i = 0; i < 2 * RPT; ++i) cv[i] = tid + i * kFwdThreads < 2 * N ? a.child_rows[tid + i * kFwdThreads] : -1;
+#pragma unroll
+  for (int i = 0; i <= RPT; ++i) ov[i] = tid + i * kFwdThreads <= L ? a.level_offsets[tid + i * kFwdThreads] : 0;
+#pragma unroll
+  for (int i = 0; i < 2 * RPT; ++i)
+    if (tid + i * kFwdThreads < 2 * N) crow[tid + i * kFwdThreads] = cv[i];
+#pragma unroll
+  for (int i = 0; i <= RPT; ++i)
+    if (tid + i * kFwdThreads <= L) off[tid + i * kFwdThreads] = ov[i];
+  for (int i = tid; i < N; i += kFwdThreads) loc[i] = -1;
+  for (int i = tid; i < L; i += kFwdThreads) loff[i] = 0;
+  CORTEX_TRACE_KERNEL(1);
+  __syncthreads();
+  // validation, levels and parents (several parents: the batch is not a forest)
+  int bad = 0, multi = 0;
+  for (int l = tid; l < L; l += kFwdThreads)
+    if (off[l + 1] < off[l] || (l == 0 && off[0] != 0) || (l == L - 1 && off[L] != N)) bad = 1;
+  // level of each row: the last l with off[l] <= r, by a branch-free search
+  // whose step count is the same for every row, so the rows of a thread
+  // search in lockstep
+  int rlev[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) rlev[i] = 0;
+  for (int step = 1 << (31 - __builtin_clz(L)); step > 0; step >>= 1) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int t = rlev[i] + step;
+      if (t < L && off[t] <= tid + i * kFwdThreads) rlev[i] = t;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int r = tid + i * kFwdThreads;
+    if (r >= N) continue;
+    const int start = off[rlev[i]];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int c = crow[2 * r + s];
+      if (c < -1 || c >= start || c >= N) {
+        bad = 1;
+      } else if (c >= 0) {
+        const int old = atomicCAS(&loc[c], -1, r);
+        if (old != -1 && old != r) multi = 1;
+      }
+    }
+    if (node[i] < 0 || node[i] >= N) bad = 1;
+  }
+  // input rows of this thread's leaf rows, requested now and used once the
+  // own rows are known
+  int xi[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int r = tid + i * kFwdThreads;
+    xi[i] = (r < N && rlev[i] == 0 && node[i] >= 0 && node[i] < N) ? a.x_index[node[i]] : -1;
+  }
+  if (__syncthreads_or(bad)) {
+    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+    return;
+  }
+  multi = __syncthreads_or(multi);
+  // the root of every row, by pointer jumping (two jumps per round)
+  for (int r = tid; r < N; r += kFwdThreads) jp[r] = loc[r] < 0 ? r : loc[r];
+  __syncthreads();
+  for (int round = 0; round < 16; ++round) {
+    int changed = 0, j[RPT];
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) j[i] = tid + i * kFwdThreads < N ? jp[tid + i * kFwdThreads] : 0;
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int jj = jp[jp[j[i]]];
+      if (tid + i * kFwdThreads < N && jj != j[i]) {
+        jp[tid + i * kFwdThreads] = jj;
+        changed = 1;
+      }
+    }
+    if (!__syncthreads_or(changed)) break;
+  }
+  // own rows: a slot in their level's counter; input rows of own leaves
+  int slot[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int r = tid + i * kFwdThreads;
+    slot[i] = -1;
+    if (r >= N) continue;
+    const uint32_t t = (uint32_t)jp[r] * 2654435761u;
+    const int owner = multi ? 0 : (int)(((uint64_t)t * (uint32_t)G) >> 32);
+    if (owner != me) continue;
+    slot[i] = atomicAdd(&loff[rlev[i]], 1);
+  }
+  __syncthreads();
+  // level starts of the own rows (exclusive scan of the counts)
+  int run = 0, tot = 0;
+  for (int base = 0; base < L; base += kFwdThreads) {
+    const int l = base + tid;
+    const int cnt = l < L ? loff[l] : 0;
+    const int ex = block_excl_scan(cnt, wsum, &tot);
+    if (l < L) loff[l] = run + ex;
+    run += tot;
+  }
+  const int n_own = run;
+  if (tid == 0) loff[L] = n_own;
+  if (n_own == 0) return;
+  __syncthreads();
+  int inrange = 1;
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int r = tid + i * kFwdThreads;
+    if (slot[i] < 0) continue;
+    const int k = loff[rlev[i]] + slot[i];
+    lrow[k] = r;
+    loc[r] = k;
+    if (rlev[i] == 0) {
+      if (xi[i] < -1 || xi[i] >= a.x_rows) {
+        inrange = 0;
+        xi[i] = -1;
+      }
+      lx[k] = xi[i];
+    }
+  }
+  if (!inrange) raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+  __syncthreads();
+  CORTEX_TRACE_KERNEL(2);
+  if (n_own <= kForestStateRows) {
+    // child slots of the own rows as local indices (a child has the owner of its parent)
+    for (int e = tid; e < 2 * n_own; e += kFwdThreads) {
+      const int c = crow[2 * lrow[e >> 1] + (e & 1)];
+      lc[e] = c >= 0 ? loc[c] : -1;
+    }
+    __syncthreads();
+    forest_levels<true>(a, crow, lrow, lc, lx, loff, L, h_s, wr, bias_s, C_s);
+    for (int e = tid; e < n_own * (H / 4); e += kFwdThreads) {
+      const int k = e / (H / 4), c4 = e % (H / 4);
+      *(float4 *)&a.h[(size_t)lrow[k] * H + 4 * c4] = *(const float4 *)&h_s[k * LDH + 4 * c4];
+    }
+  } else {
+    forest_levels<false>(a, crow, lrow, lc, lx, loff, L, h_s, wr, bias_s, C_s);
+  }
+  CORTEX_TRACE_KERNEL(3);
+}
+
+// ---------------------------------------------------------------------------
 // Child-sum TreeGRU and SimpleTreeGRU.
 //   h~ = sum_k h_k,  z = s(W_z x + U_z h~ + b_z),  r_k = s(W_r x + U_r h_k + b_r),
 //   h' = tanh(W_h x + U_h m + b_h) with m = sum_k r_k * h_k,
@@ -2221,6 +2486,7 @@ struct Instance {
   bool level_barrier_ok = false;   // honours FwdArgs.level_barrier
   bool level_range_ok = false;     // honours FwdArgs.level_lo / level_hi
   bool phase_barrier_ok = false;   // has two exchanges per level and honours level_barrier 2
+  bool one_group = false;          // the whole batch in one workgroup
 };
 
 constexpr size_t kStructCacheBudget = 40 * 1024;    // bytes of LDS for the cached linearization
@@ -2249,12 +2515,29 @@ static void pick_slice(bool cached, Instance &out) {
 // units per slice: the knob's value where an instance exists, else the default
 static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   const int64_t units = knob(CORTEX_KNOB_FWD_SLICE_UNITS);
-  if (cell == CORTEX_TREE_RNN && H == kLdsH && N <= kLdsMaxRows && knob(CORTEX_KNOB_FWD_NODE_GROUPS) <= 1) {
+  // TreeRNN at H = 64: the whole batch in one workgroup while it fits LDS,
+  // then one workgroup per tree, then hidden slices; the unroll knob forces
+  // the level-parallel slices (1) or one workgroup per tree (2)
+  const int64_t unroll = knob(CORTEX_KNOB_TREE_UNROLL);
+  const int64_t groups = knob(CORTEX_KNOB_FWD_NODE_GROUPS);
+  if (cell == CORTEX_TREE_RNN && H == kLdsH && unroll == 0 && N <= kLdsMaxRows && groups <= 1) {
     out.fn = tree_rnn_lds_kernel;        // one workgroup, every state in LDS
     out.J = kLdsH;
     out.threads = kFwdThreads;
+    out.one_group = true;
     out.lds = (size_t)N * kLdsHStride * sizeof(float) + (4 * (size_t)N + 2) * sizeof(int);
     return true;
+  }
+  if (cell == CORTEX_TREE_RNN && H == kLdsH && ((unroll == 0 && groups == 0) || unroll == 2)) {
+    if (N > kForestMaxRows) {
+      if (unroll == 2) return false;
+    } else {
+      out.fn = tree_rnn_forest_kernel;
+      out.J = kLdsH;
+      out.threads = kFwdThreads;
+      out.lds = forest_lds_bytes(N);
+      return true;
+    }
   }
   if (cell == CORTEX_NARY_TREELSTM && H == 256 && units == 2) {
     pick_slice<CORTEX_NARY_TREELSTM, 256, 2>(cached, out);
@@ -2371,8 +2654,11 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
     S = 4;
     if (q <= 0) q = cus / 4;
   } else {
+    // one slice (TreeRNN at H = 64) or one workgroup per tree: a node group
+    // per 16 nodes, up to one per compute unit; else fill the GPU with slices
     S = H / inst.J;
-    if (q <= 0) q = (S == 1) ? 1 : cus / S;
+    if (q <= 0) q = S == 1 ? std::min<int64_t>(cus, ((int64_t)lin->num_nodes + 15) / 16) : cus / S;
+    if (inst.one_group) q = 1;
   }
   if (q < 1) q = 1;
   const int64_t G = S * q;

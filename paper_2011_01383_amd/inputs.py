@@ -215,6 +215,31 @@ def tree_rnn_workload(seed: int, n_leaves: int = 32, H: int = 64) -> Workload:
                     x_index=x_index, x_table=leaves, W=W, b=b)
 
 
+def tree_rnn_forest_workload(seed: int, batch: int = 10, H: int = 64, leaf_lo: int = 32, leaf_hi: int = 32,
+                             shuffle: bool = False) -> Workload:
+    """A batch of TreeRNN trees (random splits, leaf counts drawn from
+    [leaf_lo, leaf_hi]); the cell and weight recipe of the one-tree workload.
+    ``shuffle`` renames the nodes by a random permutation, so the trees of the
+    batch interleave in id order."""
+    rng = np.random.default_rng(seed)
+    children, is_leaf = _binary_forest(rng, batch, leaf_lo, leaf_hi)
+    N = is_leaf.size
+    if shuffle:
+        perm = rng.permutation(N).astype(np.int32)
+        children = relabel(children, 2, perm)
+        moved = np.zeros(N, dtype=bool)
+        moved[perm] = is_leaf
+        is_leaf = moved
+    x_index = np.full(N, -1, dtype=np.int32)
+    x_index[is_leaf] = np.arange(int(is_leaf.sum()), dtype=np.int32)
+    leaves = _n(rng, (int(is_leaf.sum()), H))
+    W = _u(rng, -0.1, 0.1, (H, 2 * H))
+    b = np.zeros(H, dtype=np.float32)
+    name = "tree_rnn_h%d_%dx%d" % (H, batch, leaf_lo) if leaf_lo == leaf_hi else \
+        "tree_rnn_h%d_%dx%d-%d" % (H, batch, leaf_lo, leaf_hi)
+    return Workload(name, CELL_TREE_RNN, H, 2, children, x_index=x_index, x_table=leaves, W=W, b=b)
+
+
 def _binary_forest(rng, batch, leaf_lo, leaf_hi):
     sizes = [int(rng.integers(leaf_lo, leaf_hi + 1)) for _ in range(batch)]
     trees = [random_split_tree(rng, s) for s in sizes]

@@ -233,16 +233,23 @@ def test_dag_tile_list_overflow():
     compare_states(dw.states_by_node(), O.forward_workload(wl), "dag overflow")
 
 
+@pytest.mark.parametrize("unroll", [0, 1])
 @pytest.mark.parametrize("n_leaves", [1, 2, 7, 160, 161, 230])
-def test_tree_rnn_h64_lds_limit(n_leaves):
+def test_tree_rnn_h64_lds_limit(n_leaves, unroll):
     """TreeRNN at H = 64 runs in one workgroup with every state in LDS up to
-    320 rows (160 leaves: 319 rows) and in the slice kernel beyond; both
-    sides of the limit against the oracle."""
+    320 rows (160 leaves: 319 rows) and one workgroup per tree beyond (here
+    one tree: one busy workgroup); the unroll knob at 1 forces the
+    level-parallel slices.  Both sides of the limit against the oracle."""
     wl = I.tree_rnn_workload(600 + n_leaves, n_leaves=n_leaves, H=64)
-    announce("tree_rnn h64 %d leaves N=%d" % (n_leaves, wl.N))
-    dw = run(wl)
-    assert C.cortex_last_grid(1) == 1
-    compare_states(dw.states_by_node(), O.forward_workload(wl), "tree_rnn %d leaves" % n_leaves)
+    announce("tree_rnn h64 %d leaves N=%d unroll %d" % (n_leaves, wl.N, unroll))
+    C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL, unroll)
+    try:
+        dw = run(wl)
+        if unroll == 0:
+            assert C.cortex_last_grid(1) == (1 if wl.N <= 320 else min(256, (wl.N + 15) // 16))
+        compare_states(dw.states_by_node(), O.forward_workload(wl), "tree_rnn %d leaves" % n_leaves)
+    finally:
+        C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL, 0)
 
 
 LEVEL_SYNC_CASES = {
