@@ -215,9 +215,12 @@ def ablation(args):
     after every level, or one launch per level that reloads weights and
     structure each time; for the TreeGRU cells also a barrier after each of
     the level's two exchanges (the schedule without recursive refactoring,
-    Secs. 3.1 and 7.4).  One JSON line per (workload, mode): the forward
-    kernel time (for mode 2, the whole per-level launch sequence, which also
-    synchronizes once to read L)."""
+    Secs. 3.1 and 7.4).  Then, on the N-ary TreeLSTM and TreeFC batches, the
+    optimizations of Sec. 7.3 switched off (CORTEX_KNOB_ABLATE): model
+    persistence, leaf specialization, both, and both with one launch per
+    level.  One JSON line per (workload, mode): the forward kernel time (for
+    mode 2, the whole per-level launch sequence, which also synchronizes once
+    to read L)."""
     import torch
     from paper_2011_01383_amd import cortex as C
     from paper_2011_01383_amd import inputs as I
@@ -230,40 +233,52 @@ def ablation(args):
              (I.childsum_treegru_workload(I.BASE_SEED + 60, batch=10, H=256), 0),
              (I.childsum_treegru_workload(I.BASE_SEED + 60, batch=10, H=256, simple=True), 0),
              (I.make_workload(4), 64)]
+    runs = []
     for wl, units in cases:
-        C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
         for mode in ((0, 1, 3, 2) if wl.cell in (I.CELL_CHILDSUM_TREEGRU, I.CELL_SIMPLE_TREEGRU) else (0, 1, 2)):
-            C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)
-            line = {"workload": wl.name, "level_sync": mode, "mode": names[mode]}
-            dw = DeviceWorkload(wl)
-            dw.linearize()
-            try:
-                dw.forward()
-            except RuntimeError as e:
-                line.update({"supported": False, "reason": str(e)})
-                print(json.dumps(line))
-                continue
-            for _ in range(args.warmup):
-                dw.forward()
-            torch.cuda.synchronize()
-            assert dw.status_code() == 0
-            n = max(10, min(args.steps, 100))
-            t0 = time.perf_counter()
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            for _ in range(n):
-                dw.forward()
-            b.record(stream)
-            torch.cuda.synchronize()
-            assert dw.status_code() == 0
-            line.update({"supported": True, "forward_ms": a.elapsed_time(b) / n,
-                         "host_wall_ms": (time.perf_counter() - t0) / n * 1e3,
-                         "levels": int(dw.lin_host()["num_levels"]), "grid": C.cortex_last_grid(1)})
+            runs.append((wl, units, mode, 0))
+    # optimizations switched off one at a time, then all with one launch per
+    # level (Sec. 7.3): model persistence (bit 0), leaf specialization (bit 1)
+    for wl in (I.make_workload(1), I.treefc_workload(I.BASE_SEED + 61, batch=10, H=256)):
+        for mode, bits in ((0, 0), (0, 1), (0, 2), (0, 3), (2, 3)):
+            runs.append((wl, 0, mode, bits))
+    abl_names = {0: "", 1: "; weights read from memory at every tile", 2: "; leaf states staged and waited for",
+                 3: "; weights from memory and leaf states staged"}
+    for wl, units, mode, bits in runs:
+        C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
+        C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)
+        C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, bits)
+        line = {"workload": wl.name, "level_sync": mode, "ablate": bits, "mode": names[mode] + abl_names[bits]}
+        dw = DeviceWorkload(wl)
+        dw.linearize()
+        try:
+            dw.forward()
+        except RuntimeError as e:
+            line.update({"supported": False, "reason": str(e)})
             print(json.dumps(line))
-            sys.stdout.flush()
+            continue
+        for _ in range(args.warmup):
+            dw.forward()
+        torch.cuda.synchronize()
+        assert dw.status_code() == 0
+        n = max(10, min(args.steps, 100))
+        t0 = time.perf_counter()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            dw.forward()
+        b.record(stream)
+        torch.cuda.synchronize()
+        assert dw.status_code() == 0
+        line.update({"supported": True, "forward_ms": a.elapsed_time(b) / n,
+                     "host_wall_ms": (time.perf_counter() - t0) / n * 1e3,
+                     "levels": int(dw.lin_host()["num_levels"]), "grid": C.cortex_last_grid(1)})
+        print(json.dumps(line))
+        sys.stdout.flush()
         C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 0)
         C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
+        C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 0)
 
 
 def unroll_study(args):

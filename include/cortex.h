@@ -247,8 +247,20 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  *                                   2048 nodes, else CORTEX_E_INVAL; with
  *                                   FWD_NODE_GROUPS > 0 that many workgroups
  *                                   share the trees).
+ *   CORTEX_KNOB_ABLATE              bit mask switching optimizations off, for
+ *                                   ablation studies (Sec. 7.3; the results are
+ *                                   the same): bit 0 = no model persistence,
+ *                                   the weight slice is read from the weight
+ *                                   tensors at every tile instead of staying
+ *                                   in LDS; bit 1 = no leaf specialization,
+ *                                   leaf states are staged and their parents
+ *                                   wait for them instead of reading the
+ *                                   inputs directly.  Slice kernels only
+ *                                   (TreeRNN at H = 256 / 512, N-ary TreeLSTM;
+ *                                   bit 0 also DAG-RNN with 16-unit slices);
+ *                                   other forwards return CORTEX_E_INVAL.
  * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value
- * (or a LEVEL_SYNC value above 3, a TREE_UNROLL value above 2).
+ * (or a LEVEL_SYNC or ABLATE value above 3, a TREE_UNROLL value above 2).
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0
 #define CORTEX_KNOB_FWD_NODE_GROUPS 1
@@ -257,6 +269,7 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
 #define CORTEX_KNOB_FWD_SLICE_UNITS 4
 #define CORTEX_KNOB_LEVEL_SYNC 5
 #define CORTEX_KNOB_TREE_UNROLL 6
+#define CORTEX_KNOB_ABLATE 7
 int cortex_set_knob(int32_t knob, int64_t value);
 int64_t cortex_get_knob(int32_t knob);
 

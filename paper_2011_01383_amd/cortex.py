@@ -45,6 +45,7 @@ CORTEX_KNOB_COOPERATIVE = 3
 CORTEX_KNOB_FWD_SLICE_UNITS = 4
 CORTEX_KNOB_LEVEL_SYNC = 5
 CORTEX_KNOB_TREE_UNROLL = 6
+CORTEX_KNOB_ABLATE = 7
 
 CELL_IDS = {"tree_rnn": CORTEX_TREE_RNN, "nary_treelstm": CORTEX_NARY_TREELSTM,
             "childsum_treelstm": CORTEX_CHILDSUM_TREELSTM, "mvrnn": CORTEX_MVRNN,

@@ -8,8 +8,8 @@
 
 namespace cortex {
 
-constexpr int kKnobs = 7;
-static std::atomic<int64_t> g_knobs[kKnobs] = {{0}, {0}, {5000000}, {0}, {0}, {0}, {0}};
+constexpr int kKnobs = 8;
+static std::atomic<int64_t> g_knobs[kKnobs] = {{0}, {0}, {5000000}, {0}, {0}, {0}, {0}, {0}};
 static std::atomic<int32_t> g_last_grid[2] = {{0}, {0}};
 
 int64_t knob(int32_t which) {
@@ -57,6 +57,7 @@ extern "C" int cortex_set_knob(int32_t which, int64_t value) {
   if (which < 0 || which >= cortex::kKnobs || value < 0) return CORTEX_E_INVAL;
   if (which == CORTEX_KNOB_LEVEL_SYNC && value > 3) return CORTEX_E_INVAL;
   if (which == CORTEX_KNOB_TREE_UNROLL && value > 2) return CORTEX_E_INVAL;
+  if (which == CORTEX_KNOB_ABLATE && value > 3) return CORTEX_E_INVAL;
   cortex::g_knobs[which].store(value);
   return CORTEX_OK;
 }

@@ -90,6 +90,9 @@ struct FwdArgs {
   int32_t level_barrier;        // 1: a device-wide barrier closes every level (instead of per-datum waits alone);
                                 // 2 (TreeGRU): also one between the level's two exchanges
   float *keep;                  // TreeGRU, level_barrier 2: z, W_h x + b_h and h~ per (row, unit), [3][N][H]
+  int32_t ablate;               // slice kernel, for ablation studies: bit 0 (its own instance) reads the weight slice from
+                                // memory at every tile instead of LDS; bit 1 stages the leaf states and
+                                // has parents wait for them instead of reading their inputs directly
 };
 
 // ---------------------------------------------------------------------------
@@ -192,6 +195,21 @@ __device__ void load_weight_slice(const FwdArgs &a, int hbase, float *W_s, float
     }
     bias_s[m] = bv;
   }
+}
+
+// Four consecutive columns c .. c+3 of weight-slice row m (the values
+// load_weight_slice places in LDS), read from the weight tensors.
+template <int CELL, int H, int J>
+__device__ __forceinline__ float4 weight_slice_at(const FwdArgs &a, int hbase, int m, int c) {
+  using D = Dims<CELL, H, J>;
+  if (m >= D::GJ || c >= D::KA) return make_float4(0.f, 0.f, 0.f, 0.f);
+  const int g = m / J, hj = hbase + m % J, sg = c / H, o = c % H;
+  const float *src = nullptr;
+  if (CELL == CORTEX_TREE_RNN) src = a.W + (size_t)hj * 2 * H + sg * H;
+  if (CELL == CORTEX_NARY_TREELSTM) src = a.U + ((size_t)(sg * 5 + g) * H + hj) * H;
+  if (CELL == CORTEX_CHILDSUM_TREELSTM) src = (sg == 0 ? a.W : a.U) + ((size_t)childsum_gate(g) * H + hj) * H;
+  if (CELL == CELL_DAG) src = (sg == 0 ? a.W : a.U + (size_t)(sg - 1) * H * H) + (size_t)hj * H;
+  return *(const float4 *)(src + o);
 }
 
 // Fills the structure cache in LDS (kCached) or points at global memory.
@@ -399,7 +417,7 @@ __device__ bool setup_sources(const FwdArgs &a, int *cache, int &L, const int *&
         bad = 1;
         c = -1;
       }
-      if (SC::kLeafX && c >= 0 && c < off1) c = xr[c] >= 0 ? -2 - xr[c] : -1;
+      if (SC::kLeafX && !(a.ablate & 2) && c >= 0 && c < off1) c = xr[c] >= 0 ? -2 - xr[c] : -1;
       if (s < K) cd[r * SEGS + (SC::kDag ? s + 1 : s)] = c;
     }
   }
@@ -440,7 +458,7 @@ __device__ void stage_chunk_codes(const FwdArgs &a, ChunkSrc &cs, int u0, int nt
         raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
         c = -1;
       }
-      if (SC::kLeafX && c >= 0 && c < off1) {     // a leaf child: its input row
+      if (SC::kLeafX && !(a.ablate & 2) && c >= 0 && c < off1) {     // a leaf child: its input row
         const int v = a.level_nodes[c];
         int xi = -1;
         if (v < 0 || v >= a.N) raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
@@ -458,9 +476,11 @@ __device__ void stage_chunk_codes(const FwdArgs &a, ChunkSrc &cs, int u0, int nt
 
 // Leaf level of TreeRNN / N-ary TreeLSTM, spread over every thread of the
 // launch: h = input row (or 0), c = 0.  Nothing waits on these rows (parents
-// read leaf children from the input table), so they are not staged.
+// read leaf children from the input table), so they are not staged, except
+// under ablation bit 1, where parents wait for them like any other child.
 template <int H, bool kWithC>
-__device__ void write_leaf_outputs(const FwdArgs &a, const int *xrow, int r1) {
+__device__ void write_leaf_outputs(const FwdArgs &a, const int *xrow, int r1, const TagBuf &hs, const TagBuf &cs,
+                                   uint32_t tag) {
   constexpr int H4 = H / 4;
   const int total = r1 * H4;
   for (int e = blockIdx.x * kFwdThreads + threadIdx.x; e < total; e += gridDim.x * kFwdThreads) {
@@ -479,6 +499,16 @@ __device__ void write_leaf_outputs(const FwdArgs &a, const int *xrow, int r1) {
     const float4 v = xr >= 0 ? *(const float4 *)&a.x_table[(size_t)xr * H + 4 * c4] : make_float4(0.f, 0.f, 0.f, 0.f);
     *(float4 *)&a.h[(size_t)e * 4] = v;
     if (kWithC) *(float4 *)&a.c[(size_t)e * 4] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (a.ablate & 2) {
+      hs.store1((uint32_t)e * 4u + 0u, v.x, tag);
+      hs.store1((uint32_t)e * 4u + 1u, v.y, tag);
+      hs.store1((uint32_t)e * 4u + 2u, v.z, tag);
+      hs.store1((uint32_t)e * 4u + 3u, v.w, tag);
+      if (kWithC) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cs.store1((uint32_t)e * 4u + q, 0.f, tag);
+      }
+    }
   }
 }
 
@@ -506,7 +536,7 @@ struct Frag {
 // so the four lane groups of a row read one 128-byte span of staged pairs
 // with each pair of load instructions.
 // ---------------------------------------------------------------------------
-template <int CELL, int H, int J, bool kCached>
+template <int CELL, int H, int J, bool kCached, bool kWeightsFromMemory = false>
 __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   using D = Dims<CELL, H, J>;
   constexpr int GJ = D::GJ, MPAD = D::MPAD, NT = D::NT, LDW = D::LDW, KW = D::KW, NB = D::NB, KA = D::KA;
@@ -564,7 +594,7 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
       return;
     }
     if (kLeafInputs && l == 0) {
-      write_leaf_outputs<H, kLstm>(a, kCached ? xrow : nullptr, r1);
+      write_leaf_outputs<H, kLstm>(a, kCached ? xrow : nullptr, r1, hs, cs, tag);
       continue;
     }
     const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
@@ -671,15 +701,34 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
       floatx4 acc0[NT], acc1[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc0[nt] = acc1[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      const float *brow = &W_s[i16 * LDW + kw + 4 * g4];
+      if constexpr (!kWeightsFromMemory) {
+        const float *brow = &W_s[i16 * LDW + kw + 4 * g4];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const float4 av = f[b].value(code_b(cd, b) >= 0);
+        for (int b = 0; b < NB; ++b) {
+          const float4 av = f[b].value(code_b(cd, b) >= 0);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const float4 bv = *(const float4 *)(brow + nt * 16 * LDW + 16 * b);
-          if (b & 1) acc1[nt] = mfma_k16(av, bv, acc1[nt]);
-          else acc0[nt] = mfma_k16(av, bv, acc0[nt]);
+          for (int nt = 0; nt < NT; ++nt) {
+            const float4 bv = *(const float4 *)(brow + nt * 16 * LDW + 16 * b);
+            if (b & 1) acc1[nt] = mfma_k16(av, bv, acc1[nt]);
+            else acc0[nt] = mfma_k16(av, bv, acc0[nt]);
+          }
+        }
+      } else {
+        // ablation: no model persistence; the same weight-slice values,
+        // read from the weight tensors at every tile
+        float4 bw[NB][NT];
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) bw[b][nt] = weight_slice_at<CELL, H, J>(a, hbase, nt * 16 + i16, kw + 16 * b + 4 * g4);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const float4 av = f[b].value(code_b(cd, b) >= 0);
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            if (b & 1) acc1[nt] = mfma_k16(av, bw[b][nt], acc1[nt]);
+            else acc0[nt] = mfma_k16(av, bw[b][nt], acc0[nt]);
+          }
         }
       }
       CORTEX_TRACE_WAVE(l);
@@ -2487,6 +2536,7 @@ struct Instance {
   bool level_range_ok = false;     // honours FwdArgs.level_lo / level_hi
   bool phase_barrier_ok = false;   // has two exchanges per level and honours level_barrier 2
   bool one_group = false;          // the whole batch in one workgroup
+  int ablate_bits = 0;             // FwdArgs.ablate bits the kernel honours
 };
 
 constexpr size_t kStructCacheBudget = 40 * 1024;    // bytes of LDS for the cached linearization
@@ -2506,10 +2556,15 @@ static void pick_slice(bool cached, Instance &out) {
   out.J = J;
   out.threads = kFwdThreads;
   out.level_barrier_ok = out.level_range_ok = true;
-  if constexpr (CELL == CORTEX_CHILDSUM_TREELSTM)
+  if constexpr (CELL == CORTEX_CHILDSUM_TREELSTM) {
     out.fn = cached ? childsum_forward_kernel<H, true> : childsum_forward_kernel<H, false>;
-  else
-    out.fn = cached ? slice_forward_kernel<CELL, H, J, true> : slice_forward_kernel<CELL, H, J, false>;
+  } else {
+    if (knob(CORTEX_KNOB_ABLATE) & 1)       // the instance without model persistence
+      out.fn = cached ? slice_forward_kernel<CELL, H, J, true, true> : slice_forward_kernel<CELL, H, J, false, true>;
+    else
+      out.fn = cached ? slice_forward_kernel<CELL, H, J, true> : slice_forward_kernel<CELL, H, J, false>;
+    out.ablate_bits = SrcCfg<CELL>::kLeafX ? 3 : 1;
+  }
 }
 
 // units per slice: the knob's value where an instance exists, else the default
@@ -2681,6 +2736,9 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   if ((sync_mode == 1 && !inst.level_barrier_ok) || (sync_mode == 2 && !inst.level_range_ok) ||
       (sync_mode == 3 && !inst.phase_barrier_ok))
     return CORTEX_E_INVAL;
+  const int64_t ablate = knob(CORTEX_KNOB_ABLATE);
+  if (ablate & ~(int64_t)inst.ablate_bits) return CORTEX_E_INVAL;
+  a.ablate = (int32_t)ablate;
   set_last_grid(1, (int32_t)G);
   if (sync_mode == 1) a.level_barrier = 1;
   if (sync_mode == 3) a.level_barrier = 2;

@@ -84,7 +84,15 @@ def test_level_sync_knob_range(lib):
     for v in (3, 2, 1, 0):
         assert C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, v) == C.CORTEX_OK
         assert C.cortex_get_knob(C.CORTEX_KNOB_LEVEL_SYNC) == v
-    assert C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL + 1, 0) == C.CORTEX_E_INVAL
+    assert C.cortex_set_knob(C.CORTEX_KNOB_ABLATE + 1, 0) == C.CORTEX_E_INVAL
+
+
+def test_ablate_knob_range(lib):
+    assert C.cortex_get_knob(C.CORTEX_KNOB_ABLATE) == 0
+    assert C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 4) == C.CORTEX_E_INVAL
+    for v in (3, 2, 1, 0):
+        assert C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, v) == C.CORTEX_OK
+        assert C.cortex_get_knob(C.CORTEX_KNOB_ABLATE) == v
 
 
 def test_tree_unroll_knob_range(lib):

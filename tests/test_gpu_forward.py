@@ -24,6 +24,7 @@ def _gpu():
     C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, 0)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
     C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 0)
+    C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 0)
 
 
 def run(wl, groups=0):
@@ -284,6 +285,56 @@ def test_level_sync_modes_change_only_the_schedule(name, mode):
     got = run(wl).states_by_node()
     for key in ref:
         assert np.array_equal(ref[key], got[key]), key
+
+
+ABLATE_CASES = {
+    "nary": (lambda: cached_workload(1, 0), 0, 3),
+    "nary_units2": (lambda: I.nary_treelstm_workload(48, batch=4, H=256), 2, 3),
+    "nary_uncached": (lambda: I.nary_treelstm_workload(32, batch=120, H=256), 0, 3),
+    "tree_rnn_h256": (lambda: I.tree_rnn_workload(41, n_leaves=37, H=256), 0, 3),
+    "tree_rnn_h512": (lambda: I.tree_rnn_workload(49, n_leaves=23, H=512), 0, 3),
+    "dag_h256_units16": (lambda: I.dagrnn_workload(42, n_grids=3, rows=9, cols=7, H=256), 16, 1),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ABLATE_CASES))
+@pytest.mark.parametrize("bits", [1, 2, 3])
+def test_ablations_change_only_the_schedule(name, bits):
+    """Weights read from memory at every tile (bit 0) and leaf states staged
+    and waited for (bit 1) feed the same values to the same contraction
+    order, so the states are bitwise identical; a kernel without the
+    ablation rejects it on the host."""
+    make, units, supported = ABLATE_CASES[name]
+    wl = make()
+    announce("ablate %d %s N=%d" % (bits, name, wl.N))
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
+    ref = run(wl).states_by_node()
+    C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, bits)
+    if bits & ~supported:
+        dw = DeviceWorkload(wl)
+        dw.linearize()
+        with pytest.raises(RuntimeError, match="host code %d" % C.CORTEX_E_INVAL):
+            dw.forward()
+        assert dw.status_code() == 0
+        return
+    for sync in (0, 2):
+        C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, sync)
+        got = run(wl).states_by_node()
+        for key in ref:
+            assert np.array_equal(ref[key], got[key]), (key, sync)
+
+
+@pytest.mark.parametrize("k", [0, 2, 3])
+def test_ablations_unsupported(k):
+    """Kernels other than the slice kernel have no ablation switches."""
+    wl = cached_workload(k, 0)
+    announce("ablate unsupported on workload %d" % k)
+    C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 1)
+    dw = DeviceWorkload(wl)
+    dw.linearize()
+    with pytest.raises(RuntimeError, match="host code %d" % C.CORTEX_E_INVAL):
+        dw.forward()
+    assert dw.status_code() == 0
 
 
 @pytest.mark.parametrize("k", [0, 3])
