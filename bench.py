@@ -220,7 +220,8 @@ def ablation(args):
     persistence, leaf specialization, both, and both with one launch per
     level.  One JSON line per (workload, mode): the forward kernel time (for
     mode 2, the whole per-level launch sequence, which also synchronizes once
-    to read L)."""
+    to read L), the median of five rounds in which every schedule of a
+    workload is timed once."""
     import torch
     from paper_2011_01383_amd import cortex as C
     from paper_2011_01383_amd import inputs as I
@@ -244,41 +245,61 @@ def ablation(args):
             runs.append((wl, 0, mode, bits))
     abl_names = {0: "", 1: "; weights read from memory at every tile", 2: "; leaf states staged and waited for",
                  3: "; weights from memory and leaf states staged"}
-    for wl, units, mode, bits in runs:
+    def knobs(units, mode, bits):
         C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
         C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)
         C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, bits)
-        line = {"workload": wl.name, "level_sync": mode, "ablate": bits, "mode": names[mode] + abl_names[bits]}
-        dw = DeviceWorkload(wl)
-        dw.linearize()
-        try:
-            dw.forward()
-        except RuntimeError as e:
-            line.update({"supported": False, "reason": str(e)})
+
+    n = max(10, min(args.steps, 100))
+    rounds = 5
+    groups = []                           # runs of one workload, timed interleaved
+    for run in runs:
+        if groups and groups[-1][0][0] is run[0]:
+            groups[-1].append(run)
+        else:
+            groups.append([run])
+    for group in groups:
+        live = []
+        for wl, units, mode, bits in group:
+            knobs(units, mode, bits)
+            line = {"workload": wl.name, "level_sync": mode, "ablate": bits, "mode": names[mode] + abl_names[bits]}
+            dw = DeviceWorkload(wl)
+            dw.linearize()
+            try:
+                dw.forward()
+            except RuntimeError as e:
+                line.update({"supported": False, "reason": str(e)})
+                live.append((line, None, (units, mode, bits), []))
+                continue
+            line["grid"] = C.cortex_last_grid(1)
+            for _ in range(args.warmup):
+                dw.forward()
+            torch.cuda.synchronize()
+            assert dw.status_code() == 0
+            live.append((line, dw, (units, mode, bits), []))
+        # every schedule of the workload timed once per round, so slow drifts
+        # of the machine touch them alike; the median of the rounds is reported
+        for _ in range(rounds):
+            for line, dw, kb, times in live:
+                if dw is None:
+                    continue
+                knobs(*kb)
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for _ in range(n):
+                    dw.forward()
+                b.record(stream)
+                torch.cuda.synchronize()
+                assert dw.status_code() == 0
+                times.append(a.elapsed_time(b) / n)
+        for line, dw, kb, times in live:
+            if dw is not None:
+                line.update({"supported": True, "forward_ms": float(np.median(times)), "forward_ms_min": min(times),
+                             "forward_ms_rounds": times, "levels": int(dw.lin_host()["num_levels"])})
             print(json.dumps(line))
-            continue
-        for _ in range(args.warmup):
-            dw.forward()
-        torch.cuda.synchronize()
-        assert dw.status_code() == 0
-        n = max(10, min(args.steps, 100))
-        t0 = time.perf_counter()
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(n):
-            dw.forward()
-        b.record(stream)
-        torch.cuda.synchronize()
-        assert dw.status_code() == 0
-        line.update({"supported": True, "forward_ms": a.elapsed_time(b) / n,
-                     "host_wall_ms": (time.perf_counter() - t0) / n * 1e3,
-                     "levels": int(dw.lin_host()["num_levels"]), "grid": C.cortex_last_grid(1)})
-        print(json.dumps(line))
-        sys.stdout.flush()
-        C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 0)
-        C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
-        C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 0)
+            sys.stdout.flush()
+        knobs(0, 0, 0)
 
 
 def unroll_study(args):

@@ -19,9 +19,11 @@
  *                           are ordered per datum: each state element is
  *                           also published as a (value, launch tag) pair in
  *                           the workspace and a consumer waits for exactly
- *                           the elements it reads (a TreeRNN batch small
- *                           enough for one workgroup keeps its states in
- *                           LDS and orders levels with workgroup barriers).
+ *                           the elements it reads.  TreeRNN at H = 64
+ *                           runs the whole batch, or each tree (unrolled
+ *                           recursion, Sec. 3.1), in one workgroup with its
+ *                           states in LDS and levels ordered by workgroup
+ *                           barriers.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -197,7 +199,9 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
 
 /*
  * Launch knobs, process-wide, read at each launch.  They change the schedule,
- * never the results.
+ * not what is computed: outputs are bitwise those of the defaults, except where
+ * a knob picks a kernel that adds partial sums in another order (DAG-RNN slice
+ * width, TREE_UNROLL = 1), whose states agree to rounding.
  *   CORTEX_KNOB_LIN_BLOCKS          workgroups of the linearizer (0 = chosen from N)
  *   CORTEX_KNOB_FWD_NODE_GROUPS     node groups of the forward; workgroups =
  *                                   hidden slices x node groups (0 = fill the
