@@ -160,8 +160,9 @@ size_t cortex_forward_workspace_bytes(int32_t cell, int32_t N, int32_t H);
  * Sec. 4.1: a specialized leaf loop, then one fused step per level).
  *   cell        CORTEX_TREE_RNN / NARY_TREELSTM / CHILDSUM_TREELSTM / MVRNN /
  *               CHILDSUM_TREEGRU / SIMPLE_TREEGRU
- *   H           hidden size: 64, 256 or 512 for TREE_RNN; 64 or 256 for NARY, the
- *               CHILDSUM cells and the TREEGRU cells; 64 for MVRNN
+ *   H           hidden size: 64, 256 or 512 for TREE_RNN, the CHILDSUM TreeLSTM
+ *               and the TREEGRU cells; 64 or 256 for NARY; 64 or 128 for MVRNN
+ *               (other sizes return CORTEX_E_INVAL and enqueue nothing)
  *   lin         the output of cortex_linearize (K must be 2, or 1..4 for the
  *               child-sum TreeLSTM and TreeGRU cells)
  *   d_x_table   [x_rows, H] float32: leaf vectors or an embedding table
@@ -184,7 +185,7 @@ int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const 
  * Forward pass of the DAG-RNN cell (recursive part of DAG-RNN, Sec. 7.1):
  *   h(v) = tanh(W x(v) + U_0 h(slot 0) + U_1 h(slot 1) + b)
  * (for image grids slot 0 is the node above, slot 1 the node to the left).
- *   H      256 (or 64)
+ *   H      64, 256 or 512
  *   lin    the output of cortex_linearize with K == 2
  *   d_x    [N, H] float32 input by NODE ID
  *   d_W    [H, H];  d_U [2, H, H] (slot 0 then slot 1);  d_b [H]

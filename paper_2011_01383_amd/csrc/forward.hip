@@ -1287,6 +1287,10 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
   using D = Dims<CORTEX_CHILDSUM_TREELSTM, H, J>;
   constexpr int LDW = D::LDW, NBX = D::NBX, NBE = D::NBE, KWX = D::KWX, KWE = D::KWE;
   constexpr int ZW = 7 * J;                 // per row: i, o, u, then f_k * c_k for 4 slots
+  // The next tile's operands are requested during the current tile while two
+  // operand sets fit the registers; at H = 512 one set (the 16 x 4 child-slot
+  // rows alone take 128 VGPRs as tagged pairs) is loaded per tile instead.
+  constexpr bool kPrefetch = H <= 256;
   static_assert(D::MPAD == 16 && kTileM * ZW <= kFwdThreads, "one n-tile, one gate item per thread");
 
   __shared__ __attribute__((aligned(16))) float W_s[16 * LDW];
@@ -1577,17 +1581,25 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
         stage_chunk(a, chunk, u0, (u_last - u0) / Q + 1, Q, r0, r1);
         __syncthreads();
       }
-      issue(u0, ta);
-      CORTEX_TRACE_POINT(l, 6);
-      for (int u = u0;;) {
-        bool more = u + Q <= u_last;
-        process(u, ta, more, tb);
-        u += Q;
-        if (!more) break;
-        more = u + Q <= u_last;
-        process(u, tb, more, ta);
-        u += Q;
-        if (!more) break;
+      if constexpr (kPrefetch) {
+        issue(u0, ta);
+        CORTEX_TRACE_POINT(l, 6);
+        for (int u = u0;;) {
+          bool more = u + Q <= u_last;
+          process(u, ta, more, tb);
+          u += Q;
+          if (!more) break;
+          more = u + Q <= u_last;
+          process(u, tb, more, ta);
+          u += Q;
+          if (!more) break;
+        }
+      } else {
+        for (int u = u0; u <= u_last; u += Q) {
+          issue(u, ta);
+          CORTEX_TRACE_POINT(l, 6);
+          process(u, ta, false, ta);
+        }
       }
     }
     CORTEX_TRACE_POINT(l, 5);
@@ -2279,31 +2291,44 @@ __device__ __forceinline__ bool level_bounds(const FwdArgs &a, int l, int &r0, i
 }
 
 // ---------------------------------------------------------------------------
-// MV-RNN (d = 64): p = tanh(W [B a; A b]), P = W_M [A; B].
-// Node-parallel: workgroup b owns output rows [16*(b%4), 16*(b%4)+16) of every
-// node it processes (its 16 rows of W and W_M stay in LDS), and node group
-// b/4 takes nodes q, q + G/4, ... of each level.  P = W_M[A;B] runs on MFMA
-// with [A;B] staged in LDS; the matrix-vector products use VALU.  Levels are
+// MV-RNN (d = 64 or 128): p = tanh(W [B a; A b]), P = W_M [A; B].
+// Node-parallel: with RB = d / 16 row blocks, workgroup b owns output rows
+// [16*(b%RB), 16*(b%RB)+16) of every node it processes (its 16 rows of W_M in
+// LDS, its share of the same rows of W in registers), and node group b/RB
+// takes nodes q, q + G/RB, ... of each level.  P = W_M[A;B] runs on MFMA with
+// [A;B] staged in LDS (wave w computes output columns 16w .. 16w+15, so a
+// workgroup has d/16 waves); the matrix-vector products use VALU.  Levels are
 // ordered per datum, as in the slice kernels: every element of p and P is
 // also published as a (value, launch tag) pair, a workgroup waits for
 // exactly the child vectors and matrices it stages, and a leaf child is read
 // from the inputs (its state is the given (a, A)), so nothing waits on the
 // leaf level.  Child rows and the input rows of the leaves are cached in LDS
-// for batches of up to kMvCacheRows rows.
+// for batches of up to MvDims<D>::kCacheRows rows.
 // ---------------------------------------------------------------------------
-constexpr int kMvThreads = 256;
-constexpr int kMvD = 64;
-constexpr int kMvLd = 2 * kMvD + 4;        // W / W_M slice row stride
-constexpr int kMvAb = kMvD + 1;            // [A;B] row stride (odd: row-wise reads spread banks)
-constexpr int kMvGroups = 2 * kMvD * kMvD / 4 / kMvThreads;   // float4 groups of [A;B] per thread
-constexpr int kMvCacheRows = 3072;
+template <int D>
+struct MvDims {
+  static constexpr int kThreads = 4 * D;                 // d/16 waves
+  static constexpr int RB = D / 16;                      // row blocks of P per node
+  static constexpr int kLd = 2 * D + 4;                  // W_M slice row stride
+  static constexpr int kAb = D + 1;                      // [A;B] row stride (odd: row-wise reads spread banks)
+  static constexpr int kGroups = 2 * D * D / 4 / kThreads;   // float4 groups of [A;B] per thread
+  static constexpr int kSide = D * D / 4;                // float4 groups per matrix
+  static constexpr int kParts = kThreads / 16;           // partial sums per output of p (8 terms each)
+  // the cache (3 ints per row) must fit beside the static LDS: 36 KB at
+  // d = 64, 7.5 KB at d = 128 (where [A;B] alone takes 129 KB)
+  static constexpr int kCacheRows = D == 64 ? 3072 : 640;
+  static_assert(kParts * 8 == 2 * D && kGroups * kThreads * 4 == 2 * D * D, "MV-RNN tiling");
+};
+constexpr int kMvD = 64, kMvD2 = 128;
 
-__global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
-  constexpr int D = kMvD;
-  constexpr int WPER = 16 * 2 * D / kMvThreads;
-  __shared__ float WM_s[16 * kMvLd];
-  __shared__ float Wv_s[16 * kMvLd];
-  __shared__ float AB_s[2 * D * kMvAb];
+template <int D>
+__global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdArgs a) {
+  using M = MvDims<D>;
+  constexpr int kThreads = M::kThreads, RB = M::RB, kLd = M::kLd, kAb = M::kAb, kGroups = M::kGroups;
+  constexpr int kSide = M::kSide, kParts = M::kParts;
+  constexpr int WPER = 16 * 2 * D / kThreads;
+  __shared__ float WM_s[16 * kLd];
+  __shared__ float AB_s[2 * D * kAb];
   __shared__ float vec_s[2 * D];          // a (left vector), b (right vector)
   __shared__ float bab_s[2 * D];          // [B a; A b]
   __shared__ int src_s[2][2];             // per child slot: staged row or -1, input row or -1
@@ -2311,31 +2336,34 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
-  const int rblk = blockIdx.x & 3, ngroup = blockIdx.x >> 2, ngroups = gridDim.x >> 2;
+  const int rblk = blockIdx.x % RB, ngroup = blockIdx.x / RB, ngroups = gridDim.x / RB;
   const int N = a.N;
-  const bool cached = N <= kMvCacheRows;
+  const bool cached = N <= M::kCacheRows;
   const uint32_t tag = a.tag;
   const TagBuf hs(a.hs, (uint32_t)N * D * 8);
   const TagBuf ps(a.cs, (uint32_t)N * D * D * 8);
   const InBuf xv(a.x_table, a.x_table ? (uint32_t)a.x_rows * D * 4 : 0u);
   const InBuf xm(a.leaf_mat, a.leaf_mat ? (uint32_t)a.x_rows * D * D * 4 : 0u);
+  // p: output o of this workgroup's 16, partial sum over columns [8 part, 8 part + 8)
+  const int po = tid / kParts, ppart = tid % kParts;
 
   // status, level count and weights requested together
   const int status0 = load_status(a.status);
   const int L = *a.num_levels;
+  float wv[8];                            // W[16 rblk + po][8 ppart .. +8], for the whole launch
   {
-    float wm[WPER], wv[WPER];
+    float wm[WPER];
 #pragma unroll
     for (int k = 0; k < WPER; ++k) {
-      const int idx = tid + k * kMvThreads, r = idx / (2 * D), c = idx % (2 * D);
+      const int idx = tid + k * kThreads, r = idx / (2 * D), c = idx % (2 * D);
       wm[k] = a.W_M[(size_t)(rblk * 16 + r) * 2 * D + c];
-      wv[k] = a.W[(size_t)(rblk * 16 + r) * 2 * D + c];
     }
 #pragma unroll
+    for (int kk = 0; kk < 8; ++kk) wv[kk] = a.W[(size_t)(rblk * 16 + po) * 2 * D + ppart * 8 + kk];
+#pragma unroll
     for (int k = 0; k < WPER; ++k) {
-      const int idx = tid + k * kMvThreads, r = idx / (2 * D), c = idx % (2 * D);
-      WM_s[r * kMvLd + c] = wm[k];
-      Wv_s[r * kMvLd + c] = wv[k];
+      const int idx = tid + k * kThreads, r = idx / (2 * D), c = idx % (2 * D);
+      WM_s[r * kLd + c] = wm[k];
     }
   }
   if (status0 != 0) return;
@@ -2363,7 +2391,7 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
   };
   int *crow_c = mv_cache, *leafx_c = mv_cache + 2 * N;
   if (cached) {
-    for (int i = tid; i < 2 * N; i += kMvThreads) {
+    for (int i = tid; i < 2 * N; i += kThreads) {
       int c = a.child_rows[i];
       if (c < -1 || c >= N) {
         raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
@@ -2371,7 +2399,7 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
       }
       crow_c[i] = c;
     }
-    for (int r = tid; r < off1; r += kMvThreads) leafx_c[r] = leaf_input(r);
+    for (int r = tid; r < off1; r += kThreads) leafx_c[r] = leaf_input(r);
     __syncthreads();
   }
 
@@ -2383,7 +2411,7 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
       const float4 val = as_float4(xv.load4(xi >= 0 ? (uint32_t)((xi * D + tid * 4) * 4) : kNoSource));
       *(float4 *)&a.h[(size_t)r * D + tid * 4] = val;
     }
-    for (int e = tid; e < D * D / 4; e += kMvThreads) {
+    for (int e = tid; e < D * D / 4; e += kThreads) {
       const float4 val = as_float4(xm.load4(xi >= 0 ? (uint32_t)((xi * D * D + e * 4) * 4) : kNoSource));
       *(float4 *)&a.c[(size_t)r * D * D + e * 4] = val;
     }
@@ -2403,12 +2431,12 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
         src_s[tid][1] = (cr >= 0 && cr < off1) ? (cached ? leafx_c[cr] : leaf_input(cr)) : -1;
       }
       __syncthreads();
-      // [A; B]: float4 group f = tid + k*256 is side f / 1024 (0 = A from
-      // slot 0, 1 = B from slot 1), element 4 (f mod 1024) of that matrix
-      u32x4 lo[kMvGroups], hi[kMvGroups];
+      // [A; B]: float4 group f = tid + k*kThreads is side f / kSide (0 = A
+      // from slot 0, 1 = B from slot 1), element 4 (f mod kSide) of that matrix
+      u32x4 lo[kGroups], hi[kGroups];
 #pragma unroll
-      for (int k = 0; k < kMvGroups; ++k) {
-        const int f = tid + k * kMvThreads, side = f >> 10, e4 = (f & 1023) * 4;
+      for (int k = 0; k < kGroups; ++k) {
+        const int f = tid + k * kThreads, side = f / kSide, e4 = (f % kSide) * 4;
         const int st = src_s[side][0], xi = src_s[side][1];
         if (st >= 0) {
           const uint32_t so = (uint32_t)(st * D * D + e4) * 8u;
@@ -2419,8 +2447,8 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
           hi[k] = u32x4{0u, 0u, 0u, 0u};
         }
       }
-      // vectors: thread t < 128 takes element t mod 64 of side t / 64
-      const int vside = (tid >> 6) & 1, vk = tid & 63;
+      // vectors: thread t < 2d takes element t mod d of side t / d
+      const int vside = (tid / D) & 1, vk = tid % D;
       const int vst = src_s[vside][0], vxi = src_s[vside][1];
       u32x2 vv = {0u, 0u};
       if (tid < 2 * D) {
@@ -2430,8 +2458,8 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
       auto ready = [&]() -> bool {
         bool ok = !(tid < 2 * D && vst >= 0) || vv.y == tag;
 #pragma unroll
-        for (int k = 0; k < kMvGroups; ++k) {
-          const int side = (tid + k * kMvThreads) >> 10;
+        for (int k = 0; k < kGroups; ++k) {
+          const int side = (tid + k * kThreads) / kSide;
           if (src_s[side][0] >= 0) ok = ok && lo[k].y == tag && lo[k].w == tag && hi[k].y == tag && hi[k].w == tag;
         }
         return ok;
@@ -2441,10 +2469,10 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
         for (;;) {
           __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-          for (int k = 0; k < kMvGroups; ++k) {
-            const int f = tid + k * kMvThreads, side = f >> 10, st = src_s[side][0];
+          for (int k = 0; k < kGroups; ++k) {
+            const int f = tid + k * kThreads, side = f / kSide, st = src_s[side][0];
             if (st >= 0 && !(lo[k].y == tag && lo[k].w == tag && hi[k].y == tag && hi[k].w == tag)) {
-              const uint32_t so = (uint32_t)(st * D * D + (f & 1023) * 4) * 8u;
+              const uint32_t so = (uint32_t)(st * D * D + (f % kSide) * 4) * 8u;
               lo[k] = ps.load2_at(so);
               hi[k] = ps.load2_at(so + 16u);
             }
@@ -2464,12 +2492,12 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
         }
       }
 #pragma unroll
-      for (int k = 0; k < kMvGroups; ++k) {
-        const int f = tid + k * kMvThreads, side = f >> 10, e4 = (f & 1023) * 4;
+      for (int k = 0; k < kGroups; ++k) {
+        const int f = tid + k * kThreads, side = f / kSide, e4 = (f % kSide) * 4;
         const bool staged = src_s[side][0] >= 0;
         const float4 val = make_float4(as_float(lo[k].x), as_float(staged ? lo[k].z : lo[k].y),
                                        as_float(staged ? hi[k].x : lo[k].z), as_float(staged ? hi[k].z : lo[k].w));
-        float *dst = &AB_s[(side * D + e4 / D) * kMvAb + e4 % D];
+        float *dst = &AB_s[(side * D + e4 / D) * kAb + e4 % D];
         dst[0] = val.x;
         dst[1] = val.y;
         dst[2] = val.z;
@@ -2480,10 +2508,10 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
         gave_up = 1;
         break;
       }
-      // [B a; A b]: thread k<64 -> (B a)[k] = sum_n B[k][n] a[n];  k>=64 -> (A b)[k-64]
+      // [B a; A b]: thread k<d -> (B a)[k] = sum_n B[k][n] a[n];  k>=d -> (A b)[k-d]
       if (tid < 2 * D) {
         const int k = tid % D;
-        const float *mrow = (tid < D) ? &AB_s[(D + k) * kMvAb] : &AB_s[k * kMvAb];
+        const float *mrow = (tid < D) ? &AB_s[(D + k) * kAb] : &AB_s[k * kAb];
         const float *vw = (tid < D) ? &vec_s[0] : &vec_s[D];
         float s = 0.f;
         for (int n2 = 0; n2 < D; ++n2) s += mrow[n2] * vw[n2];
@@ -2492,8 +2520,8 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
       // P rows [16*rblk, +16) = W_M[rows] [A;B]: wave w -> output columns 16w..16w+15
       floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
       for (int k0 = 0; k0 < 2 * D; k0 += 8) {
-        acc0 = mfma16x16x4(WM_s[i16 * kMvLd + k0 + g4], AB_s[(k0 + g4) * kMvAb + wave * 16 + i16], acc0);
-        acc1 = mfma16x16x4(WM_s[i16 * kMvLd + k0 + 4 + g4], AB_s[(k0 + 4 + g4) * kMvAb + wave * 16 + i16], acc1);
+        acc0 = mfma16x16x4(WM_s[i16 * kLd + k0 + g4], AB_s[(k0 + g4) * kAb + wave * 16 + i16], acc0);
+        acc1 = mfma16x16x4(WM_s[i16 * kLd + k0 + 4 + g4], AB_s[(k0 + 4 + g4) * kAb + wave * 16 + i16], acc1);
       }
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
@@ -2503,15 +2531,15 @@ __global__ void __launch_bounds__(kMvThreads) mvrnn_forward_kernel(FwdArgs a) {
         a.c[el] = pv;
       }
       __syncthreads();
-      // p rows: 16 outputs x 16 partial sums of 8 terms, reduced over 16 lanes
+      // p rows: 16 outputs x kParts partial sums of 8 terms, reduced over
+      // kParts consecutive lanes
       {
-        const int o = tid >> 4, part = tid & 15;
         float s = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) s += Wv_s[o * kMvLd + part * 8 + kk] * bab_s[part * 8 + kk];
-        for (int sh = 8; sh > 0; sh >>= 1) s += __shfl_xor(s, sh, 16);
-        if (part == 0) {
-          const uint32_t el = (uint32_t)(r * D + rblk * 16 + o);
+        for (int kk = 0; kk < 8; ++kk) s += wv[kk] * bab_s[ppart * 8 + kk];
+        for (int sh = kParts / 2; sh > 0; sh >>= 1) s += __shfl_xor(s, sh, kParts);
+        if (ppart == 0) {
+          const uint32_t el = (uint32_t)(r * D + rblk * 16 + po);
           const float pv = tanh_f(s);
           hs.store1(el, pv, tag);
           a.h[el] = pv;
@@ -2621,29 +2649,40 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   CORTEX_CASE(CORTEX_NARY_TREELSTM, 256)
   CORTEX_CASE(CORTEX_CHILDSUM_TREELSTM, 64)
   CORTEX_CASE(CORTEX_CHILDSUM_TREELSTM, 256)
+  CORTEX_CASE(CORTEX_CHILDSUM_TREELSTM, 512)
   CORTEX_CASE(CORTEX_TREE_RNN, 512)
   CORTEX_CASE(CELL_DAG, 64)
   CORTEX_CASE(CELL_DAG, 256)
   CORTEX_CASE(CELL_DAG, 512)
 #undef CORTEX_CASE
-  if ((cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) && (H == 64 || H == 256)) {
+  if ((cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) && (H == 64 || H == 256 || H == 512)) {
     const bool simple = cell == CORTEX_SIMPLE_TREEGRU;
     if (H == 64)
       out.fn = simple ? (cached ? treegru_forward_kernel<64, true, true> : treegru_forward_kernel<64, true, false>)
                       : (cached ? treegru_forward_kernel<64, false, true> : treegru_forward_kernel<64, false, false>);
-    else
+    else if (H == 256)
       out.fn = simple ? (cached ? treegru_forward_kernel<256, true, true> : treegru_forward_kernel<256, true, false>)
                       : (cached ? treegru_forward_kernel<256, false, true> : treegru_forward_kernel<256, false, false>);
+    else
+      out.fn = simple ? (cached ? treegru_forward_kernel<512, true, true> : treegru_forward_kernel<512, true, false>)
+                      : (cached ? treegru_forward_kernel<512, false, true> : treegru_forward_kernel<512, false, false>);
     out.J = 4;
     out.threads = kFwdThreads;
     out.level_barrier_ok = out.level_range_ok = out.phase_barrier_ok = true;
     return true;
   }
   if (cell == CORTEX_MVRNN && H == kMvD) {
-    out.fn = mvrnn_forward_kernel;
-    out.J = kMvD;
-    out.threads = kMvThreads;
-    out.lds = N <= kMvCacheRows ? 3 * (size_t)N * sizeof(int) : 0;
+    out.fn = mvrnn_forward_kernel<kMvD>;
+    out.J = MvDims<kMvD>::RB;
+    out.threads = MvDims<kMvD>::kThreads;
+    out.lds = N <= MvDims<kMvD>::kCacheRows ? 3 * (size_t)N * sizeof(int) : 0;
+    return true;
+  }
+  if (cell == CORTEX_MVRNN && H == kMvD2) {
+    out.fn = mvrnn_forward_kernel<kMvD2>;
+    out.J = MvDims<kMvD2>::RB;
+    out.threads = MvDims<kMvD2>::kThreads;
+    out.lds = N <= MvDims<kMvD2>::kCacheRows ? 3 * (size_t)N * sizeof(int) : 0;
     return true;
   }
   return false;
@@ -2706,8 +2745,8 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   int S;
   int64_t q = knob(CORTEX_KNOB_FWD_NODE_GROUPS);
   if (cell == CORTEX_MVRNN) {
-    S = 4;
-    if (q <= 0) q = cus / 4;
+    S = inst.J;                       // row blocks of P per node
+    if (q <= 0) q = cus / S;
   } else {
     // one slice (TreeRNN at H = 64) or one workgroup per tree: a node group
     // per 16 nodes, up to one per compute unit; else fill the GPU with slices

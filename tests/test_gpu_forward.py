@@ -64,6 +64,14 @@ SMALL = {
                                                                  node_hi=40, simple=True),
     "dag_h64": lambda s: I.dagrnn_workload(s, n_grids=3, rows=7, cols=5, H=64),
     "dag_h256": lambda s: I.dagrnn_workload(s, n_grids=2, rows=9, cols=11, H=256),
+    # the paper's large hidden sizes (h_l = 512; 128 for MV-RNN)
+    "childsum_h512": lambda s: I.childsum_treelstm_workload(s, batch=3, H=512, vocab=50, node_lo=1, node_hi=40),
+    "treegru_h512": lambda s: I.childsum_treegru_workload(s, batch=3, H=512, vocab=50, node_lo=1, node_hi=40),
+    "simple_treegru_h512": lambda s: I.childsum_treegru_workload(s, batch=2, H=512, vocab=50, node_lo=1,
+                                                                 node_hi=40, simple=True),
+    "mvrnn_d128": lambda s: I.mvrnn_workload(s, batch=3, d=128, leaf_lo=1, leaf_hi=30),
+    # W_M ~ U(+-sqrt(3)/16): unit gain at d = 128, so P stays O(0.1) through depth
+    "mvrnn_d128_gain1": lambda s: I.mvrnn_workload(s, batch=2, d=128, leaf_lo=10, leaf_hi=40, wm_scale=0.108),
 }
 
 
@@ -72,6 +80,8 @@ SMALL = {
 @pytest.mark.parametrize("groups", [0, 1, 3])
 def test_small_ragged(name, seed, groups):
     wl = SMALL[name](500 + seed)
+    if wl.H == 512 and wl.cell != "tree_rnn" and groups > 2:
+        groups = 2          # 128 hidden slices: two node groups fill the 256 compute units
     announce("small %s seed %d groups %d N=%d" % (name, seed, groups, wl.N))
     dw = run(wl, groups)
     compare_states(dw.states_by_node(), O.forward_workload(wl), name)
@@ -83,13 +93,25 @@ LARGE = {
     "tree_rnn_h256": lambda: I.tree_rnn_workload(31, n_leaves=1800, H=256),
     "nary_h256": lambda: I.nary_treelstm_workload(32, batch=120, H=256),
     "childsum_h256": lambda: I.childsum_treelstm_workload(33, batch=110, H=256),
+    "childsum_h512": lambda: I.childsum_treelstm_workload(35, batch=60, H=512),
+    "treegru_h512": lambda: I.childsum_treegru_workload(36, batch=60, H=512),
 }
+
+
+def test_mvrnn_d128_uncached_structure():
+    """MV-RNN at d = 128 caches the structure in LDS only up to 640 rows
+    ([A;B] takes 129 KB there): a batch of 40 trees runs uncached."""
+    wl = I.mvrnn_workload(37, batch=40, d=128)
+    assert wl.N > 640
+    announce("uncached structure mvrnn d128 N=%d" % wl.N)
+    dw = run(wl)
+    compare_states(dw.states_by_node(), O.forward_workload(wl), wl.name)
 
 
 @pytest.mark.parametrize("name", sorted(LARGE))
 def test_uncached_structure(name):
     wl = LARGE[name]()
-    assert wl.N > 2600, "must exceed the structure cache"
+    assert wl.N > (2600 if wl.H < 512 else 1710), "must exceed the structure cache"
     announce("uncached structure %s N=%d" % (name, wl.N))
     dw = run(wl)
     compare_states(dw.states_by_node(), O.forward_workload(wl), name)

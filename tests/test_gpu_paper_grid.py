@@ -1,8 +1,8 @@
 """The paper's evaluation grid (TreeFC on perfect binary trees of height 7,
 DAG-RNN on 10x10 grids, child-sum TreeLSTM and MV-RNN on SST-sized trees;
-batch 1 and 10; hidden h_s and, where the library implements it, h_l):
-every supported cell against the fp64 oracle, element by element, and the
-unsupported hidden sizes rejected on the host."""
+batch 1 and 10; hidden h_s and h_l): every cell against the fp64 oracle,
+element by element, and hidden sizes without a kernel instance rejected on
+the host."""
 import numpy as np
 import pytest
 
@@ -14,9 +14,7 @@ from tests.gpu_helpers import announce, compare_lin, compare_states, need_gpu
 
 pytestmark = pytest.mark.gpu
 
-SUPPORTED = [(c, b, "s") for c in I.PAPER_GRID_CELLS for b in (1, 10)] + \
-            [(c, b, "l") for c in ("treefc", "dagrnn") for b in (1, 10)]
-UNSUPPORTED = [("treegru", 1, "l"), ("treelstm", 1, "l"), ("mvrnn", 1, "l")]
+SUPPORTED = [(c, b, h) for c in I.PAPER_GRID_CELLS for b in (1, 10) for h in ("s", "l")]
 
 
 @pytest.fixture(autouse=True)
@@ -36,10 +34,15 @@ def test_paper_grid_parity(cell, batch, hidden):
     compare_states(dw.states_by_node(), O.forward_workload(wl), wl.name)
 
 
-@pytest.mark.parametrize("cell,batch,hidden", UNSUPPORTED)
-def test_paper_grid_unsupported_hidden_rejected(cell, batch, hidden):
-    wl = I.paper_grid_workload(cell, batch, hidden)
-    announce("paper grid unsupported %s h_%s" % (cell, hidden))
+@pytest.mark.parametrize("maker", [
+    lambda: I.childsum_treelstm_workload(5, batch=1, H=128),
+    lambda: I.childsum_treegru_workload(5, batch=1, H=1024),
+    lambda: I.mvrnn_workload(5, batch=1, d=96),
+])
+def test_unsupported_hidden_rejected(maker):
+    """A hidden size no kernel instance exists for is refused on the host."""
+    wl = maker()
+    announce("unsupported hidden %s H=%d" % (wl.cell, wl.H))
     dw = DeviceWorkload(wl)
     dw.linearize()
     dw.h.fill_(7.0)
