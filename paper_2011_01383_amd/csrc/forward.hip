@@ -155,21 +155,32 @@ __device__ __forceinline__ int childsum_gate(int gslot) {
   return gslot == 0 ? 0 : (gslot == 1 ? 2 : (gslot == 2 ? 3 : 1));
 }
 
-// Copies the workgroup's weight slice into LDS: every load of a thread is
-// issued before the first store, so the copy costs about one round trip.
+// The workgroup's weight slice, copied into LDS: issue_weight_slice requests
+// every value of the thread (registers), commit_weight_slice stores them, so
+// the copy costs about one memory round trip, which other loads issued
+// between the two calls share.
 template <int CELL, int H, int J>
-__device__ void load_weight_slice(const FwdArgs &a, int hbase, float *W_s, float *bias_s) {
+struct WeightRegs {
   using D = Dims<CELL, H, J>;
-  constexpr int ROW4 = (D::LDW - 4) / 4, SEG4 = H / 4, KA4 = D::KA / 4;
-  constexpr int ITEMS = D::MPAD * ROW4, PER = (ITEMS + kFwdThreads - 1) / kFwdThreads;
+  static constexpr int ROW4 = (D::LDW - 4) / 4, ITEMS = D::MPAD * ROW4;
+  static constexpr int PER = (ITEMS + kFwdThreads - 1) / kFwdThreads;
   float4 v[PER];
+  float bv;                       // bias of slice row threadIdx.x (< MPAD)
+};
+
+template <int CELL, int H, int J>
+__device__ __forceinline__ void issue_weight_slice(const FwdArgs &a, int hbase, WeightRegs<CELL, H, J> &w) {
+  using D = Dims<CELL, H, J>;
+  using WR = WeightRegs<CELL, H, J>;
+  constexpr int ROW4 = WR::ROW4, SEG4 = H / 4, KA4 = D::KA / 4, ITEMS = WR::ITEMS;
+  static_assert(D::MPAD <= kFwdThreads, "one bias per thread");
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
+  for (int k = 0; k < WR::PER; ++k) {
     const int idx = threadIdx.x + k * kFwdThreads;
     const int m = idx / ROW4, c4 = idx % ROW4;
     const int g = m / J, j = m % J, hj = hbase + j;
     const int sg = c4 / SEG4, o4 = c4 % SEG4;
-    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    w.v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (idx < ITEMS && m < D::GJ && c4 < KA4) {
       const float *src = nullptr;
       if (CELL == CORTEX_TREE_RNN) src = a.W + (size_t)hj * 2 * H + sg * H;
@@ -177,24 +188,36 @@ __device__ void load_weight_slice(const FwdArgs &a, int hbase, float *W_s, float
       if (CELL == CORTEX_CHILDSUM_TREELSTM)
         src = (sg == 0 ? a.W : a.U) + ((size_t)childsum_gate(g) * H + hj) * H;
       if (CELL == CELL_DAG) src = (sg == 0 ? a.W : a.U + (size_t)(sg - 1) * H * H) + (size_t)hj * H;
-      v[k] = *(const float4 *)(src + o4 * 4);
+      w.v[k] = *(const float4 *)(src + o4 * 4);
     }
   }
+  const int m = threadIdx.x;
+  w.bv = 0.f;
+  if (m < D::GJ) {
+    const int g = m / J, hj = hbase + m % J;
+    if (CELL == CORTEX_TREE_RNN || CELL == CELL_DAG) w.bv = a.b[hj];
+    if (CELL == CORTEX_NARY_TREELSTM) w.bv = a.b[g * H + hj];
+    if (CELL == CORTEX_CHILDSUM_TREELSTM) w.bv = a.b[childsum_gate(g) * H + hj];
+  }
+}
+
+template <int CELL, int H, int J>
+__device__ __forceinline__ void commit_weight_slice(const WeightRegs<CELL, H, J> &w, float *W_s, float *bias_s) {
+  using D = Dims<CELL, H, J>;
+  using WR = WeightRegs<CELL, H, J>;
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
+  for (int k = 0; k < WR::PER; ++k) {
     const int idx = threadIdx.x + k * kFwdThreads;
-    if (idx < ITEMS) *(float4 *)&W_s[(idx / ROW4) * D::LDW + (idx % ROW4) * 4] = v[k];
+    if (idx < WR::ITEMS) *(float4 *)&W_s[(idx / WR::ROW4) * D::LDW + (idx % WR::ROW4) * 4] = w.v[k];
   }
-  for (int m = threadIdx.x; m < D::MPAD; m += kFwdThreads) {
-    const int g = m / J, j = m % J, hj = hbase + j;
-    float bv = 0.f;
-    if (m < D::GJ) {
-      if (CELL == CORTEX_TREE_RNN || CELL == CELL_DAG) bv = a.b[hj];
-      if (CELL == CORTEX_NARY_TREELSTM) bv = a.b[g * H + hj];
-      if (CELL == CORTEX_CHILDSUM_TREELSTM) bv = a.b[childsum_gate(g) * H + hj];
-    }
-    bias_s[m] = bv;
-  }
+  if (threadIdx.x < D::MPAD) bias_s[threadIdx.x] = w.bv;
+}
+
+template <int CELL, int H, int J>
+__device__ void load_weight_slice(const FwdArgs &a, int hbase, float *W_s, float *bias_s) {
+  WeightRegs<CELL, H, J> w;
+  issue_weight_slice<CELL, H, J>(a, hbase, w);
+  commit_weight_slice<CELL, H, J>(w, W_s, bias_s);
 }
 
 // Four consecutive columns c .. c+3 of weight-slice row m (the values
@@ -341,14 +364,51 @@ constexpr int kCachedRowsPerThread = (kMaxCachedRows + kFwdThreads - 1) / kFwdTh
 // codes staged per chunk of tiles.  Validates 1 <= L <= N, monotone offsets
 // from 0 to N, child rows in a strictly lower level, node ids and input rows
 // in range.
+//
+// The cached path is split in two: prefetch_sources requests every value it
+// needs (the level count, all N + 1 entries of the offsets array, whose
+// capacity is N + 1, the node ids and child rows of every row, and the input
+// row of every node id) into registers, with no load depending on another,
+// so they share one memory round trip, also with the weight loads issued
+// beside them; setup_sources then builds the cache from the registers (the
+// input row of a row is gathered through LDS).
+struct SrcRegs {
+  int L;
+  int ch[kCachedRowsPerThread][2];
+  int node[kCachedRowsPerThread];
+  int xi[kCachedRowsPerThread];          // x_index of node id tid + k*threads
+  int off[kCachedRowsPerThread + 1];     // level_offsets[tid + k*threads]
+};
+
 template <int CELL, bool kCached>
-__device__ bool setup_sources(const FwdArgs &a, int *cache, int &L, const int *&off, const int *&codes,
-                              const int *&xrow) {
+__device__ __forceinline__ void prefetch_sources(const FwdArgs &a, SrcRegs &p) {
+  using SC = SrcCfg<CELL>;
+  const int N = a.N, K = a.K, tid = threadIdx.x;
+  p.L = *a.num_levels;
+  if (!kCached) return;
+#pragma unroll
+  for (int k = 0; k < kCachedRowsPerThread; ++k) {
+    const int r = tid + k * kFwdThreads;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) p.ch[k][s] = (r < N && s < K) ? a.child_rows[r * K + s] : -1;
+    p.node[k] = r < N ? a.level_nodes[r] : -1;
+    p.xi[k] = (SC::kLeafX && r < N) ? a.x_index[r] : -1;
+  }
+#pragma unroll
+  for (int k = 0; k <= kCachedRowsPerThread; ++k) {
+    const int i = tid + k * kFwdThreads;
+    p.off[k] = i <= N ? a.level_offsets[i] : 0;
+  }
+}
+
+template <int CELL, bool kCached>
+__device__ bool setup_sources(const FwdArgs &a, const SrcRegs &p, int *cache, int &L, const int *&off,
+                              const int *&codes, const int *&xrow) {
   using SC = SrcCfg<CELL>;
   constexpr int SEGS = SC::SEGS;
   const int N = a.N, K = a.K;
   const int tid = threadIdx.x;
-  L = *a.num_levels;
+  L = p.L;
   if (L < 1 || L > N) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
     return false;
@@ -369,30 +429,38 @@ __device__ bool setup_sources(const FwdArgs &a, int *cache, int &L, const int *&
     return true;
   }
   int *o = cache, *cd = cache + (L + 1), *xr = cd + N * SEGS;
-  // one round of independent loads: offsets, node ids (and their input
-  // rows), child rows into registers
-  int ch[kCachedRowsPerThread][2];
+  int *xnode = cd;                 // input row by node id, until the codes are written (N <= N*SEGS ints)
+#pragma unroll
+  for (int k = 0; k <= kCachedRowsPerThread; ++k) {
+    const int i = tid + k * kFwdThreads;
+    if (i <= L) o[i] = p.off[k];
+  }
 #pragma unroll
   for (int k = 0; k < kCachedRowsPerThread; ++k) {
     const int r = tid + k * kFwdThreads;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) ch[k][s] = (r < N && s < K) ? a.child_rows[r * K + s] : -1;
-  }
-  for (int i = tid; i <= L; i += kFwdThreads) o[i] = a.level_offsets[i];
-  for (int r = tid; r < N; r += kFwdThreads) {
-    const int v = a.level_nodes[r];
+    if (r >= N) break;
+    const int v = p.node[k];
     if (v < 0 || v >= N) bad = 1;
     if (SC::kLeafX) {
-      int xi = (v >= 0 && v < N) ? a.x_index[v] : -1;
+      int xi = p.xi[k];
       if (xi < -1 || xi >= a.x_rows) {
         raise_status(a.status, CORTEX_ST_INPUT_RANGE);
         xi = -1;
       }
-      xr[r] = xi;
+      xnode[r] = xi;
     }
-    if (SC::kDag) cd[r * SEGS] = (v >= 0 && v < N) ? -2 - v : -1;
   }
-  __syncthreads();
+  if (SC::kLeafX) __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kCachedRowsPerThread; ++k) {
+    const int r = tid + k * kFwdThreads;
+    if (r >= N) break;
+    const int v = p.node[k];
+    const bool vok = v >= 0 && v < N;
+    if (SC::kLeafX) xr[r] = vok ? xnode[v] : -1;
+    if (SC::kDag) cd[r * SEGS] = vok ? -2 - v : -1;
+  }
+  __syncthreads();                 // offsets and input rows complete; xnode no longer read
   for (int l = tid; l < L; l += kFwdThreads) {
     const int o0 = o[l], o1 = o[l + 1];
     if (o1 < o0 || (l == 0 && o0 != 0) || (l == L - 1 && o1 != N)) bad = 1;
@@ -412,7 +480,7 @@ __device__ bool setup_sources(const FwdArgs &a, int *cache, int &L, const int *&
     const int start = o[lo];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      int c = ch[k][s];
+      int c = p.ch[k][s];
       if (c < -1 || c >= start) {          // a child must sit in a strictly lower level
         bad = 1;
         c = -1;
@@ -575,13 +643,21 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   const int cross_b = (H - o0) / 16 < NB ? (H - o0) / 16 : NB;
 
   CORTEX_TRACE_KERNEL(0);
-  const int status0 = load_status(a.status);    // one round trip with the weight loads
-  load_weight_slice<CELL, H, J>(a, hbase, W_s, bias_s);
+  // the status, the weight slice and the cached linearization are requested
+  // together: one memory round trip for all of them
+  const int status0 = load_status(a.status);
+  SrcRegs pf;
+  {
+    WeightRegs<CELL, H, J> wr;
+    issue_weight_slice<CELL, H, J>(a, hbase, wr);
+    prefetch_sources<CELL, kCached>(a, pf);
+    commit_weight_slice<CELL, H, J>(wr, W_s, bias_s);
+  }
   if (status0 != 0) return;
   CORTEX_TRACE_KERNEL(1);
   int L;
   const int *off, *codes, *xrow;
-  if (!setup_sources<CELL, kCached>(a, cache, L, off, codes, xrow)) return;
+  if (!setup_sources<CELL, kCached>(a, pf, cache, L, off, codes, xrow)) return;
   CORTEX_TRACE_KERNEL(2);
   const int off1 = off[1];
   int gave_up = 0;
