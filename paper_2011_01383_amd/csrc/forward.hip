@@ -1203,15 +1203,18 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       xc = cd[i16 * 3];
       cr = cd[i16 * 3 + 1 + rslot];
     }
-#pragma unroll
-    for (int b = 0; b < NBX; ++b)
-      t.xv[b] = xin.load4(xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 16 * b + 4 * g4) * 4) : kNoSource);
+    // one base offset per operand: the blocks and halves add constants,
+    // which the loads take as immediate offsets (an absent source stays
+    // beyond the buffer with them)
+    const uint32_t xo = xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 4 * g4) * 4) : kNoSource;
+    const uint32_t ho = cr >= 0 ? (uint32_t)(cr * H + rcol + 4 * g4) * 8u : kNoSource;
     t.cr = cr;
 #pragma unroll
+    for (int b = 0; b < NBX; ++b) t.xv[b] = xin.load4(xo + 64u * b);
+#pragma unroll
     for (int b = 0; b < NBR; ++b) {
-      const uint32_t so = cr >= 0 ? (uint32_t)(cr * H + rcol + 16 * b + 4 * g4) * 8u : kNoSource;
-      t.hv[b].lo = hs.load2_at(so);
-      t.hv[b].hi = hs.load2_at(so + 16u);
+      t.hv[b].lo = hs.load2_at(ho + 128u * b);
+      t.hv[b].hi = hs.load2_at(ho + 128u * b + 16u);
     }
   };
   auto ready = [&](const Ops &t) __attribute__((always_inline)) -> bool {
