@@ -182,6 +182,32 @@ int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const 
                         void *d_ws, size_t ws_bytes, void *stream);
 
 /*
+ * The whole hot path of a tree batch in one call: the linearization of
+ * cortex_linearize (written to *lin) followed by cortex_tree_forward, with the
+ * arguments and results of those two calls (N and K are taken from lin).
+ * Where the cell has a fused instance -- TreeRNN (H = 64 up to 320 nodes,
+ * 256, 512), N-ary TreeLSTM (64, 256), child-sum TreeLSTM and the TreeGRU
+ * cells (64, 256, 512); N <= 2048, the schedule knobs at their defaults
+ * (FWD_NODE_GROUPS aside) and the batch's linearization and structure
+ * fitting one compute unit's LDS beside the kernel's own -- this is ONE
+ * kernel launch: every workgroup linearizes the batch in LDS for itself (the
+ * single-workgroup linearizer's algorithm) and workgroup 0 writes *lin out.
+ * Otherwise (MV-RNN, larger batches) it enqueues cortex_linearize, then
+ * cortex_tree_forward.
+ *   d_children  [N*K] int32 by node id, -1 = absent slot (as cortex_linearize)
+ *   d_ws        cortex_tree_infer_workspace_bytes(cell, N, K, H) bytes of
+ *               device memory, zeroed before its first use (the linearizer's
+ *               workspace, then the forward's)
+ * Host errors return CORTEX_E_* and enqueue nothing; a child index out of
+ * range, a cycle or a broken input index set *d_status as the two calls do.
+ */
+size_t cortex_tree_infer_workspace_bytes(int32_t cell, int32_t N, int32_t K, int32_t H);
+int cortex_tree_infer(int32_t cell, int32_t H, const int32_t *d_children, const cortex_lin_t *lin,
+                      const float *d_x_table, int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
+                      const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status, void *d_ws,
+                      size_t ws_bytes, void *stream);
+
+/*
  * Forward pass of the DAG-RNN cell (recursive part of DAG-RNN, Sec. 7.1):
  *   h(v) = tanh(W x(v) + U_0 h(slot 0) + U_1 h(slot 1) + b)
  * (for image grids slot 0 is the node above, slot 1 the node to the left).

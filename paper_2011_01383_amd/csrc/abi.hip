@@ -41,8 +41,19 @@ int cached_occupancy(const void *kernel, int threads, size_t dyn_lds) {
   auto it = g_occ.find(key);
   if (it != g_occ.end()) return it->second;
   int per_cu = 0;
-  if (dyn_lds > 0) hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, dyn_lds) != hipSuccess) return -1;
+  // A request beyond the compute unit's LDS fails here: report no occupancy
+  // and clear the runtime's last error, which would otherwise surface at the
+  // caller's next HIP call.
+  if (dyn_lds > 0 &&
+      hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds) != hipSuccess) {
+    (void)hipGetLastError();
+    g_occ[key] = 0;
+    return 0;
+  }
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, dyn_lds) != hipSuccess) {
+    (void)hipGetLastError();
+    return -1;
+  }
   g_occ[key] = per_cu;
   return per_cu;
 }

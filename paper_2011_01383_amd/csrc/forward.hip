@@ -26,6 +26,7 @@
 
 #include "cortex_device.hpp"
 #include "cortex_host.hpp"
+#include "lin_small.hpp"
 
 namespace cortex {
 
@@ -90,6 +91,10 @@ struct FwdArgs {
   int32_t level_barrier;        // 1: a device-wide barrier closes every level (instead of per-datum waits alone);
                                 // 2 (TreeGRU): also one between the level's two exchanges
   float *keep;                  // TreeGRU, level_barrier 2: z, W_h x + b_h and h~ per (row, unit), [3][N][H]
+  // fused launch (cortex_tree_infer): the children to linearize, and where
+  // workgroup 0 writes the linearization
+  const int32_t *children;
+  int32_t *o_num_levels, *o_height, *o_level_offsets, *o_level_nodes, *o_node_row, *o_child_rows;
   int32_t ablate;               // slice kernel, for ablation studies: bit 0 (its own instance) reads the weight slice from
                                 // memory at every tile instead of LDS; bit 1 stages the leaf states and
                                 // has parents wait for them instead of reading their inputs directly
@@ -580,6 +585,135 @@ __device__ void write_leaf_outputs(const FwdArgs &a, const int *xrow, int r1, co
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fused launch (cortex_tree_infer): every workgroup linearizes the batch in
+// LDS itself (small_linearize), workgroup 0 also writes the linearization
+// out, and the structure cache of the slice kernel is built from the LDS
+// results, so the first level needs no global memory beyond the inputs.
+// Dynamic LDS (ints): the cache (4N + 1), the input row by node id (N), then
+// the linearizer's own arrays.  Leaf-input cells only (TreeRNN, N-ary TreeLSTM).
+// ---------------------------------------------------------------------------
+constexpr int kFusedPer = 4;                       // nodes per thread: N <= 2048
+constexpr int kFusedMaxNodes = kFwdThreads * kFusedPer;
+
+static size_t fused_lds_ints(int32_t N, int32_t K) {
+  return (size_t)4 * N + 1 + (size_t)N + small_lin_ints<kFwdThreads>(N, K);
+}
+
+template <int CELL>
+__device__ bool fused_setup(const FwdArgs &a, int *cache, int &L, const int *&off, const int *&codes,
+                            const int *&xrow) {
+  static_assert(SrcCfg<CELL>::kLeafX && SrcCfg<CELL>::SEGS == 2, "leaf-input cells");
+  const int N = a.N, K = a.K, tid = threadIdx.x;
+  int *xnode = cache + 4 * N + 1;
+  int *lin = xnode + N;
+  // the input row of every node id, requested before the linearizer's loads
+  int xi[kFusedPer];
+#pragma unroll
+  for (int k = 0; k < kFusedPer; ++k) {
+    const int v = tid + k * kFwdThreads;
+    xi[k] = v < N ? a.x_index[v] : -1;
+  }
+  SmallLin m;
+  L = small_linearize<kFwdThreads, kFusedPer>(a.children, N, K, a.status, lin, m, nullptr);
+  if (L == 0) return false;
+  if (blockIdx.x == 0)
+    small_lin_emit<kFwdThreads>(m, N, K, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,
+                                a.o_node_row, a.o_child_rows);
+  int *o = cache, *cd = cache + (L + 1), *xr = cd + 2 * N;
+  for (int i = tid; i <= L; i += kFwdThreads) o[i] = i < L ? m.lcount[i] : N;
+#pragma unroll
+  for (int k = 0; k < kFusedPer; ++k) {
+    const int v = tid + k * kFwdThreads;
+    if (v < N) {
+      int x = xi[k];
+      if (x < -1 || x >= a.x_rows) {
+        raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+        x = -1;
+      }
+      xnode[v] = x;
+    }
+  }
+  __syncthreads();
+  for (int r = tid; r < N; r += kFwdThreads) xr[r] = xnode[m.order[r]];
+  __syncthreads();
+  const int off1 = o[1];
+  // source codes: a child row, or (a leaf child) -2 - its input row
+  for (int r = tid; r < N; r += kFwdThreads) {
+    const int v = m.order[r];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      int c = -1;
+      if (s < K) {
+        const int ch = m.ch[v * K + s];
+        c = ch < 0 ? -1 : m.nrow[ch];
+      }
+      if (!(a.ablate & 2) && c >= 0 && c < off1) c = xr[c] >= 0 ? -2 - xr[c] : -1;
+      cd[r * 2 + s] = c;
+    }
+  }
+  __syncthreads();
+  off = o;
+  codes = cd;
+  xrow = xr;
+  return true;
+}
+
+// The Structure<true> cache (off, crow, xrow) built the same way from an
+// in-LDS linearization, for the kernels that read child rows (TreeRNN at
+// H = 64, child-sum TreeLSTM, TreeGRU cells).  Dynamic LDS (ints) from
+// `cache`: off (N + 1), crow (N*K), xrow (N), the input row by node id (N),
+// then the linearizer's arrays.
+__host__ __device__ inline size_t fused_struct_ints(int N, int K) {
+  return (size_t)N + 1 + (size_t)N * K + 2 * (size_t)N + small_lin_ints<kFwdThreads>(N, K);
+}
+
+__device__ bool fused_structure(const FwdArgs &a, int *cache, Structure<true> &st, int &L) {
+  const int N = a.N, K = a.K, tid = threadIdx.x;
+  int *o = cache, *crow = o + (N + 1), *xr = crow + N * K, *xnode = xr + N, *lin = xnode + N;
+  int xi[kFusedPer];
+#pragma unroll
+  for (int k = 0; k < kFusedPer; ++k) {
+    const int v = tid + k * kFwdThreads;
+    xi[k] = v < N ? a.x_index[v] : -1;
+  }
+  SmallLin m;
+  L = small_linearize<kFwdThreads, kFusedPer>(a.children, N, K, a.status, lin, m, nullptr);
+  if (L == 0) return false;
+  if (blockIdx.x == 0)
+    small_lin_emit<kFwdThreads>(m, N, K, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,
+                                a.o_node_row, a.o_child_rows);
+  for (int i = tid; i <= L; i += kFwdThreads) o[i] = i < L ? m.lcount[i] : N;
+#pragma unroll
+  for (int k = 0; k < kFusedPer; ++k) {
+    const int v = tid + k * kFwdThreads;
+    if (v < N) {
+      int x = xi[k];
+      if (x < -1 || x >= a.x_rows) {
+        raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+        x = -1;
+      }
+      xnode[v] = x;
+    }
+  }
+  __syncthreads();
+  for (int r = tid; r < N; r += kFwdThreads) {
+    const int v = m.order[r];
+    xr[r] = xnode[v];
+    for (int s = 0; s < K; ++s) {
+      const int c = m.ch[v * K + s];
+      crow[r * K + s] = c < 0 ? -1 : m.nrow[c];
+    }
+  }
+  __syncthreads();
+  st.off = o;
+  st.crow = crow;
+  st.xrow = xr;
+  st.node = nullptr;
+  st.K = K;
+  return true;
+}
+
 // Operand fragment: four consecutive k of one tile row, either staged (two
 // (value, tag) pairs of pairs in lo and hi) or plain (four floats in lo: an
 // input row, or zeros for an absent source).  Each lane issues only the loads
@@ -604,7 +738,7 @@ struct Frag {
 // so the four lane groups of a row read one 128-byte span of staged pairs
 // with each pair of load instructions.
 // ---------------------------------------------------------------------------
-template <int CELL, int H, int J, bool kCached, bool kWeightsFromMemory = false>
+template <int CELL, int H, int J, bool kCached, bool kWeightsFromMemory = false, bool kFused = false>
 __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   using D = Dims<CELL, H, J>;
   constexpr int GJ = D::GJ, MPAD = D::MPAD, NT = D::NT, LDW = D::LDW, KW = D::KW, NB = D::NB, KA = D::KA;
@@ -646,18 +780,31 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   // the status, the weight slice and the cached linearization are requested
   // together: one memory round trip for all of them
   const int status0 = load_status(a.status);
-  SrcRegs pf;
-  {
-    WeightRegs<CELL, H, J> wr;
-    issue_weight_slice<CELL, H, J>(a, hbase, wr);
-    prefetch_sources<CELL, kCached>(a, pf);
-    commit_weight_slice<CELL, H, J>(wr, W_s, bias_s);
-  }
-  if (status0 != 0) return;
-  CORTEX_TRACE_KERNEL(1);
   int L;
   const int *off, *codes, *xrow;
-  if (!setup_sources<CELL, kCached>(a, pf, cache, L, off, codes, xrow)) return;
+  if constexpr (kFused) {
+    // the weight loads share their round trip with the children and input
+    // rows the linearizer requests
+    static_assert(kCached && !kWeightsFromMemory, "fused launches cache the structure");
+    WeightRegs<CELL, H, J> wr;
+    issue_weight_slice<CELL, H, J>(a, hbase, wr);
+    const bool ok = fused_setup<CELL>(a, cache, L, off, codes, xrow);
+    commit_weight_slice<CELL, H, J>(wr, W_s, bias_s);
+    if (!ok || status0 != 0) return;
+    __syncthreads();                  // the weight slice is in LDS before any tile reads it
+    CORTEX_TRACE_KERNEL(1);
+  } else {
+    SrcRegs pf;
+    {
+      WeightRegs<CELL, H, J> wr;
+      issue_weight_slice<CELL, H, J>(a, hbase, wr);
+      prefetch_sources<CELL, kCached>(a, pf);
+      commit_weight_slice<CELL, H, J>(wr, W_s, bias_s);
+    }
+    if (status0 != 0) return;
+    CORTEX_TRACE_KERNEL(1);
+    if (!setup_sources<CELL, kCached>(a, pf, cache, L, off, codes, xrow)) return;
+  }
   CORTEX_TRACE_KERNEL(2);
   const int off1 = off[1];
   int gave_up = 0;
@@ -903,6 +1050,7 @@ constexpr int kLdsH = 64;
 constexpr int kLdsHStride = kLdsH + 4;        // h row stride in LDS
 constexpr int kLdsMaxRows = 320;              // rows kept in LDS
 
+template <bool kFused = false>
 __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
   constexpr int H = kLdsH, LDH = kLdsHStride, NB = H / 16;
   constexpr int EPI = kTileM * H / kFwdThreads;
@@ -925,11 +1073,17 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
   for (int b = 0; b < NB; ++b)
     wr[b] = *(const float4 *)(a.W + (size_t)(16 * nt + i16) * 2 * H + kh * H + 16 * b + 4 * g4);
   if (tid < H) bias_s[tid] = a.b[tid];
-  if (status0 != 0) return;
-  CORTEX_TRACE_KERNEL(1);
   Structure<true> st;
   int L;
-  if (!setup_structure<true, true, false>(a, cache, st, L)) return;
+  if constexpr (kFused) {
+    // the batch is linearized here (its loads share the weights' round trip)
+    if (!fused_structure(a, cache, st, L) || status0 != 0) return;
+    CORTEX_TRACE_KERNEL(1);
+  } else {
+    if (status0 != 0) return;
+    CORTEX_TRACE_KERNEL(1);
+    if (!setup_structure<true, true, false>(a, cache, st, L)) return;
+  }
   CORTEX_TRACE_KERNEL(2);
 
   // level 0: the leaves are their input rows (zeros without one)
@@ -1360,7 +1514,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
 // slot reads zero rows, so it adds exactly zero).  Child states come from the
 // tagged staging as in the kernel above.
 // ---------------------------------------------------------------------------
-template <int H, bool kCached>
+template <int H, bool kCached, bool kFused = false>
 __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a) {
   constexpr int J = 4;
   using D = Dims<CORTEX_CHILDSUM_TREELSTM, H, J>;
@@ -1397,12 +1551,23 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
 
   CORTEX_TRACE_KERNEL(0);
   const int status0 = load_status(a.status);    // one round trip with the weight loads
-  load_weight_slice<CORTEX_CHILDSUM_TREELSTM, H, J>(a, hbase, W_s, bias_s);
-  if (status0 != 0) return;
-  CORTEX_TRACE_KERNEL(1);
   Structure<kCached> st;
   int L;
-  if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
+  if constexpr (kFused) {
+    static_assert(kCached, "fused launches cache the structure");
+    WeightRegs<CORTEX_CHILDSUM_TREELSTM, H, J> wr;
+    issue_weight_slice<CORTEX_CHILDSUM_TREELSTM, H, J>(a, hbase, wr);
+    const bool ok = fused_structure(a, cache, st, L);
+    commit_weight_slice<CORTEX_CHILDSUM_TREELSTM, H, J>(wr, W_s, bias_s);
+    if (!ok || status0 != 0) return;
+    __syncthreads();                  // the weight slice is in LDS before any tile reads it
+    CORTEX_TRACE_KERNEL(1);
+  } else {
+    load_weight_slice<CORTEX_CHILDSUM_TREELSTM, H, J>(a, hbase, W_s, bias_s);
+    if (status0 != 0) return;
+    CORTEX_TRACE_KERNEL(1);
+    if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
+  }
   CORTEX_TRACE_KERNEL(2);
   int gave_up = 0;
 
@@ -1967,7 +2132,7 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_forest_kernel(FwdArgs a)
 // rows (the other rows' results are unused).  Leaves (no child) have m = 0
 // and h~ = 0: a leaf phase evaluates them from their inputs alone.
 // ---------------------------------------------------------------------------
-template <int H, bool kSimple, bool kCached>
+template <int H, bool kSimple, bool kCached, bool kFused = false>
 __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a) {
   constexpr int J = 4;
   constexpr int LDW = 2 * H + 4;
@@ -2004,6 +2169,9 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
 
   CORTEX_TRACE_KERNEL(0);
   const int status0 = load_status(a.status);
+  Structure<kCached> st;
+  int L;
+  bool fused_ok = true;
   {
     // weight slice: row m = g*J + j (g = z, r, h, zero); columns [W | U]
     constexpr int ROW4 = (LDW - 4) / 4, ITEMS = 16 * ROW4, PER = (ITEMS + kFwdThreads - 1) / kFwdThreads;
@@ -2015,18 +2183,26 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
       v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (idx < ITEMS && g < 3) v[k] = *(const float4 *)((sg == 0 ? a.W : a.U) + ((size_t)g * H + hj) * H + o4 * 4);
     }
+    const float bv = tid < 16 && tid / J < 3 ? a.b[(tid / J) * H + hbase + tid % J] : 0.f;
+    if constexpr (kFused) {
+      // the batch is linearized while the weight loads are in flight
+      static_assert(kCached, "fused launches cache the structure");
+      fused_ok = fused_structure(a, cache, st, L);
+    }
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int idx = tid + k * kFwdThreads;
       if (idx < ITEMS) *(float4 *)&W_s[(idx / ROW4) * LDW + (idx % ROW4) * 4] = v[k];
     }
-    if (tid < 16) bias_s[tid] = tid / J < 3 ? a.b[(tid / J) * H + hbase + tid % J] : 0.f;
+    if (tid < 16) bias_s[tid] = bv;
   }
-  if (status0 != 0) return;
+  if (!fused_ok || status0 != 0) return;
   CORTEX_TRACE_KERNEL(1);
-  Structure<kCached> st;
-  int L;
-  if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
+  if constexpr (kFused) {
+    __syncthreads();                  // the weight slice is in LDS before any tile reads it
+  } else {
+    if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
+  }
   CORTEX_TRACE_KERNEL(2);
   int gave_up = 0;
 
@@ -2683,7 +2859,7 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   const int64_t unroll = knob(CORTEX_KNOB_TREE_UNROLL);
   const int64_t groups = knob(CORTEX_KNOB_FWD_NODE_GROUPS);
   if (cell == CORTEX_TREE_RNN && H == kLdsH && unroll == 0 && N <= kLdsMaxRows && groups <= 1) {
-    out.fn = tree_rnn_lds_kernel;        // one workgroup, every state in LDS
+    out.fn = tree_rnn_lds_kernel<false>;  // one workgroup, every state in LDS
     out.J = kLdsH;
     out.threads = kFwdThreads;
     out.one_group = true;
@@ -2767,6 +2943,53 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   return false;
 }
 
+// The fused instance (linearization inside the forward launch) for a cell
+// and hidden size, at the default schedule; false where there is none.
+static bool pick_fused(int cell, int H, int32_t N, int32_t K, Instance &out) {
+  const int64_t units = knob(CORTEX_KNOB_FWD_SLICE_UNITS);
+  if (N > kFusedMaxNodes) return false;
+  out.threads = kFwdThreads;
+  if (cell == CORTEX_TREE_RNN && H == kLdsH) {
+    if (knob(CORTEX_KNOB_TREE_UNROLL) != 0 || N > kLdsMaxRows || knob(CORTEX_KNOB_FWD_NODE_GROUPS) > 1) return false;
+    out.fn = tree_rnn_lds_kernel<true>;
+    out.J = kLdsH;
+    out.one_group = true;
+    out.lds = (size_t)N * kLdsHStride * sizeof(float) + fused_struct_ints(N, K) * sizeof(int);
+    return true;
+  }
+  if ((cell == CORTEX_NARY_TREELSTM && (H == 64 || H == 256)) || (cell == CORTEX_TREE_RNN && (H == 256 || H == 512))) {
+    const int J = cell == CORTEX_NARY_TREELSTM ? 4 : 16;
+    if ((units != 0 && units != J) || K != 2 || N > kMaxCachedRows) return false;
+    if (cell == CORTEX_NARY_TREELSTM)
+      out.fn = H == 64 ? slice_forward_kernel<CORTEX_NARY_TREELSTM, 64, 4, true, false, true>
+                       : slice_forward_kernel<CORTEX_NARY_TREELSTM, 256, 4, true, false, true>;
+    else
+      out.fn = H == 256 ? slice_forward_kernel<CORTEX_TREE_RNN, 256, 16, true, false, true>
+                        : slice_forward_kernel<CORTEX_TREE_RNN, 512, 16, true, false, true>;
+    out.J = J;
+    out.lds = fused_lds_ints(N, K) * sizeof(int);
+    return true;
+  }
+  const bool gru = cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU;
+  if ((cell == CORTEX_CHILDSUM_TREELSTM || gru) && (H == 64 || H == 256 || H == 512)) {
+    if (units != 0 && units != 4) return false;
+    const bool simple = cell == CORTEX_SIMPLE_TREEGRU;
+    if (!gru)
+      out.fn = H == 64 ? childsum_forward_kernel<64, true, true>
+                       : (H == 256 ? childsum_forward_kernel<256, true, true> : childsum_forward_kernel<512, true, true>);
+    else if (H == 64)
+      out.fn = simple ? treegru_forward_kernel<64, true, true, true> : treegru_forward_kernel<64, false, true, true>;
+    else if (H == 256)
+      out.fn = simple ? treegru_forward_kernel<256, true, true, true> : treegru_forward_kernel<256, false, true, true>;
+    else
+      out.fn = simple ? treegru_forward_kernel<512, true, true, true> : treegru_forward_kernel<512, false, true, true>;
+    out.J = 4;
+    out.lds = fused_struct_ints(N, K) * sizeof(int);
+    return true;
+  }
+  return false;
+}
+
 // Workspace of a forward launch: barrier words, the trace area, then the
 // tagged staging of h (and of c for the LSTM cells, of P for MV-RNN), 8 bytes
 // per element.
@@ -2797,8 +3020,12 @@ static uint32_t next_tag() {
   return t;
 }
 
+// fused_children != nullptr: the fused instance, which linearizes the batch
+// itself and writes *lin; where there is none, or it does not fit one compute
+// unit, nothing is enqueued and *launched stays false.
 static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, void *d_ws, size_t ws_bytes,
-                          void *stream) {
+                          void *stream, const int32_t *fused_children = nullptr, bool *launched = nullptr) {
+  if (launched) *launched = false;
   // state and staging arrays are addressed with 32-bit byte offsets
   const uint64_t state_bytes = (uint64_t)lin->num_nodes * H * (cell == CORTEX_MVRNN ? H : 1) * 8;
   const uint64_t table_bytes = (uint64_t)(a.x_rows > 0 ? a.x_rows : 0) * H * (cell == CORTEX_MVRNN ? H : 1) * 4;
@@ -2807,19 +3034,27 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
     return CORTEX_E_WORKSPACE;
   size_t dyn = 0;
   bool cached = false;
-  if (cell != CORTEX_MVRNN) {
+  Instance inst;
+  if (fused_children) {
+    if (knob(CORTEX_KNOB_LIN_BLOCKS) != 0 || knob(CORTEX_KNOB_LEVEL_SYNC) != 0 || knob(CORTEX_KNOB_ABLATE) != 0 ||
+        !pick_fused(cell, H, lin->num_nodes, lin->max_arity, inst))
+      return CORTEX_OK;
+    dyn = inst.lds;
+  } else if (cell != CORTEX_MVRNN) {
     dyn = cache_ints(cell, lin->num_nodes, lin->max_arity) * sizeof(int);
     const bool childsum_like =
         cell == CORTEX_CHILDSUM_TREELSTM || cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU;
     cached = dyn <= kStructCacheBudget && (childsum_like || lin->num_nodes <= kMaxCachedRows);
     if (!cached) dyn = 0;
   }
-  Instance inst;
-  if (!pick(cell, H, lin->num_nodes, cached, inst)) return CORTEX_E_INVAL;
-  if (inst.lds != SIZE_MAX) dyn = inst.lds;
+  if (!fused_children) {
+    if (!pick(cell, H, lin->num_nodes, cached, inst)) return CORTEX_E_INVAL;
+    if (inst.lds != SIZE_MAX) dyn = inst.lds;
+  }
   const int per_cu = cached_occupancy((const void *)inst.fn, inst.threads, dyn);
   const int cus = num_cus();
-  if (per_cu <= 0 || cus <= 0) return CORTEX_E_HIP;
+  if (cus <= 0) return CORTEX_E_HIP;
+  if (per_cu <= 0) return fused_children ? CORTEX_OK : CORTEX_E_HIP;
   const int cap = per_cu * cus;
   int S;
   int64_t q = knob(CORTEX_KNOB_FWD_NODE_GROUPS);
@@ -2860,6 +3095,17 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   set_last_grid(1, (int32_t)G);
   if (sync_mode == 1) a.level_barrier = 1;
   if (sync_mode == 3) a.level_barrier = 2;
+  if (fused_children) {
+    a.children = fused_children;
+    a.o_num_levels = lin->num_levels;
+    a.o_height = lin->height;
+    a.o_level_offsets = lin->level_offsets;
+    a.o_level_nodes = lin->level_nodes;
+    a.o_node_row = lin->node_row;
+    a.o_child_rows = lin->child_rows;
+    set_last_grid(0, 0);
+    *launched = true;
+  }
   if (sync_mode != 2) return launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
   // one launch per level (ablation): L is read back first; every launch
   // reloads weights and structure and keeps the launch tag, so a level
@@ -2905,13 +3151,10 @@ extern "C" size_t cortex_forward_workspace_bytes(int32_t cell, int32_t N, int32_
          (staged >= 2 ? cortex::second_staging_bytes(cell, N, H) : 0);
 }
 
-extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,
-                                   int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
-                                   const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status,
-                                   void *d_ws, size_t ws_bytes, void *stream) {
-  if (!lin_ok(lin) || !w || !d_status || x_rows < 0) return CORTEX_E_INVAL;
-  if (cell < CORTEX_TREE_RNN || cell > CORTEX_SIMPLE_TREEGRU) return CORTEX_E_INVAL;
-  if (lin->num_nodes == 0) return CORTEX_OK;
+// Host checks of a tree forward's arguments (N > 0) and its argument block.
+static int tree_args(int32_t cell, const cortex_lin_t *lin, const float *d_x_table, int32_t x_rows,
+                     const int32_t *d_x_index, const float *d_leaf_mat, const cortex_weights_t *w, float *d_h,
+                     float *d_c_or_P, int32_t *d_status, void *d_ws, FwdArgs &a) {
   if (!d_ws || !d_h || !d_x_index || (x_rows > 0 && !d_x_table)) return CORTEX_E_INVAL;
   const int K = lin->max_arity;
   if (cell == CORTEX_CHILDSUM_TREELSTM) {
@@ -2925,7 +3168,7 @@ extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *
     if (cell == CORTEX_MVRNN && (!w->W || !w->W_M || !d_c_or_P || (x_rows > 0 && !d_leaf_mat)))
       return CORTEX_E_INVAL;
   }
-  FwdArgs a = {};
+  a = FwdArgs{};
   fill_lin(a, lin);
   a.x_rows = x_rows;
   a.x_table = d_x_table;
@@ -2938,6 +3181,19 @@ extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *
   a.h = d_h;
   a.c = d_c_or_P;
   a.status = d_status;
+  return CORTEX_OK;
+}
+
+extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,
+                                   int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
+                                   const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status,
+                                   void *d_ws, size_t ws_bytes, void *stream) {
+  if (!lin_ok(lin) || !w || !d_status || x_rows < 0) return CORTEX_E_INVAL;
+  if (cell < CORTEX_TREE_RNN || cell > CORTEX_SIMPLE_TREEGRU) return CORTEX_E_INVAL;
+  if (lin->num_nodes == 0) return CORTEX_OK;
+  FwdArgs a;
+  const int rc = tree_args(cell, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status, d_ws, a);
+  if (rc != CORTEX_OK) return rc;
   return launch_forward(cell, H, lin, a, d_ws, ws_bytes, stream);
 }
 
@@ -2957,4 +3213,39 @@ extern "C" int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const floa
   a.h = d_h;
   a.status = d_status;
   return launch_forward(CELL_DAG, H, lin, a, d_ws, ws_bytes, stream);
+}
+
+extern "C" size_t cortex_tree_infer_workspace_bytes(int32_t cell, int32_t N, int32_t K, int32_t H) {
+  if (cell < CORTEX_TREE_RNN || cell > CORTEX_SIMPLE_TREEGRU) return 0;
+  const size_t lw = cortex_linearize_workspace_bytes(N, K), fw = cortex_forward_workspace_bytes(cell, N, H);
+  if (lw == 0 || fw == 0) return 0;
+  return align_up(lw, 256) + fw;
+}
+
+extern "C" int cortex_tree_infer(int32_t cell, int32_t H, const int32_t *d_children, const cortex_lin_t *lin,
+                                 const float *d_x_table, int32_t x_rows, const int32_t *d_x_index,
+                                 const float *d_leaf_mat, const cortex_weights_t *w, float *d_h, float *d_c_or_P,
+                                 int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream) {
+  if (!lin_ok(lin) || !w || !d_status || x_rows < 0 || !lin->height || !lin->node_row) return CORTEX_E_INVAL;
+  if (cell < CORTEX_TREE_RNN || cell > CORTEX_SIMPLE_TREEGRU) return CORTEX_E_INVAL;
+  const int32_t N = lin->num_nodes, K = lin->max_arity;
+  if (N == 0) return cortex_linearize(d_children, 0, K, lin, d_status, d_ws, ws_bytes, stream);
+  if (!d_children) return CORTEX_E_INVAL;
+  FwdArgs a;
+  int rc = tree_args(cell, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status, d_ws, a);
+  if (rc != CORTEX_OK) return rc;
+  const size_t need = cortex_tree_infer_workspace_bytes(cell, N, K, H);
+  if (need == 0) return CORTEX_E_INVAL;
+  if (ws_bytes < need) return CORTEX_E_WORKSPACE;
+  const size_t lw = align_up(cortex_linearize_workspace_bytes(N, K), 256);
+  void *fws = (char *)d_ws + lw;
+  const size_t fws_bytes = ws_bytes - lw;
+  // one launch where a fused instance exists and fits; else the two calls
+  bool launched = false;
+  rc = launch_forward(cell, H, lin, a, fws, fws_bytes, stream, d_children, &launched);
+  if (rc != CORTEX_OK || launched) return rc;
+  rc = cortex_linearize(d_children, N, K, lin, d_status, d_ws, lw, stream);
+  if (rc != CORTEX_OK) return rc;
+  return cortex_tree_forward(cell, H, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status,
+                             fws, fws_bytes, stream);
 }

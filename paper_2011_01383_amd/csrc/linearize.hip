@@ -17,6 +17,7 @@
 //      child rows through node_row.
 #include "cortex_device.hpp"
 #include "cortex_host.hpp"
+#include "lin_small.hpp"
 
 namespace cortex {
 
@@ -42,12 +43,6 @@ struct LinArgs {
   uint64_t timeout;
 };
 
-__device__ __forceinline__ int lds_load(const int *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-__device__ __forceinline__ void lds_store(int *p, int v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
 
 // Maximum over the workgroup (tmp: kLinThreads ints of LDS); every thread gets it.
 __device__ __forceinline__ int block_max(int v, int *tmp) {
@@ -61,119 +56,6 @@ __device__ __forceinline__ int block_max(int v, int *tmp) {
   return m;
 }
 
-// Exclusive prefix sum of data[0..n) in LDS by the whole workgroup: each
-// thread scans a contiguous segment, segment sums are scanned with wave
-// shuffles and the wave totals in wsum[THREADS/64 + 1].  Returns the total.
-template <int THREADS>
-__device__ int block_exclusive_scan(int *data, int n, int *wsum) {
-  constexpr int W = THREADS / 64;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int seg = (n + THREADS - 1) / THREADS;
-  const int lo = min(n, tid * seg), hi = min(n, lo + seg);
-  int sum = 0;
-  for (int i = lo; i < hi; ++i) sum += data[i];
-  int x = sum;
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) wsum[wave] = x;
-  __syncthreads();
-  if (tid == 0) {
-    int run = 0;
-    for (int w = 0; w < W; ++w) {
-      const int t = wsum[w];
-      wsum[w] = run;
-      run += t;
-    }
-    wsum[W] = run;
-  }
-  __syncthreads();
-  int run = wsum[wave] + x - sum;
-  for (int i = lo; i < hi; ++i) {
-    const int t = data[i];
-    data[i] = run;
-    run += t;
-  }
-  const int total = wsum[W];
-  __syncthreads();
-  return total;
-}
-
-// ---------------------------------------------------------------------------
-// Height relaxation over a block of nodes whose heights live in LDS (hs).  A
-// thread owns the nodes i = tid + j*THREADS (j < PER) and holds their child
-// slots in registers: lc = the child's index inside the block (-1 when the
-// slot is empty or the child lies outside), ext = a fixed lower bound on the
-// height of a child outside the block (-1 otherwise).  A sweep raises h(i) to
-// 1 + max over its children.  Values only grow and never pass the true
-// height, so sweeps run without barriers, each wave reading whatever the
-// others last wrote.  After kSweepBatch such sweeps come a barrier and one
-// more sweep: if that sweep changes nothing anywhere, every h(i) equals
-// 1 + max over its children as they stand, which is the fixed point, i.e.
-// the height.  A value >= N proves a cycle.
-// ---------------------------------------------------------------------------
-constexpr int kSweepBatch = 4;
-
-template <int PER, int THREADS, int KS>
-__device__ __forceinline__ bool height_sweep(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER],
-                                             int *hs, int n, int N, bool &cyc) {
-  bool changed = false;
-  // A wave reads the child heights of its live nodes back to back, with one
-  // wait: whether round j holds live nodes is uniform over the wave, and an
-  // empty slot reads entry 0 of the block and is masked.  KS = slots read.
-  const int wave_first = (int)(threadIdx.x & ~63u);
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    if (wave_first + j * THREADS >= n) break;
-    int hv[KS];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) hv[s] = lds_load(&hs[lc[j][s] >= 0 ? lc[j][s] : 0]);
-    const int i = (int)threadIdx.x + j * THREADS;
-    int m = -1;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) m = max(m, max(lc[j][s] >= 0 ? hv[s] : -1, ext[j][s]));
-    if (i < n && m + 1 > myh[j]) {
-      myh[j] = m + 1;
-      lds_store(&hs[i], m + 1);
-      changed = true;
-      if (m + 1 >= N) cyc = true;
-    }
-  }
-  return changed;
-}
-
-// Sweeps to the fixed point over child slots [0, KS).  Returns (uniformly
-// over the workgroup) whether any height changed; *cycle is set when a value
-// reached N.  Every thread of the workgroup calls it.
-template <int PER, int THREADS, int KS>
-__device__ bool relax_heights_k(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
-                                int N, bool *cycle, int *sweeps) {
-  bool any = false;
-  *cycle = false;
-  for (;;) {
-    bool cyc = false;
-#pragma unroll 1
-    for (int r = 0; r < kSweepBatch; ++r) any |= height_sweep<PER, THREADS, KS>(lc, ext, myh, hs, n, N, cyc);
-    __syncthreads();
-    const bool ch = height_sweep<PER, THREADS, KS>(lc, ext, myh, hs, n, N, cyc);
-    any |= ch;
-    *sweeps += kSweepBatch + 1;
-    if (__syncthreads_or(cyc)) {
-      *cycle = true;
-      break;
-    }
-    if (!__syncthreads_or(ch)) break;
-  }
-  return __syncthreads_or(any) != 0;
-}
-
-template <int PER, int THREADS>
-__device__ bool relax_heights(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
-                              int K, int N, bool *cycle, int *sweeps) {
-  if (K <= 2) return relax_heights_k<PER, THREADS, 2>(lc, ext, myh, hs, n, N, cycle, sweeps);
-  return relax_heights_k<PER, THREADS, 4>(lc, ext, myh, hs, n, N, cycle, sweeps);
-}
 
 // Trace builds only: workgroup 0 stamps phase boundaries into uint64 slots
 // 1..15 of the barrier header (the generation word uses slot 0 only).
@@ -450,263 +332,29 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
 
 
 // ---------------------------------------------------------------------------
-// Small batches: one workgroup does the whole linearization in LDS.
-//   children -> LDS; height sweeps until nothing changes (a value >= N proves
-//   a cycle); a stable counting sort on height with 8-bit digits (one pass
-//   while L <= 256): a global digit histogram gives each digit's first row,
-//   then 1024-node chunks in id order are ranked with wave ballots, per-wave
-//   digit counts and a running cursor per digit; finally every output array
-//   is written once, coalesced.
-// LDS (ints): children N*K, height N, perm 2N, node_row N, level count N+1,
-// wave-digit counts 16*256, digit cursors 256*2.
+// Small batches: one workgroup does the whole linearization in LDS
+// (small_linearize), then writes every output array once, coalesced.
 // ---------------------------------------------------------------------------
-#ifdef CORTEX_TRACE
-#define CORTEX_LIN_STAMP(k)                                         \
-  do {                                                              \
-    if (threadIdx.x == 0) ((uint64_t *)a.sync)[(k)] = wall_clock64(); \
-  } while (0)
-#else
-#define CORTEX_LIN_STAMP(k) \
-  do {                      \
-  } while (0)
-#endif
-
 constexpr int kSmallThreads = 1024;
-constexpr int kSmallWaves = kSmallThreads / 64;
 constexpr int kSmallPer = 4;                         // nodes per thread: N <= 4096
 constexpr size_t kSmallLdsMax = 150 * 1024;
 
-static size_t small_lds_bytes(int32_t N, int32_t K) {
-  return sizeof(int) * ((size_t)N * K + 5 * (size_t)N + 1 + kSmallWaves * 256 + 2 * 256 + 64);
-}
+static size_t small_lds_bytes(int32_t N, int32_t K) { return sizeof(int) * small_lin_ints<kSmallThreads>(N, K); }
+
 
 __global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs a) {
   extern __shared__ int sm[];
-  const int N = a.N, K = a.K;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  int *ch = sm;                       // [N*K]
-  int *hgt = ch + N * K;              // [N]
-  int *perm0 = hgt + N;               // [N]
-  int *perm1 = perm0 + N;             // [N]
-  int *nrow = perm1 + N;              // [N]
-  int *lcount = nrow + N;             // [N+1]
-  int *wcnt = lcount + N + 1;         // [16][256]
-  int *dstart = wcnt + kSmallWaves * 256;   // [256]
-  int *cursor = dstart + 256;         // [256]
-  int *flags = cursor + 256;          // [64] scratch
-
-  CORTEX_LIN_STAMP(0);
-  const int status0 = load_status(a.status);     // requested together with the children
-  // 1. children: into registers for the sweeps (node v = tid + j*threads) and
-  //    into LDS for the output phase; range check
-  int myc[kSmallPer][4], myh[kSmallPer];
-  int bad = 0;
-  // every load is issued before any result is used (an absent slot reads
-  // entry 0 and is masked), so they cost one memory round trip together
-#pragma unroll
-  for (int j = 0; j < kSmallPer; ++j)
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int v = tid + j * kSmallThreads;
-      myc[j][s] = a.children[(v < N && s < K) ? (size_t)v * K + s : 0];
-    }
-#pragma unroll
-  for (int j = 0; j < kSmallPer; ++j) {
-    const int v = tid + j * kSmallThreads;
-    myh[j] = 0;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      int c = (v < N && s < K) ? myc[j][s] : -1;
-      if (c < -1 || c >= N) { bad = 1; c = -1; }
-      myc[j][s] = c;
-      if (v < N && s < K) ch[v * K + s] = c;
-    }
-    if (v < N) hgt[v] = 0;
-  }
-  if (__syncthreads_or(status0 != 0)) return;
-  if (__syncthreads_or(bad)) {
-    if (tid == 0) raise_status(a.status, CORTEX_ST_CHILD_RANGE);
-    return;
-  }
-  CORTEX_LIN_STAMP(1);
-  // 2. heights.  Forest (every node fills at most one child slot in the
-  //    whole batch): a last-arriver walk.  Each node counts its pending
-  //    children; the thread of a leaf climbs towards the root: at each
-  //    parent it raises the parent's height to its own + 1, then takes one
-  //    off the parent's count, and the thread that empties the count holds
-  //    the parent's final height and climbs on.  A node still pending
-  //    afterwards lies on or above a cycle.  Any other DAG: barrier-free
-  //    sweeps to the fixed point.  (perm0, nrow and lcount serve as the
-  //    parent-count, parent and pending arrays here; all are rewritten later.)
-  //    The walk's LDS operations stay in program order (compiler fences) and
-  //    the LDS unit performs one wave's operations in that order, so the
-  //    raise lands before the decrement and the last decrement sees every
-  //    sibling's raise.
-  int *npar = perm0, *parent = nrow, *pend = lcount;
-#pragma unroll
-  for (int j = 0; j < kSmallPer; ++j) {
-    const int v = tid + j * kSmallThreads;
-    if (v < N) {
-      npar[v] = 0;
-      parent[v] = -1;
-      pend[v] = (myc[j][0] >= 0) + (myc[j][1] >= 0) + (myc[j][2] >= 0) + (myc[j][3] >= 0);
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < kSmallPer; ++j) {
-    const int v = tid + j * kSmallThreads;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int c = myc[j][s];
-      if (c >= 0) {
-        __hip_atomic_fetch_add(&npar[c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        parent[c] = v;
-      }
-    }
-  }
-  __syncthreads();
-  int multi = 0;
-#pragma unroll
-  for (int j = 0; j < kSmallPer; ++j) {
-    const int v = tid + j * kSmallThreads;
-    if (v < N && npar[v] > 1) multi = 1;
-  }
-  if (!__syncthreads_or(multi)) {
-#pragma unroll 1
-    for (int j = 0; j < kSmallPer; ++j) {
-      const int v = tid + j * kSmallThreads;
-      if (v >= N || (myc[j][0] >= 0) + (myc[j][1] >= 0) + (myc[j][2] >= 0) + (myc[j][3] >= 0) != 0) continue;
-      int hu = 0, p = parent[v];
-      while (p >= 0) {
-        __hip_atomic_fetch_max(&hgt[p], hu + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        const int left = __hip_atomic_fetch_sub(&pend[p], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        if (left != 1) break;
-        hu = lds_load(&hgt[p]);
-        p = lds_load(&parent[p]);
-      }
-    }
-    __syncthreads();
-    int stuck = 0;
-#pragma unroll
-    for (int j = 0; j < kSmallPer; ++j) {
-      const int v = tid + j * kSmallThreads;
-      if (v < N) {
-        if (pend[v] != 0) stuck = 1;
-        myh[j] = hgt[v];
-      }
-    }
-    if (__syncthreads_or(stuck)) {
-      if (tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
-      return;
-    }
-  } else {
-    int ext[kSmallPer][4];
-#pragma unroll
-    for (int j = 0; j < kSmallPer; ++j)
-#pragma unroll
-      for (int s = 0; s < 4; ++s) ext[j][s] = -1;
-    bool cyc;
-    int sweeps = 0;
-    relax_heights<kSmallPer, kSmallThreads>(myc, ext, myh, hgt, N, K, N, &cyc, &sweeps);
-    if (cyc) {
-      if (tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
-      return;
-    }
-  }
-  CORTEX_LIN_STAMP(2);
-  // L = 1 + max height, level counts
-  int mx = 0;
-#pragma unroll
-  for (int j = 0; j < kSmallPer; ++j) mx = max(mx, myh[j]);
-  for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
-  if (lane == 0) flags[wave] = mx;
-  for (int i = tid; i <= N; i += kSmallThreads) lcount[i] = 0;
-  __syncthreads();
-  int L = 0;
-  for (int w = 0; w < kSmallWaves; ++w) L = max(L, flags[w]);
-  L += 1;
-  for (int v = tid; v < N; v += kSmallThreads) atomicAdd(&lcount[hgt[v]], 1);
-  __syncthreads();
-  // level offsets = exclusive scan of the level counts (kept in lcount)
-  const int total = block_exclusive_scan<kSmallThreads>(lcount, L, flags);
-  for (int l = tid; l < L; l += kSmallThreads) a.level_offsets[l] = lcount[l];
-  if (tid == 0) {
-    a.level_offsets[L] = total;
-    *a.num_levels = L;
-  }
-  CORTEX_LIN_STAMP(3);
-  // 3. stable LSD counting sort on height, 8-bit digits.  With one pass
-  //    (L <= 256) the digit is the height itself: its starts are the level
-  //    offsets, and only bits(L-1) ballots and L digit columns are needed.
-  int passes = 1;
-  for (int v = (L - 1) >> 8; v > 0; v >>= 8) ++passes;
-  const int nbits = passes == 1 ? 32 - __clz(L - 1) : 8;      // __clz(0) = 32: L = 1 needs none
-  const int ndig = passes == 1 ? L : 256;
-  const unsigned long long lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-  for (int p = 0; p < passes; ++p) {
-    const int shift = 8 * p;
-    const int *in = (p & 1) ? perm0 : perm1;    // pass 0 reads ids directly
-    int *out = (p & 1) ? perm1 : perm0;
-    if (passes == 1) {
-      if (tid < L) dstart[tid] = lcount[tid];
-    } else {
-      if (tid < 256) dstart[tid] = 0;
-      __syncthreads();
-      for (int i = tid; i < N; i += kSmallThreads) {
-        const int v = p == 0 ? i : in[i];
-        atomicAdd(&dstart[(hgt[v] >> shift) & 255], 1);
-      }
-      __syncthreads();
-      block_exclusive_scan<kSmallThreads>(dstart, 256, flags);
-    }
-    if (tid < 256) cursor[tid] = 0;
-    __syncthreads();
-    for (int base = 0; base < N; base += kSmallThreads) {
-      const int idx = base + tid;
-      const bool valid = idx < N;
-      const int item = valid ? (p == 0 ? idx : in[idx]) : 0;
-      const int dig = valid ? ((hgt[item] >> shift) & 255) : 0;
-      unsigned long long peers = __ballot(valid);
-      for (int b = 0; b < nbits; ++b) {
-        const bool bit = (dig >> b) & 1;
-        const unsigned long long m = __ballot(bit);
-        peers &= bit ? m : ~m;
-      }
-      const int rank = __popcll(peers & lt_mask);
-      for (int i = tid; i < kSmallWaves * ndig; i += kSmallThreads) wcnt[(i / ndig) * 256 + i % ndig] = 0;
-      __syncthreads();
-      if (valid && rank == 0) wcnt[wave * 256 + dig] = __popcll(peers);
-      __syncthreads();
-      if (tid < ndig) {            // per digit: wave offsets within the chunk, then advance the cursor
-        int run = cursor[tid];
-        for (int w = 0; w < kSmallWaves; ++w) { const int x = wcnt[w * 256 + tid]; wcnt[w * 256 + tid] = run; run += x; }
-        cursor[tid] = run;
-      }
-      __syncthreads();
-      if (valid) out[dstart[dig] + wcnt[wave * 256 + dig] + rank] = item;
-      __syncthreads();
-    }
-  }
-  CORTEX_LIN_STAMP(4);
-  const int *order = ((passes - 1) & 1) ? perm1 : perm0;
-  for (int r = tid; r < N; r += kSmallThreads) nrow[order[r]] = r;
-  __syncthreads();
-  // 4. outputs
-  for (int r = tid; r < N; r += kSmallThreads) {
-    const int v = order[r];
-    a.level_nodes[r] = v;
-    a.node_row[v] = r;
-    a.height[r] = hgt[r];             // by node id (r doubles as a node id here)
-    for (int s = 0; s < K; ++s) {
-      const int c = ch[v * K + s];
-      a.child_rows[(size_t)r * K + s] = c < 0 ? -1 : nrow[c];
-    }
-  }
-  CORTEX_LIN_STAMP(5);
-  CORTEX_LIN_STAMP(6);
+  SmallLin m;
+  uint64_t *stamps = nullptr;
+#ifdef CORTEX_TRACE
+  stamps = (uint64_t *)a.sync;
+#endif
+  const int L = small_linearize<kSmallThreads, kSmallPer>(a.children, a.N, a.K, a.status, sm, m, stamps);
+  if (L == 0) return;
+  small_lin_emit<kSmallThreads>(m, a.N, a.K, L, a.num_levels, a.height, a.level_offsets, a.level_nodes,
+                                a.node_row, a.child_rows);
+  LIN_STAMP(5);
+  LIN_STAMP(6);
 }
 
 static size_t lin_tiles(int32_t N) { return (size_t)(N + kTile - 1) / kTile; }

@@ -2,9 +2,11 @@
 
 ``DeviceWorkload`` uploads a workload's structure, inputs and weights once,
 allocates the caller-owned linearization, outputs, status word and workspaces,
-and enqueues the path: ``cortex_linearize`` then ``cortex_tree_forward`` (or
-``cortex_dag_forward``) on one stream.  It only marshals arguments; all the
-work is done by the library's kernels.
+and enqueues the path on one stream: for tree cells ``cortex_tree_infer``
+(linearization and forward in one call, one launch where the cell has a fused
+instance), for the DAG cell ``cortex_linearize`` then ``cortex_dag_forward``;
+the two tree entry points can also be called on their own.  It only marshals
+arguments; all the work is done by the library's kernels.
 """
 from __future__ import annotations
 
@@ -36,6 +38,8 @@ class DeviceWorkload:
         self.is_dag = wl.cell == "dagrnn"
         self.cell = -1 if self.is_dag else C.CELL_IDS[wl.cell]
         self.ws_fwd = C.workspace(C.cortex_forward_workspace_bytes(self.cell, self.N, self.H), device)
+        self.ws_inf = None if self.is_dag else C.workspace(
+            C.cortex_tree_infer_workspace_bytes(self.cell, self.N, self.K, self.H), device)
         rows = max(self.N, 1)
         self.h = torch.empty(rows, self.H, dtype=torch.float32, device=device)
         if wl.cell in ("nary_treelstm", "childsum_treelstm"):
@@ -62,8 +66,25 @@ class DeviceWorkload:
                                        ws=self.ws_fwd, stream=self.stream)
         C.check(rc, "forward")
 
+    def infer(self) -> None:
+        """Tree cells: linearization and forward through cortex_tree_infer."""
+        rc = C.cortex_tree_infer(self.cell, self.H, self.children, self.lin, self.x_table, self.x_rows,
+                                 self.x_index, self.leaf_mat, W=self.W, U=self.U, b=self.b, W_M=self.W_M,
+                                 h=self.h, c_or_P=self.c, status=self.status, ws=self.ws_inf,
+                                 stream=self.stream)
+        C.check(rc, "cortex_tree_infer")
+
     def step(self) -> None:
-        """One pass of the hot path: linearize, then the fused forward."""
+        """One pass of the hot path: linearization and forward (for tree cells
+        one cortex_tree_infer call, for the DAG cell the two calls)."""
+        if self.is_dag:
+            self.linearize()
+            self.forward()
+        else:
+            self.infer()
+
+    def step_two_calls(self) -> None:
+        """The same pass as cortex_linearize, then the forward entry point."""
         self.linearize()
         self.forward()
 
@@ -77,6 +98,8 @@ class DeviceWorkload:
         self.status.zero_()
         self.ws_lin.zero_()
         self.ws_fwd.zero_()
+        if self.ws_inf is not None:
+            self.ws_inf.zero_()
 
     def lin_host(self) -> Dict[str, np.ndarray]:
         torch.cuda.synchronize()
