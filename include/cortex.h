@@ -187,13 +187,13 @@ int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const 
  * arguments and results of those two calls (N and K are taken from lin).
  * Where the cell has a fused instance -- TreeRNN (H = 64 up to 320 nodes,
  * 256, 512), N-ary TreeLSTM (64, 256), child-sum TreeLSTM and the TreeGRU
- * cells (64, 256, 512); N <= 2048, the schedule knobs at their defaults
+ * cells (64, 256, 512), MV-RNN (d = 64); N <= 2048, the schedule knobs at their defaults
  * (FWD_NODE_GROUPS aside) and the batch's linearization and structure
  * fitting one compute unit's LDS beside the kernel's own -- this is ONE
  * kernel launch: every workgroup linearizes the batch in LDS for itself (the
  * single-workgroup linearizer's algorithm) and workgroup 0 writes *lin out.
- * Otherwise (MV-RNN, larger batches) it enqueues cortex_linearize, then
- * cortex_tree_forward.
+ * Otherwise (MV-RNN at d = 128, larger batches) it enqueues cortex_linearize,
+ * then cortex_tree_forward.
  *   d_children  [N*K] int32 by node id, -1 = absent slot (as cortex_linearize)
  *   d_ws        cortex_tree_infer_workspace_bytes(cell, N, K, H) bytes of
  *               device memory, zeroed before its first use (the linearizer's

@@ -2576,7 +2576,17 @@ struct MvDims {
 };
 constexpr int kMvD = 64, kMvD2 = 128;
 
+// Fused launches (cortex_tree_infer): the batch is linearized in LDS first.
+// Dynamic LDS (ints): child rows (2N), leaf input rows (N), level offsets
+// (N + 1), input row by node id (N), then the linearizer's arrays.
 template <int D>
+constexpr int kMvFusedPer = kFusedMaxNodes / MvDims<D>::kThreads;      // nodes per thread: N <= 2048
+template <int D>
+__host__ __device__ inline size_t mv_fused_ints(int N) {
+  return 5 * (size_t)N + 1 + small_lin_ints<MvDims<D>::kThreads>(N, 2);
+}
+
+template <int D, bool kFused = false>
 __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdArgs a) {
   using M = MvDims<D>;
   constexpr int kThreads = M::kThreads, RB = M::RB, kLd = M::kLd, kAb = M::kAb, kGroups = M::kGroups;
@@ -2593,7 +2603,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
   const int i16 = lane & 15, g4 = lane >> 4;
   const int rblk = blockIdx.x % RB, ngroup = blockIdx.x / RB, ngroups = gridDim.x / RB;
   const int N = a.N;
-  const bool cached = N <= M::kCacheRows;
+  const bool cached = kFused || N <= M::kCacheRows;
   const uint32_t tag = a.tag;
   const TagBuf hs(a.hs, (uint32_t)N * D * 8);
   const TagBuf ps(a.cs, (uint32_t)N * D * D * 8);
@@ -2604,7 +2614,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
 
   // status, level count and weights requested together
   const int status0 = load_status(a.status);
-  const int L = *a.num_levels;
+  int L = kFused ? 0 : *a.num_levels;
   float wv[8];                            // W[16 rblk + po][8 ppart .. +8], for the whole launch
   {
     float wm[WPER];
@@ -2621,13 +2631,65 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
       WM_s[r * kLd + c] = wm[k];
     }
   }
+  int *crow_c = mv_cache, *leafx_c = mv_cache + 2 * N, *lvo = mv_cache + 3 * N;
+  if constexpr (kFused) {
+    // linearize the batch (its loads share the weights' round trip), then
+    // child rows, level offsets and the leaves' input rows from LDS
+    constexpr int PER = kMvFusedPer<D>;
+    int *xnode = lvo + N + 1, *lin = xnode + N;
+    int xi[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int v = tid + k * kThreads;
+      xi[k] = v < N ? a.x_index[v] : -1;
+    }
+    SmallLin m;
+    L = small_linearize<kThreads, PER>(a.children, N, 2, a.status, lin, m, nullptr);
+    if (L == 0) return;
+    if (blockIdx.x == 0)
+      small_lin_emit<kThreads>(m, N, 2, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,
+                               a.o_node_row, a.o_child_rows);
+    for (int i = tid; i <= L; i += kThreads) lvo[i] = i < L ? m.lcount[i] : N;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int v = tid + k * kThreads;
+      if (v < N) {
+        int x = xi[k];
+        if (x < -1 || x >= a.x_rows) {
+          raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+          x = -1;
+        }
+        xnode[v] = x;
+      }
+    }
+    __syncthreads();
+    for (int r = tid; r < N; r += kThreads) {
+      const int v = m.order[r];
+      leafx_c[r] = xnode[v];
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int c = m.ch[v * 2 + s];
+        crow_c[r * 2 + s] = c < 0 ? -1 : m.nrow[c];
+      }
+    }
+    __syncthreads();
+  }
   if (status0 != 0) return;
   if (L < 1 || L > N) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
     return;
   }
   int r0, r1;
-  if (!level_bounds(a, 0, r0, r1)) return;
+  auto bounds = [&](int l) -> bool {
+    if constexpr (kFused) {
+      r0 = lvo[l];
+      r1 = lvo[l + 1];
+      return true;
+    } else {
+      return level_bounds(a, l, r0, r1);
+    }
+  };
+  if (!bounds(0)) return;
   const int off1 = r1;
 
   // input row of leaf row r (validated), -1 = none
@@ -2644,8 +2706,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
     }
     return xi;
   };
-  int *crow_c = mv_cache, *leafx_c = mv_cache + 2 * N;
-  if (cached) {
+  if (cached && !kFused) {
     for (int i = tid; i < 2 * N; i += kThreads) {
       int c = a.child_rows[i];
       if (c < -1 || c >= N) {
@@ -2674,7 +2735,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
 
   int gave_up = 0;
   for (int l = 1; l < L && !gave_up; ++l) {
-    if (!level_bounds(a, l, r0, r1)) return;
+    if (!bounds(l)) return;
     for (int r = r0 + ngroup; r < r1; r += ngroups) {
       if (tid < 2) {
         int cr = cached ? crow_c[r * 2 + tid] : a.child_rows[(size_t)r * 2 + tid];
@@ -2927,14 +2988,14 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
     return true;
   }
   if (cell == CORTEX_MVRNN && H == kMvD) {
-    out.fn = mvrnn_forward_kernel<kMvD>;
+    out.fn = mvrnn_forward_kernel<kMvD, false>;
     out.J = MvDims<kMvD>::RB;
     out.threads = MvDims<kMvD>::kThreads;
     out.lds = N <= MvDims<kMvD>::kCacheRows ? 3 * (size_t)N * sizeof(int) : 0;
     return true;
   }
   if (cell == CORTEX_MVRNN && H == kMvD2) {
-    out.fn = mvrnn_forward_kernel<kMvD2>;
+    out.fn = mvrnn_forward_kernel<kMvD2, false>;
     out.J = MvDims<kMvD2>::RB;
     out.threads = MvDims<kMvD2>::kThreads;
     out.lds = N <= MvDims<kMvD2>::kCacheRows ? 3 * (size_t)N * sizeof(int) : 0;
@@ -2968,6 +3029,13 @@ static bool pick_fused(int cell, int H, int32_t N, int32_t K, Instance &out) {
                         : slice_forward_kernel<CORTEX_TREE_RNN, 512, 16, true, false, true>;
     out.J = J;
     out.lds = fused_lds_ints(N, K) * sizeof(int);
+    return true;
+  }
+  if (cell == CORTEX_MVRNN && (H == kMvD || H == kMvD2) && K == 2) {
+    out.fn = H == kMvD ? mvrnn_forward_kernel<kMvD, true> : mvrnn_forward_kernel<kMvD2, true>;
+    out.J = H == kMvD ? MvDims<kMvD>::RB : MvDims<kMvD2>::RB;
+    out.threads = H == kMvD ? MvDims<kMvD>::kThreads : MvDims<kMvD2>::kThreads;
+    out.lds = (H == kMvD ? mv_fused_ints<kMvD>(N) : mv_fused_ints<kMvD2>(N)) * sizeof(int);
     return true;
   }
   const bool gru = cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU;

@@ -1,5 +1,6 @@
 """cortex_tree_infer: linearization and forward in one call.  For the cells
-with a fused instance (TreeRNN, N-ary and child-sum TreeLSTM, TreeGRU cells)
+with a fused instance (TreeRNN, N-ary and child-sum TreeLSTM, TreeGRU cells,
+MV-RNN at d = 64)
 it is one launch in which every workgroup linearizes the batch itself;
 its linearization must be bit-exact and its states bitwise those of
 cortex_linearize followed by cortex_tree_forward (the same contraction in the
@@ -68,10 +69,12 @@ FUSED = {
     "treegru_h256_b10": lambda: I.childsum_treegru_workload(70, batch=10, H=256),
     "simple_treegru_h64": lambda: I.childsum_treegru_workload(80, batch=4, H=64, simple=True),
     "treegru_h512_b2": lambda: I.childsum_treegru_workload(81, batch=2, H=512),
+    "mvrnn_d64_b10": lambda: cached_workload(3, 0),
+    "mvrnn_d64_ragged": lambda: I.mvrnn_workload(82, batch=4, d=64, leaf_lo=1, leaf_hi=30),
 }
 
 ORACLE_CACHED = {"nary_h256_b10": (1, 0), "nary_h256_b10_seed1": (1, 1), "tree_rnn_h64_1x32": (0, 0),
-                 "childsum_h256_b10": (2, 0)}
+                 "childsum_h256_b10": (2, 0), "mvrnn_d64_b10": (3, 0)}
 
 
 def _relabeled(wl, seed):
@@ -112,7 +115,8 @@ def test_fused_launch_node_groups(groups):
 TWO_LAUNCH = {
     "tree_rnn_h64_over_320": (lambda: I.tree_rnn_workload(71, n_leaves=200, H=64), None),
     "tree_rnn_h64_unroll": (lambda: I.tree_rnn_workload(72, n_leaves=40, H=64), (C.CORTEX_KNOB_TREE_UNROLL, 2)),
-    "mvrnn_d64": (lambda: I.mvrnn_workload(73, batch=3, d=64), None),
+    # d = 128: [A; B] alone takes 129 KB of LDS, the linearization does not fit beside it
+    "mvrnn_d128": (lambda: I.mvrnn_workload(73, batch=3, d=128), None),
     "treegru_h256_phase_barrier": (lambda: I.childsum_treegru_workload(74, batch=3, H=256),
                                    (C.CORTEX_KNOB_LEVEL_SYNC, 3)),
     "nary_h256_over_2048": (lambda: I.nary_treelstm_workload(75, batch=90, H=256), None),
