@@ -4,8 +4,10 @@
 
 Loads ``libcortex_trace.so`` (built by ``python -m paper_2011_01383_amd.build
 --trace``, i.e. with -DCORTEX_TRACE), runs a few warm passes of one workload,
-clears the timeline, runs one more pass and reads the stamps the forward
-kernel left in its workspace: every workgroup (the first 256) stamps the
+clears the timeline, runs one more pass (the step's one launch where the
+cell has a fused instance, else cortex_linearize then the forward;
+``--two-calls`` forces the latter) and reads the stamps the forward kernel
+left in its workspace: every workgroup (the first 256) stamps the
 100 MHz wall clock at fixed points of every level.  The report gives, per
 level, when the first workgroup entered it and when the last one left it
 (both relative to the earliest kernel entry), the critical-path time of the
@@ -38,12 +40,22 @@ TRACE_BLOCKS, TRACE_LEVELS, TRACE_SLOTS = 256, 64, 16
 TICKS_PER_US = 100.0
 
 
-def read_timeline(dw):
+def forward_ws(dw, fused):
+    """The forward workspace of the last launch: the forward part of the
+    cortex_tree_infer workspace for a fused launch, else the forward's own."""
+    if not fused:
+        return dw.ws_fwd
+    from . import cortex as C
+    lw = (C.cortex_linearize_workspace_bytes(dw.N, dw.K) + 255) // 256 * 256
+    return dw.ws_inf[lw:]
+
+
+def read_timeline(dw, fused=False):
     """The timeline of the last forward launch of ``dw`` as uint64 [256, 64, 16]."""
     import torch
     torch.cuda.synchronize()
     n = TRACE_BLOCKS * TRACE_LEVELS * TRACE_SLOTS * 8
-    raw = dw.ws_fwd[SYNC_BYTES:SYNC_BYTES + n].cpu().numpy()
+    raw = forward_ws(dw, fused)[SYNC_BYTES:SYNC_BYTES + n].cpu().numpy()
     return raw.view(np.uint64).reshape(TRACE_BLOCKS, TRACE_LEVELS, TRACE_SLOTS)
 
 
@@ -110,6 +122,8 @@ def main():
     ap.add_argument("--json", default=None)
     ap.add_argument("--markdown", default=None)
     ap.add_argument("--npy", default=None, help="also save the raw stamps, uint64 [256, 64, 16]")
+    ap.add_argument("--two-calls", action="store_true",
+                    help="trace cortex_linearize, then the forward entry point, instead of the step's launch")
     args = ap.parse_args()
 
     import torch
@@ -126,18 +140,24 @@ def main():
     for _ in range(args.warm):
         dw.step()
     torch.cuda.synchronize()
+    # a step is one launch where the batch's cell has a fused instance
+    fused = not dw.is_dag and C.cortex_last_grid(0) == 0 and not args.two_calls
     n = TRACE_BLOCKS * TRACE_LEVELS * TRACE_SLOTS * 8
-    dw.ws_fwd[SYNC_BYTES:SYNC_BYTES + n].zero_()
+    forward_ws(dw, fused)[SYNC_BYTES:SYNC_BYTES + n].zero_()
     dw.ws_lin.zero_()                     # a zeroed workspace is always a valid start
-    dw.linearize()
-    torch.cuda.synchronize()
-    lin_stamps = dw.ws_lin[:56].cpu().numpy().view(np.uint64).astype(np.int64)
-    dw.forward()
+    if fused:
+        dw.step()
+        lin_stamps = np.zeros(7, dtype=np.int64)
+    else:
+        dw.linearize()
+        torch.cuda.synchronize()
+        lin_stamps = dw.ws_lin[:56].cpu().numpy().view(np.uint64).astype(np.int64)
+        dw.forward()
     st = dw.status_code()
     if st != 0:
         raise RuntimeError("device status %d" % st)
     L = int(dw.lin_host()["num_levels"])
-    raw = read_timeline(dw)
+    raw = read_timeline(dw, fused)
     if args.npy:
         np.save(args.npy, raw)
     rep = summarize(raw, L, C.cortex_last_grid(1))
@@ -157,7 +177,11 @@ def main():
         # single-workgroup linearizer: entry, children loaded, heights done,
         # level counts, sort done, outputs written, offsets written
         rep["linearize_phases_us"] = [float(t - lin_stamps[0]) / TICKS_PER_US for t in lin_stamps]
+    rep["one_launch"] = bool(fused)
     md = as_markdown(rep, "%s (grid %d, %d levels)" % (wl.name, rep["grid"], L))
+    if fused:
+        md += ("\n\nOne launch: every workgroup linearizes the batch in LDS first, so \"weights resident\" and "
+               "\"structure ready\" both mark the end of that linearization.")
     if "linearize_phases_us" in rep:
         md += ("\n\nLinearizer (one workgroup), from its entry: children loaded %.2f, heights %.2f, "
                "level counts and offsets %.2f, sort %.2f, outputs %.2f (end %.2f) us." % tuple(rep["linearize_phases_us"][1:]))
