@@ -312,8 +312,10 @@ def unroll_study(args):
     CORTEX_KNOB_TREE_UNROLL): the whole batch in one workgroup (up to 320
     nodes), one workgroup per tree, and level-parallel hidden slices that
     exchange states between workgroups at every level.  One JSON line per
-    (batch, schedule): the forward kernel time and the step (linearize +
-    forward), both averaged over back-to-back launches between two events."""
+    (batch, schedule): the forward kernel time and the step as the two calls
+    (cortex_linearize, then cortex_tree_forward, so that every schedule is
+    timed the same way), both averaged over back-to-back launches between two
+    events."""
     import torch
     from paper_2011_01383_amd import cortex as C
     from paper_2011_01383_amd import inputs as I
@@ -349,7 +351,7 @@ def unroll_study(args):
             torch.cuda.synchronize()
             assert dw.status_code() == 0
             fwd = timed(dw.forward)
-            step = timed(dw.step)
+            step = timed(dw.step_two_calls)
             assert dw.status_code() == 0
             print(json.dumps({"workload": wl.name, "nodes": wl.N, "levels": int(dw.lin_host()["num_levels"]),
                               "schedule": names[mode], "tree_unroll": mode, "grid": C.cortex_last_grid(1),

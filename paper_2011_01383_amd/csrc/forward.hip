@@ -594,6 +594,17 @@ __device__ void write_leaf_outputs(const FwdArgs &a, const int *xrow, int r1, co
 // the linearizer's own arrays.  Leaf-input cells only (TreeRNN, N-ary TreeLSTM).
 // ---------------------------------------------------------------------------
 constexpr int kFusedPer = 4;                       // nodes per thread: N <= 2048
+
+// Trace builds: workgroup 0 stamps the in-kernel linearizer's phases into
+// slots 4.. of its kernel-wide trace row (entry, children loaded, heights,
+// level offsets, sort); nullptr otherwise.
+__device__ __forceinline__ uint64_t *fused_lin_stamps(const FwdArgs &a) {
+#ifdef CORTEX_TRACE
+  if (blockIdx.x == 0) return a.trace + (size_t)(kTraceLevels - 1) * kTraceSlots + 4;
+#endif
+  (void)a;
+  return nullptr;
+}
 constexpr int kFusedMaxNodes = kFwdThreads * kFusedPer;
 
 static size_t fused_lds_ints(int32_t N, int32_t K) {
@@ -615,7 +626,7 @@ __device__ bool fused_setup(const FwdArgs &a, int *cache, int &L, const int *&of
     xi[k] = v < N ? a.x_index[v] : -1;
   }
   SmallLin m;
-  L = small_linearize<kFwdThreads, kFusedPer>(a.children, N, K, a.status, lin, m, nullptr);
+  L = small_linearize<kFwdThreads, kFusedPer>(a.children, N, K, a.status, lin, m, fused_lin_stamps(a));
   if (L == 0) return false;
   if (blockIdx.x == 0)
     small_lin_emit<kFwdThreads>(m, N, K, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,
@@ -678,7 +689,7 @@ __device__ bool fused_structure(const FwdArgs &a, int *cache, Structure<true> &s
     xi[k] = v < N ? a.x_index[v] : -1;
   }
   SmallLin m;
-  L = small_linearize<kFwdThreads, kFusedPer>(a.children, N, K, a.status, lin, m, nullptr);
+  L = small_linearize<kFwdThreads, kFusedPer>(a.children, N, K, a.status, lin, m, fused_lin_stamps(a));
   if (L == 0) return false;
   if (blockIdx.x == 0)
     small_lin_emit<kFwdThreads>(m, N, K, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,
@@ -2644,7 +2655,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
       xi[k] = v < N ? a.x_index[v] : -1;
     }
     SmallLin m;
-    L = small_linearize<kThreads, PER>(a.children, N, 2, a.status, lin, m, nullptr);
+    L = small_linearize<kThreads, PER>(a.children, N, 2, a.status, lin, m, fused_lin_stamps(a));
     if (L == 0) return;
     if (blockIdx.x == 0)
       small_lin_emit<kThreads>(m, N, 2, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,

@@ -180,8 +180,14 @@ def main():
     rep["one_launch"] = bool(fused)
     md = as_markdown(rep, "%s (grid %d, %d levels)" % (wl.name, rep["grid"], L))
     if fused:
+        k0 = raw[0, TRACE_LEVELS - 1].astype(np.int64)
+        lin = [float(k0[4 + i] - k0[4]) / TICKS_PER_US for i in range(5)] if k0[4] > 0 else None
+        rep["linearize_in_kernel_us"] = lin
         md += ("\n\nOne launch: every workgroup linearizes the batch in LDS first, so \"weights resident\" and "
                "\"structure ready\" both mark the end of that linearization.")
+        if lin:
+            md += (" Workgroup 0's linearizer, from its start: children loaded %.2f, heights %.2f, level counts and "
+                   "offsets %.2f, sort %.2f us." % tuple(lin[1:]))
     if "linearize_phases_us" in rep:
         md += ("\n\nLinearizer (one workgroup), from its entry: children loaded %.2f, heights %.2f, "
                "level counts and offsets %.2f, sort %.2f, outputs %.2f (end %.2f) us." % tuple(rep["linearize_phases_us"][1:]))
