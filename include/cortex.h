@@ -222,6 +222,21 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
                        const float *d_U, const float *d_b, float *d_h, int32_t *d_status,
                        void *d_ws, size_t ws_bytes, void *stream);
 
+/*
+ * The whole hot path of a DAG-RNN batch in one call: cortex_linearize, then
+ * cortex_dag_forward, with the arguments and results of those two calls.  One
+ * kernel launch where the batch fits the fused instance of the kernel with
+ * 16-unit slices (H = 64 or 512, or 256 below the 64-unit kernel's range of
+ * 12288 nodes; N <= 2048, default schedule knobs, the linearization fitting
+ * one compute unit's LDS beside the weight slice): every workgroup linearizes
+ * the batch in LDS and workgroup 0 writes *lin out.  Otherwise the two calls.
+ *   d_ws   cortex_dag_infer_workspace_bytes(N, K, H) bytes, zeroed before first use
+ */
+size_t cortex_dag_infer_workspace_bytes(int32_t N, int32_t K, int32_t H);
+int cortex_dag_infer(int32_t H, const int32_t *d_children, const cortex_lin_t *lin, const float *d_x,
+                     const float *d_W, const float *d_U, const float *d_b, float *d_h, int32_t *d_status,
+                     void *d_ws, size_t ws_bytes, void *stream);
+
 /* ---- tuning and diagnostics ---------------------------------------------- */
 
 /*

@@ -54,6 +54,7 @@ CELL_IDS = {"tree_rnn": CORTEX_TREE_RNN, "nary_treelstm": CORTEX_NARY_TREELSTM,
 EXPORTED = [
     "cortex_linearize_workspace_bytes", "cortex_linearize", "cortex_forward_workspace_bytes",
     "cortex_tree_forward", "cortex_dag_forward", "cortex_tree_infer_workspace_bytes", "cortex_tree_infer",
+    "cortex_dag_infer_workspace_bytes", "cortex_dag_infer",
     "cortex_set_knob", "cortex_get_knob",
     "cortex_last_grid", "cortex_version",
 ]
@@ -99,6 +100,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cortex_tree_infer.argtypes = [I32, I32, P, ctypes.POINTER(cortex_lin_t), P, I32, P, P,
                                       ctypes.POINTER(cortex_weights_t), P, P, P, P, SZ, P]
     lib.cortex_tree_infer.restype = ctypes.c_int
+    lib.cortex_dag_infer_workspace_bytes.argtypes = [I32, I32, I32]
+    lib.cortex_dag_infer_workspace_bytes.restype = SZ
+    lib.cortex_dag_infer.argtypes = [I32, P, ctypes.POINTER(cortex_lin_t), P, P, P, P, P, P, P, SZ, P]
+    lib.cortex_dag_infer.restype = ctypes.c_int
     lib.cortex_set_knob.argtypes = [I32, I64]
     lib.cortex_set_knob.restype = ctypes.c_int
     lib.cortex_get_knob.argtypes = [I32]
@@ -170,6 +175,18 @@ def cortex_tree_infer(cell: int, H: int, children: torch.Tensor, lin: "Lineariza
     return load().cortex_tree_infer(cell, H, _ptr(children), ctypes.byref(lin.struct), _ptr(x_table), x_rows,
                                     _ptr(x_index), _ptr(leaf_mat), ctypes.byref(w), _ptr(h), _ptr(c_or_P),
                                     _ptr(status), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
+
+
+def cortex_dag_infer_workspace_bytes(N: int, K: int, H: int) -> int:
+    return load().cortex_dag_infer_workspace_bytes(N, K, H)
+
+
+def cortex_dag_infer(H: int, children: torch.Tensor, lin: "Linearization", x: torch.Tensor, W: torch.Tensor,
+                     U: torch.Tensor, b: torch.Tensor, h: torch.Tensor, status: torch.Tensor, ws: torch.Tensor,
+                     stream=None) -> int:
+    return load().cortex_dag_infer(H, _ptr(children), ctypes.byref(lin.struct), _ptr(x), _ptr(W), _ptr(U),
+                                   _ptr(b), _ptr(h), _ptr(status), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _stream(stream))
 
 
 def cortex_set_knob(knob: int, value: int) -> int:

@@ -614,16 +614,19 @@ static size_t fused_lds_ints(int32_t N, int32_t K) {
 template <int CELL>
 __device__ bool fused_setup(const FwdArgs &a, int *cache, int &L, const int *&off, const int *&codes,
                             const int *&xrow) {
-  static_assert(SrcCfg<CELL>::kLeafX && SrcCfg<CELL>::SEGS == 2, "leaf-input cells");
+  using SC = SrcCfg<CELL>;
+  constexpr int SEGS = SC::SEGS;
+  static_assert((SC::kLeafX && SEGS == 2) || (SC::kDag && SEGS == 3), "leaf-input or DAG cells");
   const int N = a.N, K = a.K, tid = threadIdx.x;
   int *xnode = cache + 4 * N + 1;
   int *lin = xnode + N;
-  // the input row of every node id, requested before the linearizer's loads
+  // the input row of every node id (leaf-input cells), requested before the
+  // linearizer's loads
   int xi[kFusedPer];
 #pragma unroll
   for (int k = 0; k < kFusedPer; ++k) {
     const int v = tid + k * kFwdThreads;
-    xi[k] = v < N ? a.x_index[v] : -1;
+    xi[k] = (SC::kLeafX && v < N) ? a.x_index[v] : -1;
   }
   SmallLin m;
   L = small_linearize<kFwdThreads, kFusedPer>(a.children, N, K, a.status, lin, m, fused_lin_stamps(a));
@@ -631,27 +634,31 @@ __device__ bool fused_setup(const FwdArgs &a, int *cache, int &L, const int *&of
   if (blockIdx.x == 0)
     small_lin_emit<kFwdThreads>(m, N, K, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,
                                 a.o_node_row, a.o_child_rows);
-  int *o = cache, *cd = cache + (L + 1), *xr = cd + 2 * N;
+  int *o = cache, *cd = cache + (L + 1), *xr = cd + SEGS * N;
   for (int i = tid; i <= L; i += kFwdThreads) o[i] = i < L ? m.lcount[i] : N;
+  if constexpr (SC::kLeafX) {
 #pragma unroll
-  for (int k = 0; k < kFusedPer; ++k) {
-    const int v = tid + k * kFwdThreads;
-    if (v < N) {
-      int x = xi[k];
-      if (x < -1 || x >= a.x_rows) {
-        raise_status(a.status, CORTEX_ST_INPUT_RANGE);
-        x = -1;
+    for (int k = 0; k < kFusedPer; ++k) {
+      const int v = tid + k * kFwdThreads;
+      if (v < N) {
+        int x = xi[k];
+        if (x < -1 || x >= a.x_rows) {
+          raise_status(a.status, CORTEX_ST_INPUT_RANGE);
+          x = -1;
+        }
+        xnode[v] = x;
       }
-      xnode[v] = x;
     }
+    __syncthreads();
+    for (int r = tid; r < N; r += kFwdThreads) xr[r] = xnode[m.order[r]];
+    __syncthreads();
   }
-  __syncthreads();
-  for (int r = tid; r < N; r += kFwdThreads) xr[r] = xnode[m.order[r]];
-  __syncthreads();
-  const int off1 = o[1];
-  // source codes: a child row, or (a leaf child) -2 - its input row
+  const int off1 = L > 1 ? m.lcount[1] : N;
+  // source codes: a child row, or (a leaf child of a leaf-input cell) -2 -
+  // its input row; DAG-RNN: segment 0 is the node's own input row, -2 - id
   for (int r = tid; r < N; r += kFwdThreads) {
     const int v = m.order[r];
+    if (SC::kDag) cd[r * SEGS] = -2 - v;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       int c = -1;
@@ -659,14 +666,14 @@ __device__ bool fused_setup(const FwdArgs &a, int *cache, int &L, const int *&of
         const int ch = m.ch[v * K + s];
         c = ch < 0 ? -1 : m.nrow[ch];
       }
-      if (!(a.ablate & 2) && c >= 0 && c < off1) c = xr[c] >= 0 ? -2 - xr[c] : -1;
-      cd[r * 2 + s] = c;
+      if (SC::kLeafX && !(a.ablate & 2) && c >= 0 && c < off1) c = xr[c] >= 0 ? -2 - xr[c] : -1;
+      cd[r * SEGS + (SC::kDag ? s + 1 : s)] = c;
     }
   }
   __syncthreads();
   off = o;
   codes = cd;
-  xrow = xr;
+  xrow = SC::kLeafX ? xr : nullptr;
   return true;
 }
 
@@ -3042,6 +3049,18 @@ static bool pick_fused(int cell, int H, int32_t N, int32_t K, Instance &out) {
     out.lds = fused_lds_ints(N, K) * sizeof(int);
     return true;
   }
+  if (cell == CELL_DAG && (H == 64 || H == 256 || H == 512)) {
+    // the slice kernel with 16-unit slices (at H = 256 the batches below the
+    // 64-unit kernel's range)
+    if ((units != 0 && units != 16) || K != 2 || N > kMaxCachedRows) return false;
+    if (H == 256 && units == 0 && N >= kDagWideMinRows) return false;
+    out.fn = H == 64 ? slice_forward_kernel<CELL_DAG, 64, 16, true, false, true>
+                     : (H == 256 ? slice_forward_kernel<CELL_DAG, 256, 16, true, false, true>
+                                 : slice_forward_kernel<CELL_DAG, 512, 16, true, false, true>);
+    out.J = 16;
+    out.lds = fused_lds_ints(N, K) * sizeof(int);
+    return true;
+  }
   if (cell == CORTEX_MVRNN && (H == kMvD || H == kMvD2) && K == 2) {
     out.fn = H == kMvD ? mvrnn_forward_kernel<kMvD, true> : mvrnn_forward_kernel<kMvD2, true>;
     out.J = H == kMvD ? MvDims<kMvD>::RB : MvDims<kMvD2>::RB;
@@ -3327,4 +3346,40 @@ extern "C" int cortex_tree_infer(int32_t cell, int32_t H, const int32_t *d_child
   if (rc != CORTEX_OK) return rc;
   return cortex_tree_forward(cell, H, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status,
                              fws, fws_bytes, stream);
+}
+
+extern "C" size_t cortex_dag_infer_workspace_bytes(int32_t N, int32_t K, int32_t H) {
+  const size_t lw = cortex_linearize_workspace_bytes(N, K), fw = cortex_forward_workspace_bytes(-1, N, H);
+  if (lw == 0 || fw == 0) return 0;
+  return align_up(lw, 256) + fw;
+}
+
+extern "C" int cortex_dag_infer(int32_t H, const int32_t *d_children, const cortex_lin_t *lin, const float *d_x,
+                                const float *d_W, const float *d_U, const float *d_b, float *d_h,
+                                int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream) {
+  if (!lin_ok(lin) || !d_status || !lin->height || !lin->node_row) return CORTEX_E_INVAL;
+  if (lin->max_arity != 2) return CORTEX_E_INVAL;
+  const int32_t N = lin->num_nodes, K = lin->max_arity;
+  if (N == 0) return cortex_linearize(d_children, 0, K, lin, d_status, d_ws, ws_bytes, stream);
+  if (!d_children || !d_x || !d_W || !d_U || !d_b || !d_h || !d_ws) return CORTEX_E_INVAL;
+  const size_t need = cortex_dag_infer_workspace_bytes(N, K, H);
+  if (need == 0) return CORTEX_E_INVAL;
+  if (ws_bytes < need) return CORTEX_E_WORKSPACE;
+  const size_t lw = align_up(cortex_linearize_workspace_bytes(N, K), 256);
+  void *fws = (char *)d_ws + lw;
+  const size_t fws_bytes = ws_bytes - lw;
+  FwdArgs a = {};
+  fill_lin(a, lin);
+  a.x = d_x;
+  a.W = d_W;
+  a.U = d_U;
+  a.b = d_b;
+  a.h = d_h;
+  a.status = d_status;
+  bool launched = false;
+  int rc = launch_forward(CELL_DAG, H, lin, a, fws, fws_bytes, stream, d_children, &launched);
+  if (rc != CORTEX_OK || launched) return rc;
+  rc = cortex_linearize(d_children, N, K, lin, d_status, d_ws, lw, stream);
+  if (rc != CORTEX_OK) return rc;
+  return cortex_dag_forward(H, lin, d_x, d_W, d_U, d_b, d_h, d_status, fws, fws_bytes, stream);
 }

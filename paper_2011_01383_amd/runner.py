@@ -2,10 +2,10 @@
 
 ``DeviceWorkload`` uploads a workload's structure, inputs and weights once,
 allocates the caller-owned linearization, outputs, status word and workspaces,
-and enqueues the path on one stream: for tree cells ``cortex_tree_infer``
-(linearization and forward in one call, one launch where the cell has a fused
-instance), for the DAG cell ``cortex_linearize`` then ``cortex_dag_forward``;
-the two tree entry points can also be called on their own.  It only marshals
+and enqueues the path on one stream through ``cortex_tree_infer`` or
+``cortex_dag_infer`` (linearization and forward in one call, one launch where
+the cell and batch have a fused instance); the two separate entry points can
+also be called on their own.  It only marshals
 arguments; all the work is done by the library's kernels.
 """
 from __future__ import annotations
@@ -38,8 +38,8 @@ class DeviceWorkload:
         self.is_dag = wl.cell == "dagrnn"
         self.cell = -1 if self.is_dag else C.CELL_IDS[wl.cell]
         self.ws_fwd = C.workspace(C.cortex_forward_workspace_bytes(self.cell, self.N, self.H), device)
-        self.ws_inf = None if self.is_dag else C.workspace(
-            C.cortex_tree_infer_workspace_bytes(self.cell, self.N, self.K, self.H), device)
+        self.ws_inf = C.workspace(C.cortex_dag_infer_workspace_bytes(self.N, self.K, self.H) if self.is_dag else
+                                  C.cortex_tree_infer_workspace_bytes(self.cell, self.N, self.K, self.H), device)
         rows = max(self.N, 1)
         self.h = torch.empty(rows, self.H, dtype=torch.float32, device=device)
         if wl.cell in ("nary_treelstm", "childsum_treelstm"):
@@ -67,21 +67,21 @@ class DeviceWorkload:
         C.check(rc, "forward")
 
     def infer(self) -> None:
-        """Tree cells: linearization and forward through cortex_tree_infer."""
-        rc = C.cortex_tree_infer(self.cell, self.H, self.children, self.lin, self.x_table, self.x_rows,
-                                 self.x_index, self.leaf_mat, W=self.W, U=self.U, b=self.b, W_M=self.W_M,
-                                 h=self.h, c_or_P=self.c, status=self.status, ws=self.ws_inf,
-                                 stream=self.stream)
-        C.check(rc, "cortex_tree_infer")
+        """Linearization and forward in one call (cortex_tree_infer or cortex_dag_infer)."""
+        if self.is_dag:
+            rc = C.cortex_dag_infer(self.H, self.children, self.lin, self.x, self.W, self.U, self.b, self.h,
+                                    self.status, self.ws_inf, self.stream)
+        else:
+            rc = C.cortex_tree_infer(self.cell, self.H, self.children, self.lin, self.x_table, self.x_rows,
+                                     self.x_index, self.leaf_mat, W=self.W, U=self.U, b=self.b, W_M=self.W_M,
+                                     h=self.h, c_or_P=self.c, status=self.status, ws=self.ws_inf,
+                                     stream=self.stream)
+        C.check(rc, "infer")
 
     def step(self) -> None:
-        """One pass of the hot path: linearization and forward (for tree cells
-        one cortex_tree_infer call, for the DAG cell the two calls)."""
-        if self.is_dag:
-            self.linearize()
-            self.forward()
-        else:
-            self.infer()
+        """One pass of the hot path: linearization and forward through the
+        one-call entry point (one launch where the cell and batch allow)."""
+        self.infer()
 
     def step_two_calls(self) -> None:
         """The same pass as cortex_linearize, then the forward entry point."""
@@ -98,8 +98,7 @@ class DeviceWorkload:
         self.status.zero_()
         self.ws_lin.zero_()
         self.ws_fwd.zero_()
-        if self.ws_inf is not None:
-            self.ws_inf.zero_()
+        self.ws_inf.zero_()
 
     def lin_host(self) -> Dict[str, np.ndarray]:
         torch.cuda.synchronize()

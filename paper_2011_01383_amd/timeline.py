@@ -141,7 +141,7 @@ def main():
         dw.step()
     torch.cuda.synchronize()
     # a step is one launch where the batch's cell has a fused instance
-    fused = not dw.is_dag and C.cortex_last_grid(0) == 0 and not args.two_calls
+    fused = C.cortex_last_grid(0) == 0 and not args.two_calls
     n = TRACE_BLOCKS * TRACE_LEVELS * TRACE_SLOTS * 8
     forward_ws(dw, fused)[SYNC_BYTES:SYNC_BYTES + n].zero_()
     dw.ws_lin.zero_()                     # a zeroed workspace is always a valid start

@@ -1,6 +1,6 @@
-"""cortex_tree_infer: linearization and forward in one call.  For the cells
+"""cortex_tree_infer and cortex_dag_infer: linearization and forward in one call.  For the cells
 with a fused instance (TreeRNN, N-ary and child-sum TreeLSTM, TreeGRU cells,
-MV-RNN at d = 64)
+MV-RNN at d = 64, DAG-RNN with 16-unit slices)
 it is one launch in which every workgroup linearizes the batch itself;
 its linearization must be bit-exact and its states bitwise those of
 cortex_linearize followed by cortex_tree_forward (the same contraction in the
@@ -71,6 +71,10 @@ FUSED = {
     "treegru_h512_b2": lambda: I.childsum_treegru_workload(81, batch=2, H=512),
     "mvrnn_d64_b10": lambda: cached_workload(3, 0),
     "mvrnn_d64_ragged": lambda: I.mvrnn_workload(82, batch=4, d=64, leaf_lo=1, leaf_hi=30),
+    "dag_h256_10x10": lambda: I.paper_grid_workload("dagrnn", 1, "s"),
+    "dag_h256_10x10_b10": lambda: I.paper_grid_workload("dagrnn", 10, "s"),
+    "dag_h64_ragged": lambda: I.dagrnn_workload(83, n_grids=3, rows=7, cols=5, H=64),
+    "dag_h512_ragged": lambda: I.dagrnn_workload(84, n_grids=2, rows=9, cols=11, H=512),
 }
 
 ORACLE_CACHED = {"nary_h256_b10": (1, 0), "nary_h256_b10_seed1": (1, 1), "tree_rnn_h64_1x32": (0, 0),
@@ -101,6 +105,18 @@ def test_fused_launch_matches_two_calls_and_oracle(name):
     compare_states(st_a, ref, name)
 
 
+def test_dag_64_grids_two_launches():
+    """The 65,536-node grid batch: cortex_dag_infer takes the two launches."""
+    wl = cached_workload(4, 0)
+    announce("dag infer 64 grids N=%d" % wl.N)
+    dw = DeviceWorkload(wl)
+    _states(dw)
+    dw.infer()
+    assert dw.status_code() == 0
+    assert C.cortex_last_grid(0) >= 1
+    compare_states(dw.states_by_node(), cached_oracle(4, 0), wl.name)
+
+
 @pytest.mark.parametrize("groups", [1, 3])
 def test_fused_launch_node_groups(groups):
     wl = cached_workload(1, 2)
@@ -124,6 +140,8 @@ TWO_LAUNCH = {
     "nary_h256_beyond_lds": (lambda: I.nary_treelstm_workload(63, batch=40, H=256), None),
     "nary_h256_units2": (lambda: I.nary_treelstm_workload(76, batch=5, H=256), (C.CORTEX_KNOB_FWD_SLICE_UNITS, 2)),
     "nary_h256_level_sync": (lambda: I.nary_treelstm_workload(77, batch=5, H=256), (C.CORTEX_KNOB_LEVEL_SYNC, 1)),
+    "dag_h256_units64": (lambda: I.dagrnn_workload(85, n_grids=3, rows=9, cols=7, H=256),
+                         (C.CORTEX_KNOB_FWD_SLICE_UNITS, 64)),
 }
 
 
