@@ -634,6 +634,7 @@ __device__ bool fused_setup(const FwdArgs &a, int *cache, int &L, const int *&of
   if (blockIdx.x == 0)
     small_lin_emit<kFwdThreads>(m, N, K, L, a.o_num_levels, a.o_height, a.o_level_offsets, a.o_level_nodes,
                                 a.o_node_row, a.o_child_rows);
+  CORTEX_TRACE_KERNEL(9);
   int *o = cache, *cd = cache + (L + 1), *xr = cd + SEGS * N;
   for (int i = tid; i <= L; i += kFwdThreads) o[i] = i < L ? m.lcount[i] : N;
   if constexpr (SC::kLeafX) {
@@ -671,6 +672,7 @@ __device__ bool fused_setup(const FwdArgs &a, int *cache, int &L, const int *&of
     }
   }
   __syncthreads();
+  CORTEX_TRACE_KERNEL(10);
   off = o;
   codes = cd;
   xrow = SC::kLeafX ? xr : nullptr;

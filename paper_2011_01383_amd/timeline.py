@@ -186,8 +186,11 @@ def main():
         md += ("\n\nOne launch: every workgroup linearizes the batch in LDS first, so \"weights resident\" and "
                "\"structure ready\" both mark the end of that linearization.")
         if lin:
+            post = [float(k0[i] - k0[4]) / TICKS_PER_US if k0[i] > 0 else float("nan") for i in (9, 10)]
+            rep["linearize_in_kernel_post_us"] = post
             md += (" Workgroup 0's linearizer, from its start: children loaded %.2f, heights %.2f, level counts and "
-                   "offsets %.2f, sort %.2f us." % tuple(lin[1:]))
+                   "offsets %.2f, sort %.2f us; linearization written out %.2f, structure cache built %.2f us."
+                   % (tuple(lin[1:]) + tuple(post)))
     if "linearize_phases_us" in rep:
         md += ("\n\nLinearizer (one workgroup), from its entry: children loaded %.2f, heights %.2f, "
                "level counts and offsets %.2f, sort %.2f, outputs %.2f (end %.2f) us." % tuple(rep["linearize_phases_us"][1:]))
