@@ -1,16 +1,19 @@
 """Benchmark of the level-synchronous recursive-inference hot path on one GPU.
 
-One step = one pass of the whole path over one batch: cortex_linearize (node
-heights, level lists, child rows) followed by the fused persistent forward
-kernel, both enqueued on one stream with the inputs already resident in HBM.
+One step = one pass of the whole path over one batch: linearization (node
+heights, level lists, child rows) and the persistent forward, through one
+cortex_tree_infer / cortex_dag_infer call on one stream (a single launch where
+the cell and batch have a fused instance) with the inputs already resident in
+HBM.
 
 Default workload: binary N-ary TreeLSTM, hidden 256, a batch of 10 random
 binary trees with 10-40 leaves each (seeded synthetic stand-in for the SST
 trees of the paper's TreeLSTM evaluation).
 
 Prints ONE JSON line with the contract fields plus:
-  roofline      the forward kernel's achieved algorithmic FLOP/s (or GB/s) from
-                its own HIP-event-timed launches, against the MI355X peak
+  roofline      the step's dominant kernel's achieved algorithmic FLOP/s (or
+                GB/s) from its own HIP-event-timed launches, against the MI355X
+                nominal peak and against the rate measured on the GPU itself
   cpu_baseline  the fp64 oracle timed on this host's cores over a bounded sample
   breakdown     latency percentiles and the linearize / forward split
 """
@@ -113,6 +116,41 @@ def measured_traffic(wl):
         return float(fields["forward_hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def measured_peaks(stream):
+    """Sustained rates of this GPU, beside the nominal peaks: fp32 matrix-core
+    throughput from the library's register-only MFMA probe, and HBM bandwidth
+    from a 1 GiB device copy (bytes read + bytes written).  Best of five
+    launches each."""
+    import torch
+    from paper_2011_01383_amd import cortex as C
+
+    def best_ms(fn, reps=5):
+        fn()
+        out = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            out.append(a.elapsed_time(b))
+        return min(out)
+
+    iters = 20000
+    sink = torch.empty(C.cortex_probe_mfma_sink_floats(), dtype=torch.float32, device="cuda")
+    C.check(C.cortex_probe_mfma(sink, 0, stream), "cortex_probe_mfma")
+    mfma_ms = best_ms(lambda: C.cortex_probe_mfma(sink, iters, stream))
+    n = (1 << 30) // 4
+    src = torch.rand(n, device="cuda")
+    dst = torch.empty_like(src)
+    copy_ms = best_ms(lambda: dst.copy_(src))
+    del src, dst
+    return {"fp32_mfma_tflops": C.cortex_probe_mfma_flops(iters) / (mfma_ms / 1e3) / 1e12,
+            "hbm_copy_gbs": 2.0 * n * 4 / (copy_ms / 1e3) / 1e9,
+            "note": "register-only fp32 MFMA probe (16x16x4) on every CU; 1 GiB device copy, read + write"}
 
 
 def cpu_baseline(wl, seconds):
@@ -493,6 +531,10 @@ def main():
         achieved = byts / fwd_avg_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+    peaks = measured_peaks(stream)
+    roof["peak_measured"] = peaks["fp32_mfma_tflops"] if bound == "mfma" else peaks["hbm_copy_gbs"]
+    roof["frac_of_measured"] = achieved / roof["peak_measured"]
+    roof["peak_measured_note"] = peaks["note"]
     roof["traffic"] = measured_traffic(wl)
     roof["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = ("linearize + forward in one launch (%s)" if fused else "forward (%s)") % wl.cell
@@ -532,6 +574,8 @@ def main():
             "two_calls_note": "cortex_linearize and cortex_tree_forward / cortex_dag_forward timed on their own",
             "linearize_kernel_avg_ms": lin_avg_ms,
             "forward_kernel_avg_ms": fwd_avg_ms,
+            "measured_fp32_mfma_tflops": peaks["fp32_mfma_tflops"],
+            "measured_hbm_copy_gbs": peaks["hbm_copy_gbs"],
             "host_wall_s": wall,
         },
     }

@@ -322,6 +322,20 @@ int64_t cortex_get_knob(int32_t knob);
 /* Workgroups the last launch of each kind used (for reports; host-side). */
 int32_t cortex_last_grid(int32_t which /* 0 = linearize, 1 = forward */);
 
+/* Matrix-core throughput probe, for reporting achieved rates beside a sustained
+ * (measured) peak as well as the nominal one.  cortex_probe_mfma enqueues one
+ * workgroup of 8 waves per compute unit on `stream`; every wave runs `iters`
+ * rounds of 16 chained v_mfma_f32_16x16x4_f32 on register operands (no memory
+ * traffic) and writes one float per lane to d_sink, which must hold
+ * cortex_probe_mfma_sink_floats() floats (device memory, caller-owned).
+ * cortex_probe_mfma_flops(iters) is the fp32 flop count of one such launch
+ * (2 x 16 x 16 x 4 per instruction).  Returns CORTEX_E_INVAL for a NULL sink or
+ * negative iters, CORTEX_E_HIP if the device cannot be queried or the launch
+ * fails; the sizes return 0 then.  The sink values carry no meaning. */
+size_t cortex_probe_mfma_sink_floats(void);
+double cortex_probe_mfma_flops(int32_t iters);
+int cortex_probe_mfma(float *d_sink, int32_t iters, void *stream);
+
 /* Library version string. */
 const char *cortex_version(void);
 

@@ -25,7 +25,7 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
 ]
-SOURCES = ["abi.hip", "linearize.hip", "forward.hip"]
+SOURCES = ["abi.hip", "linearize.hip", "forward.hip", "probe.hip"]
 
 
 def _hipcc() -> str:

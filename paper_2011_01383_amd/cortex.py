@@ -57,6 +57,7 @@ EXPORTED = [
     "cortex_dag_infer_workspace_bytes", "cortex_dag_infer",
     "cortex_set_knob", "cortex_get_knob",
     "cortex_last_grid", "cortex_version",
+    "cortex_probe_mfma_sink_floats", "cortex_probe_mfma_flops", "cortex_probe_mfma",
 ]
 
 
@@ -110,6 +111,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cortex_get_knob.restype = I64
     lib.cortex_last_grid.argtypes = [I32]
     lib.cortex_last_grid.restype = I32
+    lib.cortex_probe_mfma_sink_floats.argtypes = []
+    lib.cortex_probe_mfma_sink_floats.restype = SZ
+    lib.cortex_probe_mfma_flops.argtypes = [I32]
+    lib.cortex_probe_mfma_flops.restype = ctypes.c_double
+    lib.cortex_probe_mfma.argtypes = [P, I32, P]
+    lib.cortex_probe_mfma.restype = ctypes.c_int
     lib.cortex_version.argtypes = []
     lib.cortex_version.restype = ctypes.c_char_p
     _lib = lib
@@ -199,6 +206,18 @@ def cortex_get_knob(knob: int) -> int:
 
 def cortex_last_grid(which: int) -> int:
     return load().cortex_last_grid(which)
+
+
+def cortex_probe_mfma_sink_floats() -> int:
+    return load().cortex_probe_mfma_sink_floats()
+
+
+def cortex_probe_mfma_flops(iters: int) -> float:
+    return load().cortex_probe_mfma_flops(iters)
+
+
+def cortex_probe_mfma(sink: torch.Tensor, iters: int, stream=None) -> int:
+    return load().cortex_probe_mfma(_ptr(sink), iters, _stream(stream))
 
 
 def cortex_version() -> str:
