@@ -153,6 +153,43 @@ def measured_peaks(stream):
             "note": "register-only fp32 MFMA probe (16x16x4) on every CU; 1 GiB device copy, read + write"}
 
 
+def level_floor(stream, grid, levels):
+    """The fixed cost of a level loop at the forward's grid: an empty
+    persistent launch, and per level the device-wide barrier (what a
+    barrier-per-level schedule pays) and the per-datum all-to-all tagged
+    exchange (what the forward's ordering pays at the least), each from
+    cortex_probe_levels launched back to back with 0 and 64 empty levels."""
+    import torch
+    from paper_2011_01383_amd import cortex as C
+
+    ws = C.workspace(C.cortex_probe_levels_workspace_bytes())
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    reps, deep = 50, 64
+
+    def avg_us(mode, n_levels):
+        run = lambda: C.check(C.cortex_probe_levels(mode, grid, n_levels, status, ws, stream), "cortex_probe_levels")
+        for _ in range(5):
+            run()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            run()
+        b.record(stream)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0, "probe status %d" % int(status.item())
+        return a.elapsed_time(b) * 1e3 / reps
+
+    launch = avg_us(1, 0)
+    barrier = (avg_us(0, deep) - launch) / deep
+    exchange = (avg_us(1, deep) - launch) / deep
+    return {"grid": grid, "levels": levels, "launch_us": launch, "barrier_us_per_level": barrier,
+            "exchange_us_per_level": exchange, "barrier_floor_us": launch + (levels - 1) * barrier,
+            "exchange_floor_us": launch + (levels - 1) * exchange,
+            "note": "empty persistent launch + (levels - 1) x an empty level, 512-thread workgroups"}
+
+
 def cpu_baseline(wl, seconds):
     """The fp64 oracle (linearize + recursive forward) on a bounded sample."""
     from oracle import cortex_oracle as O
@@ -542,11 +579,18 @@ def main():
     roof["algorithmic_flops"] = flops
     roof["algorithmic_bytes"] = byts
 
+    def frac_at(ms):
+        if bound == "mfma":
+            return flops / (ms / 1e3) / 1e12 / PEAK_FP32_TFLOPS
+        return byts / (ms / 1e3) / 1e9 / PEAK_HBM_GBS
+
+    lin_host = dw.lin_host()
+    floor = level_floor(stream, grid_fwd, int(lin_host["num_levels"]))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, args.cpu_seconds)
 
-    lin_host = dw.lin_host()
     out = {
         "metric": METRIC,
         "value": wl.N / (ms_per_step / 1e3),
@@ -565,6 +609,7 @@ def main():
                    "grid_linearize": grid_lin, "grid_forward": grid_fwd, "one_launch": fused},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "level_floor": floor,
         "breakdown": {
             "latency_note": "percentiles from a second pass with an event pair around each step",
             "latency_ms_p10": float(np.percentile(step_ms, 10)),
@@ -574,6 +619,8 @@ def main():
             "two_calls_note": "cortex_linearize and cortex_tree_forward / cortex_dag_forward timed on their own",
             "linearize_kernel_avg_ms": lin_avg_ms,
             "forward_kernel_avg_ms": fwd_avg_ms,
+            "roofline_frac_forward_only": frac_at(fwd_avg_ms),
+            "roofline_frac_end_to_end": frac_at(ms_per_step),
             "measured_fp32_mfma_tflops": peaks["fp32_mfma_tflops"],
             "measured_hbm_copy_gbs": peaks["hbm_copy_gbs"],
             "host_wall_s": wall,

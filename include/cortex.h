@@ -336,6 +336,26 @@ size_t cortex_probe_mfma_sink_floats(void);
 double cortex_probe_mfma_flops(int32_t iters);
 int cortex_probe_mfma(float *d_sink, int32_t iters, void *stream);
 
+/* Level-ordering probe, for the fixed cost a level loop pays before any work:
+ * a persistent launch of `grid` workgroups of 512 threads (1 <= grid <= the
+ * number of compute units, one per unit, as the forward kernels launch) that
+ * runs `levels` empty levels.  mode 0 ends each level with a device-wide
+ * barrier; mode 1 orders levels per datum as the forward kernels do: every
+ * workgroup publishes one (value, tag) pair, in a 128-byte line of its own,
+ * with a device-scope store and waits until the pair of every workgroup
+ * carries that level's tag.
+ * levels = 0 measures the launch alone.  d_ws (device, caller-owned, at least
+ * cortex_probe_levels_workspace_bytes()) must be zeroed before its first use
+ * and again after a launch that ended with a non-zero *d_status; every wait is
+ * bounded by CORTEX_KNOB_BARRIER_TIMEOUT_US and raises
+ * CORTEX_ST_BARRIER_TIMEOUT when it runs out.  Returns CORTEX_E_INVAL (NULL
+ * pointer, mode not 0 or 1, levels < 0, grid < 1), CORTEX_E_TOO_LARGE (grid
+ * above the compute-unit count), CORTEX_E_WORKSPACE or CORTEX_E_HIP, and then
+ * enqueues nothing.  Calls that share a workspace must not overlap. */
+size_t cortex_probe_levels_workspace_bytes(void);
+int cortex_probe_levels(int32_t mode, int32_t grid, int32_t levels, int32_t *d_status, void *d_ws,
+                        size_t ws_bytes, void *stream);
+
 /* Library version string. */
 const char *cortex_version(void);
 

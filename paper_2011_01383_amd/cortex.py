@@ -58,6 +58,7 @@ EXPORTED = [
     "cortex_set_knob", "cortex_get_knob",
     "cortex_last_grid", "cortex_version",
     "cortex_probe_mfma_sink_floats", "cortex_probe_mfma_flops", "cortex_probe_mfma",
+    "cortex_probe_levels_workspace_bytes", "cortex_probe_levels",
 ]
 
 
@@ -117,6 +118,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cortex_probe_mfma_flops.restype = ctypes.c_double
     lib.cortex_probe_mfma.argtypes = [P, I32, P]
     lib.cortex_probe_mfma.restype = ctypes.c_int
+    lib.cortex_probe_levels_workspace_bytes.argtypes = []
+    lib.cortex_probe_levels_workspace_bytes.restype = SZ
+    lib.cortex_probe_levels.argtypes = [I32, I32, I32, P, P, SZ, P]
+    lib.cortex_probe_levels.restype = ctypes.c_int
     lib.cortex_version.argtypes = []
     lib.cortex_version.restype = ctypes.c_char_p
     _lib = lib
@@ -218,6 +223,16 @@ def cortex_probe_mfma_flops(iters: int) -> float:
 
 def cortex_probe_mfma(sink: torch.Tensor, iters: int, stream=None) -> int:
     return load().cortex_probe_mfma(_ptr(sink), iters, _stream(stream))
+
+
+def cortex_probe_levels_workspace_bytes() -> int:
+    return load().cortex_probe_levels_workspace_bytes()
+
+
+def cortex_probe_levels(mode: int, grid: int, levels: int, status: torch.Tensor, ws: torch.Tensor,
+                        stream=None) -> int:
+    return load().cortex_probe_levels(mode, grid, levels, _ptr(status), _ptr(ws), ws.numel() * ws.element_size(),
+                                      _stream(stream))
 
 
 def cortex_version() -> str:
