@@ -765,6 +765,12 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   constexpr bool kLeafInputs = CELL == CORTEX_TREE_RNN || CELL == CORTEX_NARY_TREELSTM;
   constexpr bool kLstm = CELL == CORTEX_NARY_TREELSTM;
   constexpr int EPI = kTileM * J;          // (row, unit) pairs of a tile
+  // Gate rows beyond the last full 16-row MFMA tile: when only four remain
+  // (N-ary TreeLSTM, J = 4: the u gate), an MFMA tile would be three-quarters
+  // padding, so they are contracted on the vector ALU, from the same operand
+  // registers, while the matrix cores run the full tiles.
+  constexpr bool kVecTail = GJ % 16 == 4 && NT >= 2;
+  constexpr int NTM = kVecTail ? NT - 1 : NT;    // MFMA tiles of gate rows
   constexpr int SEGS = SrcCfg<CELL>::SEGS;
   // A block's 16 columns never straddle two operand segments (H is a
   // multiple of 16), so the segment of block b is the same for the whole
@@ -944,33 +950,51 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
       floatx4 acc0[NT], acc1[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc0[nt] = acc1[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      // vector-ALU rows: this lane's row i16 over its 4 NB columns, for the
+      // four gate rows 16 NTM .. +3
+      float tail[4] = {0.f, 0.f, 0.f, 0.f};
       if constexpr (!kWeightsFromMemory) {
         const float *brow = &W_s[i16 * LDW + kw + 4 * g4];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const float4 av = f[b].value(code_b(cd, b) >= 0);
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
+          for (int nt = 0; nt < NTM; ++nt) {
             const float4 bv = *(const float4 *)(brow + nt * 16 * LDW + 16 * b);
             if (b & 1) acc1[nt] = mfma_k16(av, bv, acc1[nt]);
             else acc0[nt] = mfma_k16(av, bv, acc0[nt]);
+          }
+          if constexpr (kVecTail) {
+            const float *trow = &W_s[16 * NTM * LDW + kw + 16 * b + 4 * g4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float4 w = *(const float4 *)(trow + q * LDW);
+              tail[q] = fmaf(av.x, w.x, fmaf(av.y, w.y, fmaf(av.z, w.z, fmaf(av.w, w.w, tail[q]))));
+            }
           }
         }
       } else {
         // ablation: no model persistence; the same weight-slice values,
         // read from the weight tensors at every tile
-        float4 bw[NB][NT];
+        float4 bw[NB][NTM];
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) bw[b][nt] = weight_slice_at<CELL, H, J>(a, hbase, nt * 16 + i16, kw + 16 * b + 4 * g4);
+          for (int nt = 0; nt < NTM; ++nt) bw[b][nt] = weight_slice_at<CELL, H, J>(a, hbase, nt * 16 + i16, kw + 16 * b + 4 * g4);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const float4 av = f[b].value(code_b(cd, b) >= 0);
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
+          for (int nt = 0; nt < NTM; ++nt) {
             if (b & 1) acc1[nt] = mfma_k16(av, bw[b][nt], acc1[nt]);
             else acc0[nt] = mfma_k16(av, bw[b][nt], acc0[nt]);
+          }
+          if constexpr (kVecTail) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float4 w = weight_slice_at<CELL, H, J>(a, hbase, 16 * NTM + q, kw + 16 * b + 4 * g4);
+              tail[q] = fmaf(av.x, w.x, fmaf(av.y, w.y, fmaf(av.z, w.z, fmaf(av.w, w.w, tail[q]))));
+            }
           }
         }
       }
@@ -979,10 +1003,20 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
       // (vector memory operations retire in order, so their first use
       // waits for them alone).
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
+      for (int nt = 0; nt < NTM; ++nt)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
           C_s[(wave * kTileM + 4 * g4 + v) * MPAD + nt * 16 + i16] = acc0[nt][v] + acc1[nt][v];
+      if constexpr (kVecTail) {
+        // the four lanes of row i16 (lane groups g4) hold disjoint column sets
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          tail[q] += __shfl_xor(tail[q], 16);
+          tail[q] += __shfl_xor(tail[q], 32);
+        }
+        if (g4 == 0)
+          *(float4 *)&C_s[(wave * kTileM + i16) * MPAD + 16 * NTM] = make_float4(tail[0], tail[1], tail[2], tail[3]);
+      }
       __syncthreads();
       CORTEX_TRACE_POINT(l, 3);
       // ---- gates: one thread per (row, gate row) sums the wave partials

@@ -119,8 +119,9 @@ def test_uncached_structure(name):
 
 @pytest.mark.parametrize("groups", [0, 1])
 def test_slice_units_change_only_the_schedule(groups):
-    """Two hidden units per slice instead of four: the same sums in the same
-    order, so the states are bitwise identical."""
+    """Two hidden units per slice instead of four: the same contractions; at
+    four units the u gate's rows are summed on the vector ALU (in another order
+    than the MFMA tiles), so the states agree to fp32 rounding."""
     wl = cached_workload(1, groups)
     announce("slice units 2 vs default, seed %d, groups %d" % (groups, groups))
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 0)
@@ -130,7 +131,7 @@ def test_slice_units_change_only_the_schedule(groups):
     assert C.cortex_last_grid(1) == 128 * (groups if groups else 2)
     got = dw.states_by_node()
     for key in ref:
-        assert np.array_equal(ref[key], got[key]), key
+        assert float(np.abs(ref[key] - got[key]).max()) <= 1e-5, key
     compare_states(got, cached_oracle(1, groups), wl.name)
 
 
