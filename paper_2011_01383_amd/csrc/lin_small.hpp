@@ -167,6 +167,182 @@ struct SmallLin {
   } while (0)
 #endif
 
+// ---------------------------------------------------------------------------
+// Batches of at most 64 * kWavePer nodes: wave 0 linearizes alone, with no
+// workgroup barrier (the others wait at one).  One wave's LDS operations are
+// performed in program order, so a value one lane stores is what any lane
+// of the wave loads afterwards; compiler fences keep that order.  Node v
+// sits in lane v % 64, slot v / 64.
+//   heights  rounds of h(v) = 1 + max over its children (0 for a leaf), all
+//            nodes in every round, until a round changes nothing: values only
+//            grow and never pass the true height, so the fixed point is the
+//            height; a value >= N proves a cycle;
+//   offsets  level counts by LDS atomics, then an exclusive scan by the wave
+//            in chunks of 64 levels;
+//   rows     slots in order (ids ascending); within a slot the lanes of one
+//            height are matched by ballots on the height's bits and ranked by
+//            lane, after the rows already taken in that level (a cursor per
+//            level): the stable (height, id) order.
+// Same LDS layout and results as the multi-wave path below.
+// ---------------------------------------------------------------------------
+constexpr int kWavePer = 2;
+
+template <int THREADS, int KS>
+__device__ int wave_linearize(const int32_t *children, int N, int K, int32_t *status, int status0, int *sm,
+                              SmallLin &m, uint64_t *stamps) {
+  (void)stamps;
+  const int tid = threadIdx.x, lane = tid & 63;
+  int *ch = sm;                       // [N*K]
+  int *hgt = ch + N * K;              // [N]
+  int *perm0 = hgt + N;               // [N]  row -> node
+  int *perm1 = perm0 + N;             // [N]  level cursors
+  int *nrow = perm1 + N;              // [N]
+  int *lcount = nrow + N;             // [N+1]
+  int *flags = lcount + N + 1 + (THREADS / 64) * 256 + 2 * 256;   // [64] scratch
+  if (tid < 64) {
+    int myc[kWavePer][KS], myh[kWavePer];
+#pragma unroll
+    for (int p = 0; p < kWavePer; ++p)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const int v = lane + 64 * p;
+        myc[p][s] = children[(v < N && s < K) ? (size_t)v * K + s : 0];
+      }
+    int bad = 0;
+#pragma unroll
+    for (int p = 0; p < kWavePer; ++p) {
+      const int v = lane + 64 * p;
+      myh[p] = 0;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        int c = (v < N && s < K) ? myc[p][s] : -1;
+        if (c < -1 || c >= N) { bad = 1; c = -1; }
+        myc[p][s] = c;
+        if (v < N && s < K) lds_store(&ch[v * K + s], c);
+      }
+      if (v < N) {
+        lds_store(&hgt[v], 0);
+        lds_store(&lcount[v], 0);
+      }
+    }
+    LIN_STAMP(1);
+    int err = __shfl(status0, 0) != 0 ? -1 : (__ballot(bad) != 0ull ? CORTEX_ST_CHILD_RANGE : 0);
+    int L = 0;
+    const int nslots = (N + 63) >> 6;
+    if (err == 0) {
+      for (;;) {
+        // a round: every child height is requested first, then every node
+        // updated, so the round costs one LDS round trip
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        int hv[kWavePer][KS];
+#pragma unroll
+        for (int p = 0; p < kWavePer; ++p)
+          if (p < nslots) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s) hv[p][s] = lds_load(&hgt[myc[p][s] >= 0 ? myc[p][s] : 0]);
+          }
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        bool changed = false, cyc = false;
+#pragma unroll
+        for (int p = 0; p < kWavePer; ++p) {
+          const int v = lane + 64 * p;
+          if (p >= nslots) break;
+          int mx = -1;
+#pragma unroll
+          for (int s = 0; s < KS; ++s) mx = max(mx, myc[p][s] >= 0 ? hv[p][s] : -1);
+          if (v < N && mx + 1 > myh[p]) {
+            myh[p] = mx + 1;
+            lds_store(&hgt[v], mx + 1);
+            changed = true;
+            if (mx + 1 >= N) cyc = true;
+          }
+        }
+        if (__ballot(cyc) != 0ull) {
+          err = CORTEX_ST_CYCLE;
+          break;
+        }
+        if (__ballot(changed) == 0ull) break;
+      }
+    }
+    LIN_STAMP(2);
+    if (err == 0) {
+      int mx = 0;
+#pragma unroll
+      for (int p = 0; p < kWavePer; ++p)
+        if (lane + 64 * p < N) mx = max(mx, myh[p]);
+      for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
+      L = mx + 1;
+      // level counts (lcount was cleared above, by this wave)
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+#pragma unroll
+      for (int p = 0; p < kWavePer; ++p)
+        if (lane + 64 * p < N)
+          __hip_atomic_fetch_add(&lcount[myh[p]], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      // exclusive scan into lcount (level offsets) and perm1 (cursors)
+      int carry = 0;
+      for (int base = 0; base < L; base += 64) {
+        const int l = base + lane;
+        const int cnt = l < L ? lds_load(&lcount[l]) : 0;
+        int x = cnt;
+        for (int off = 1; off < 64; off <<= 1) {
+          const int y = __shfl_up(x, off);
+          if (lane >= off) x += y;
+        }
+        if (l < L) {
+          lds_store(&lcount[l], carry + x - cnt);
+          lds_store(&perm1[l], carry + x - cnt);
+        }
+        carry += __shfl(x, 63);
+      }
+      LIN_STAMP(3);
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      const int nbits = 32 - __clz(L - 1);                      // bits of the largest height
+      const unsigned long long lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+#pragma unroll
+      for (int p = 0; p < kWavePer; ++p) {
+        const int v = lane + 64 * p;
+        if (p >= nslots) break;
+        const bool valid = v < N;
+        const int dig = valid ? myh[p] : 0;
+        unsigned long long peers = __ballot(valid);
+        for (int b = 0; b < nbits; ++b) {
+          const bool bit = (dig >> b) & 1;
+          const unsigned long long mb = __ballot(bit);
+          peers &= bit ? mb : ~mb;
+        }
+        const int base = lds_load(&perm1[dig]);                // every lane reads before any writes
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        const int row = base + __popcll(peers & lt_mask);
+        if (valid) {
+          if ((peers & lt_mask) == 0ull) lds_store(&perm1[dig], base + __popcll(peers));
+          lds_store(&perm0[row], v);
+          lds_store(&nrow[v], row);
+        }
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      }
+      LIN_STAMP(4);
+    }
+    if (lane == 0) {
+      flags[0] = err == 0 ? L : 0;
+      flags[1] = err;
+    }
+  }
+  __syncthreads();
+  const int L = flags[0], err = flags[1];
+  if (err > 0) {
+    if (tid == 0) raise_status(status, err);
+    return 0;
+  }
+  if (err != 0) return 0;
+  m.ch = ch;
+  m.hgt = hgt;
+  m.nrow = nrow;
+  m.lcount = lcount;
+  m.order = perm0;
+  return L;
+}
+
 // Returns L >= 1, or 0 (uniformly) after raising a status: a child index out
 // of range, a cycle, or a non-zero status on entry.
 template <int THREADS, int PER>
@@ -188,6 +364,9 @@ __device__ int small_linearize(const int32_t *children, int N, int K, int32_t *s
 
   LIN_STAMP(0);
   const int status0 = load_status(status);     // requested together with the children
+  if (N <= 64 * kWavePer)
+    return K <= 2 ? wave_linearize<THREADS, 2>(children, N, K, status, status0, sm, m, stamps)
+                  : wave_linearize<THREADS, 4>(children, N, K, status, status0, sm, m, stamps);
   // 1. children: into registers for the sweeps (node v = tid + j*threads) and
   //    into LDS for the output phase; range check
   int myc[PER][4], myh[PER];

@@ -195,3 +195,38 @@ def test_deterministic_repeats():
         st2, again, _ = gpu_linearize(wl.children, 2)
         assert st2 == 0
         compare_lin(again, first, 2)
+
+
+@pytest.mark.parametrize("K", [1, 2, 4])
+def test_single_wave_sizes(K):
+    """Batches of at most 128 nodes are linearized by one wave; sizes around
+    its limits and around a wave's 64 lanes, random DAGs, chains (one node per
+    level) and shuffled ids, bit-exact against the oracle."""
+    rng = np.random.default_rng(128 + K)
+    for N in (1, 2, 31, 63, 64, 65, 100, 127, 128, 129, 130):
+        cases = [I.random_dag(rng, N, K, p_absent=float(rng.uniform(0.0, 0.8)))]
+        chain = np.full((N, K), -1, dtype=np.int32)
+        chain[1:, K - 1] = np.arange(N - 1, dtype=np.int32)            # node v's last slot holds v - 1
+        cases.append(chain.reshape(-1))
+        perm = rng.permutation(N).astype(np.int32)
+        cases.append(I.relabel(chain.reshape(-1), K, perm))
+        for i, ch in enumerate(cases):
+            announce("single-wave N=%d K=%d case %d" % (N, K, i))
+            st, got, _ = gpu_linearize(ch, K, 0)
+            assert st == 0, (N, K, i)
+            compare_lin(got, O.linearize(ch, K), K)
+
+
+def test_single_wave_errors():
+    """Range errors and cycles in batches small enough for the one-wave path."""
+    announce("single-wave errors")
+    assert gpu_linearize(np.array([0], np.int32), 1, 0)[0] == C.CORTEX_ST_CYCLE
+    ring = np.roll(np.arange(100, dtype=np.int32), 1)                    # 100-node cycle
+    assert gpu_linearize(ring, 1, 0)[0] == C.CORTEX_ST_CYCLE
+    ch = np.array([-1, -1, 0, 2, 3, -1, 1, -1], dtype=np.int32)         # 1 -> 2 -> 3 -> 1 under a tree
+    assert gpu_linearize(ch, 2, 0)[0] == C.CORTEX_ST_CYCLE
+    assert gpu_linearize(np.array([-1, -1, 0, 7, 1, 2], np.int32), 2, 0)[0] == C.CORTEX_ST_CHILD_RANGE
+    assert gpu_linearize(np.array([-1, -1, -5, 0], np.int32), 2, 0)[0] == C.CORTEX_ST_CHILD_RANGE
+    big = np.full(128 * 4, -1, dtype=np.int32)
+    big[127 * 4 + 3] = 128                                               # last slot of the last node
+    assert gpu_linearize(big, 4, 0)[0] == C.CORTEX_ST_CHILD_RANGE
