@@ -413,6 +413,7 @@ __device__ int small_linearize(const int32_t *children, int N, int K, int32_t *s
   //    raise lands before the decrement and the last decrement sees every
   //    sibling's raise.
   int *npar = perm0, *parent = nrow, *pend = lcount;
+  int multi = 0;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int v = tid + j * THREADS;
@@ -430,17 +431,11 @@ __device__ int small_linearize(const int32_t *children, int N, int K, int32_t *s
     for (int s = 0; s < 4; ++s) {
       const int c = myc[j][s];
       if (c >= 0) {
-        __hip_atomic_fetch_add(&npar[c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        // a second parent of c is seen by the thread whose increment finds 1
+        if (__hip_atomic_fetch_add(&npar[c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) != 0) multi = 1;
         parent[c] = v;
       }
     }
-  }
-  __syncthreads();
-  int multi = 0;
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int v = tid + j * THREADS;
-    if (v < N && npar[v] > 1) multi = 1;
   }
   if (!__syncthreads_or(multi)) {
 #pragma unroll 1
@@ -500,9 +495,22 @@ __device__ int small_linearize(const int32_t *children, int N, int K, int32_t *s
   L += 1;
   for (int v = tid; v < N; v += THREADS) atomicAdd(&lcount[hgt[v]], 1);
   __syncthreads();
-  // level offsets = exclusive scan of the level counts (kept in lcount)
-  const int total = block_exclusive_scan<THREADS>(lcount, L, flags);
-  (void)total;                      // = N: every node has a level
+  // level offsets = exclusive scan of the level counts (kept in lcount): by
+  // wave 0 alone up to 64 levels, else by the whole workgroup
+  if (L <= 64) {
+    if (tid < 64) {
+      const int cnt = tid < L ? lcount[tid] : 0;
+      int x = cnt;
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+      }
+      if (tid < L) lcount[tid] = x - cnt;
+    }
+    __syncthreads();
+  } else {
+    block_exclusive_scan<THREADS>(lcount, L, flags);
+  }
   LIN_STAMP(3);
   // 3. stable LSD counting sort on height, 8-bit digits.  With one pass
   //    (L <= 256) the digit is the height itself: its starts are the level
