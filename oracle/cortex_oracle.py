@@ -21,8 +21,8 @@ The oracle is therefore the plain recursive definition:
   leaf case + recursive case) returning every node's state in node-id order.
 * ``forward_levels``: the same cell evaluated level by level over the
   linearization (the loop nest of Sec. 4.1), used to check order invariance.
-* ``paper_linearize_trees``: the paper's DFS linearizer for trees (Sec. 4.2),
-  generalised to K slots, used to pin ``linearize``.
+* ``dfs_batches``: the depth-first, post-order batching the paper describes
+  for trees (Sec. 4.2), with K slots, used to pin ``linearize``.
 
 All arithmetic is float64 on float32 inputs (upcast once), with
 sigma(z) = 1/(1+exp(-z)) and numpy's tanh/exp.  An absent child slot (-1)
@@ -160,44 +160,49 @@ def linearize(children: np.ndarray, K: int) -> Dict[str, np.ndarray]:
     }
 
 
-def paper_linearize_trees(children: np.ndarray, K: int):
-    """The paper's DFS linearizer for trees (Sec. 4.2), with K child slots.
+def dfs_batches(children: np.ndarray, K: int) -> List[List[int]]:
+    """Batches of a tree forest in depth-first post-order (Sec. 4.2).
 
-    Roots (nodes that are nobody's child) are visited in ascending id.  A leaf
-    is appended to the leaf batch; an internal node first linearizes its
-    children, then is appended to the internal batch of its height.  Returns
-    ``(leaf_batch, internal_batches)`` where ``internal_batches[j]`` holds the
-    nodes of height j+1 (the pseudocode's list-of-lists index, read as
-    starting at the first internal height).
+    The paper linearizes a tree by visiting it depth first and appending each
+    node, once all of its children are done, to the batch of its height; leaves
+    form batch 0.  Here the traversal is an explicit stack over the roots
+    (nodes that fill no child slot) in ascending id: a frame is a node and the
+    next child slot to descend into.  When a frame has no slot left, its
+    node's height is one more than the largest child height (0 without
+    children) and the node is appended to ``batches[height]``.
+
+    Returns ``batches``: ``batches[h]`` lists the nodes of height h in the
+    order the traversal completes them.
     """
     children = np.asarray(children, dtype=np.int32)
     N = children.size // K
-    is_child = np.zeros(N, dtype=bool)
+    has_parent = np.zeros(N, dtype=bool)
     for c in children:
         if c >= 0:
-            is_child[c] = True
-    leaf_batch: List[int] = []
-    internal_batches: List[List[int]] = []
-    height: Dict[int, int] = {}
-
-    def lin(n: int) -> int:
-        kids = [c for c in _kids(children, K, n) if c >= 0]
-        if not kids:
-            leaf_batch.append(n)
-            height[n] = 0
-            return 0
-        hh = 1 + max(lin(c) for c in kids)
-        height[n] = hh
-        while len(internal_batches) < hh:
-            internal_batches.append([])
-        internal_batches[hh - 1].append(n)
-        return hh
-
-    with _deep_recursion(N + 1000):
-        for root in range(N):
-            if not is_child[root]:
-                lin(root)
-    return leaf_batch, internal_batches
+            has_parent[c] = True
+    height = np.full(N, -1, dtype=np.int64)
+    batches: List[List[int]] = []
+    for root in range(N):
+        if has_parent[root]:
+            continue
+        stack = [[root, 0]]
+        while stack:
+            frame = stack[-1]
+            node, slot = frame
+            if slot < K:
+                frame[1] = slot + 1
+                c = int(children[node * K + slot])
+                if c >= 0:
+                    stack.append([c, 0])
+                continue
+            stack.pop()
+            kid_heights = [int(height[c]) for c in _kids(children, K, node) if c >= 0]
+            hgt = 1 + max(kid_heights) if kid_heights else 0
+            height[node] = hgt
+            while len(batches) <= hgt:
+                batches.append([])
+            batches[hgt].append(node)
+    return batches
 
 
 # ---------------------------------------------------------------------------
@@ -372,24 +377,3 @@ def forward_workload(wl) -> Dict[str, np.ndarray]:
     """Convenience wrapper over an ``inputs.Workload``-like object."""
     return forward(wl.cell, wl.children, wl.K, wl.H, x_index=wl.x_index, x_table=wl.x_table,
                    leaf_mat=wl.leaf_mat, x=wl.x, W=wl.W, U=wl.U, b=wl.b, W_M=wl.W_M)
-
-
-def node_state(wl, v: int, memo: Optional[Dict[int, tuple]] = None) -> tuple:
-    """State of a single node (memoized over its descendants only).
-
-    Used to check sampled outputs of workloads too large to evaluate whole.
-    """
-    p = _Params(wl.cell, wl.H, wl.K, x_index=wl.x_index, x_table=wl.x_table,
-                leaf_mat=wl.leaf_mat, x=wl.x, W=wl.W, U=wl.U, b=wl.b, W_M=wl.W_M)
-    memo = {} if memo is None else memo
-    children = np.asarray(wl.children, dtype=np.int32)
-
-    def state(u: int) -> tuple:
-        if u in memo:
-            return memo[u]
-        kids = [None if c < 0 else state(c) for c in _kids(children, wl.K, u)]
-        memo[u] = cell_apply(p, u, kids)
-        return memo[u]
-
-    with _deep_recursion(wl.N + 1000):
-        return state(int(v))

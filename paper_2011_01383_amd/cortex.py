@@ -132,6 +132,87 @@ def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
 
+def _need(t, name: str, dtype: torch.dtype, min_numel: int, optional: bool = False) -> None:
+    """Reject a tensor the library would misread: the library takes raw
+    pointers, so a wrong dtype, a strided view, too few elements or host
+    memory would be read as something else (or past the allocation)."""
+    _need_all([(t, name, dtype, min_numel, optional)])
+
+
+def _need_all(specs) -> None:
+    """_need over several tensors: every dtype, layout and size first, then
+    that each tensor is in device memory."""
+    for t, name, dtype, min_numel, optional in specs:
+        if t is None:
+            if optional:
+                continue
+            raise ValueError("%s is required" % name)
+        if not isinstance(t, torch.Tensor):
+            raise ValueError("%s must be a torch.Tensor, got %s" % (name, type(t).__name__))
+        if dtype is not None and t.dtype != dtype:
+            raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % name)
+        if t.numel() < min_numel:
+            raise ValueError("%s holds %d elements, needs at least %d" % (name, t.numel(), min_numel))
+    for t, name, _, _, _ in specs:
+        if t is not None and not t.is_cuda:
+            raise ValueError("%s must be in device memory" % name)
+
+
+def _need_count(v: int, name: str) -> None:
+    if int(v) < 0:
+        raise ValueError("%s must be non-negative, got %d" % (name, int(v)))
+
+
+# Elements of each weight tensor per cell, as functions of H (layouts of the
+# header: row-major [out, in] float32).
+_WEIGHT_ELEMS = {
+    CORTEX_TREE_RNN: {"W": lambda H: 2 * H * H, "b": lambda H: H},
+    CORTEX_NARY_TREELSTM: {"U": lambda H: 10 * H * H, "b": lambda H: 5 * H},
+    CORTEX_CHILDSUM_TREELSTM: {"W": lambda H: 4 * H * H, "U": lambda H: 4 * H * H, "b": lambda H: 4 * H},
+    CORTEX_MVRNN: {"W": lambda H: 2 * H * H, "W_M": lambda H: 2 * H * H},
+    CORTEX_CHILDSUM_TREEGRU: {"W": lambda H: 3 * H * H, "U": lambda H: 3 * H * H, "b": lambda H: 3 * H},
+    CORTEX_SIMPLE_TREEGRU: {"W": lambda H: 3 * H * H, "U": lambda H: 3 * H * H, "b": lambda H: 3 * H},
+}
+
+
+def _check_tree_args(cell: int, H: int, N: int, x_table, x_rows: int, x_index, leaf_mat, weights: dict, h,
+                     c_or_P, status, ws) -> None:
+    if cell not in _WEIGHT_ELEMS:
+        return                      # the library rejects the cell id itself
+    _need_count(H, "H")
+    _need_count(x_rows, "x_rows")
+    f32, i32 = torch.float32, torch.int32
+    specs = [(x_table, "x_table", f32, x_rows * H, x_rows == 0), (x_index, "x_index", i32, N, False)]
+    if cell == CORTEX_MVRNN:
+        specs.append((leaf_mat, "leaf_mat", f32, x_rows * H * H, x_rows == 0))
+    for name, elems in _WEIGHT_ELEMS[cell].items():
+        specs.append((weights.get(name), name, f32, elems(H), False))
+    specs.append((h, "h", f32, N * H, False))
+    if cell in (CORTEX_NARY_TREELSTM, CORTEX_CHILDSUM_TREELSTM):
+        specs.append((c_or_P, "c", f32, N * H, False))
+    elif cell == CORTEX_MVRNN:
+        specs.append((c_or_P, "P", f32, N * H * H, False))
+    specs += [(status, "status", i32, 1, False), (ws, "ws", None, 1, False)]
+    _need_all(specs)
+
+
+def _check_dag_args(H: int, N: int, x, W, U, b, h, status, ws) -> None:
+    _need_count(H, "H")
+    f32 = torch.float32
+    _need_all([(x, "x", f32, N * H, False), (W, "W", f32, H * H, False), (U, "U", f32, 2 * H * H, False),
+               (b, "b", f32, H, False), (h, "h", f32, N * H, False), (status, "status", torch.int32, 1, False),
+               (ws, "ws", None, 1, False)])
+
+
+def _check_lin(lin: "Linearization", N: int, K: int) -> None:
+    if not isinstance(lin, Linearization):
+        raise ValueError("lin must be a Linearization")
+    if lin.N != N or lin.K != K:
+        raise ValueError("lin was allocated for N=%d K=%d, the call has N=%d K=%d" % (lin.N, lin.K, N, K))
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -150,6 +231,12 @@ def cortex_forward_workspace_bytes(cell: int, N: int, H: int) -> int:
 
 def cortex_linearize(children: torch.Tensor, N: int, K: int, lin: "Linearization",
                      status: torch.Tensor, ws: torch.Tensor, stream=None) -> int:
+    _need_count(N, "N")
+    _need_count(K, "K")
+    _need(children, "children", torch.int32, N * K)
+    _check_lin(lin, N, K)
+    _need(status, "status", torch.int32, 1)
+    _need(ws, "ws", None, 1)
     return load().cortex_linearize(_ptr(children), N, K, ctypes.byref(lin.struct), _ptr(status),
                                    _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
 
@@ -159,6 +246,9 @@ def cortex_tree_forward(cell: int, H: int, lin: "Linearization", x_table: Option
                         W=None, U=None, b=None, W_M=None, h: torch.Tensor = None,
                         c_or_P: Optional[torch.Tensor] = None, status: torch.Tensor = None,
                         ws: torch.Tensor = None, stream=None) -> int:
+    _check_lin(lin, lin.N, lin.K)
+    _check_tree_args(cell, H, lin.N, x_table, x_rows, x_index, leaf_mat, {"W": W, "U": U, "b": b, "W_M": W_M},
+                     h, c_or_P, status, ws)
     w = cortex_weights_t(_ptr(W), _ptr(U), _ptr(b), _ptr(W_M))
     return load().cortex_tree_forward(cell, H, ctypes.byref(lin.struct), _ptr(x_table), x_rows,
                                       _ptr(x_index), _ptr(leaf_mat), ctypes.byref(w), _ptr(h),
@@ -169,6 +259,8 @@ def cortex_tree_forward(cell: int, H: int, lin: "Linearization", x_table: Option
 def cortex_dag_forward(H: int, lin: "Linearization", x: torch.Tensor, W: torch.Tensor,
                        U: torch.Tensor, b: torch.Tensor, h: torch.Tensor, status: torch.Tensor,
                        ws: torch.Tensor, stream=None) -> int:
+    _check_lin(lin, lin.N, lin.K)
+    _check_dag_args(H, lin.N, x, W, U, b, h, status, ws)
     return load().cortex_dag_forward(H, ctypes.byref(lin.struct), _ptr(x), _ptr(W), _ptr(U), _ptr(b),
                                      _ptr(h), _ptr(status), _ptr(ws), ws.numel() * ws.element_size(),
                                      _stream(stream))
@@ -183,6 +275,10 @@ def cortex_tree_infer(cell: int, H: int, children: torch.Tensor, lin: "Lineariza
                       leaf_mat: Optional[torch.Tensor], W=None, U=None, b=None, W_M=None,
                       h: torch.Tensor = None, c_or_P: Optional[torch.Tensor] = None,
                       status: torch.Tensor = None, ws: torch.Tensor = None, stream=None) -> int:
+    _check_lin(lin, lin.N, lin.K)
+    _need(children, "children", torch.int32, lin.N * lin.K)
+    _check_tree_args(cell, H, lin.N, x_table, x_rows, x_index, leaf_mat, {"W": W, "U": U, "b": b, "W_M": W_M},
+                     h, c_or_P, status, ws)
     w = cortex_weights_t(_ptr(W), _ptr(U), _ptr(b), _ptr(W_M))
     return load().cortex_tree_infer(cell, H, _ptr(children), ctypes.byref(lin.struct), _ptr(x_table), x_rows,
                                     _ptr(x_index), _ptr(leaf_mat), ctypes.byref(w), _ptr(h), _ptr(c_or_P),
@@ -196,6 +292,9 @@ def cortex_dag_infer_workspace_bytes(N: int, K: int, H: int) -> int:
 def cortex_dag_infer(H: int, children: torch.Tensor, lin: "Linearization", x: torch.Tensor, W: torch.Tensor,
                      U: torch.Tensor, b: torch.Tensor, h: torch.Tensor, status: torch.Tensor, ws: torch.Tensor,
                      stream=None) -> int:
+    _check_lin(lin, lin.N, lin.K)
+    _need(children, "children", torch.int32, lin.N * lin.K)
+    _check_dag_args(H, lin.N, x, W, U, b, h, status, ws)
     return load().cortex_dag_infer(H, _ptr(children), ctypes.byref(lin.struct), _ptr(x), _ptr(W), _ptr(U),
                                    _ptr(b), _ptr(h), _ptr(status), _ptr(ws), ws.numel() * ws.element_size(),
                                    _stream(stream))
@@ -222,6 +321,7 @@ def cortex_probe_mfma_flops(iters: int) -> float:
 
 
 def cortex_probe_mfma(sink: torch.Tensor, iters: int, stream=None) -> int:
+    _need(sink, "sink", torch.float32, cortex_probe_mfma_sink_floats())
     return load().cortex_probe_mfma(_ptr(sink), iters, _stream(stream))
 
 
@@ -231,6 +331,8 @@ def cortex_probe_levels_workspace_bytes() -> int:
 
 def cortex_probe_levels(mode: int, grid: int, levels: int, status: torch.Tensor, ws: torch.Tensor,
                         stream=None) -> int:
+    _need(status, "status", torch.int32, 1)
+    _need(ws, "ws", None, 1)
     return load().cortex_probe_levels(mode, grid, levels, _ptr(status), _ptr(ws), ws.numel() * ws.element_size(),
                                       _stream(stream))
 
@@ -254,6 +356,10 @@ class Linearization:
     child_rows: torch.Tensor
 
     def __post_init__(self):
+        sizes = {"num_levels": 1, "height": self.N, "level_offsets": self.N + 1, "level_nodes": self.N,
+                 "node_row": self.N, "child_rows": self.N * self.K}
+        for name, n in sizes.items():
+            _need(getattr(self, name), name, torch.int32, n)
         self.struct = cortex_lin_t(self.N, self.K, _ptr(self.num_levels), _ptr(self.height),
                                    _ptr(self.level_offsets), _ptr(self.level_nodes),
                                    _ptr(self.node_row), _ptr(self.child_rows))

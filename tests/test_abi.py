@@ -101,3 +101,64 @@ def test_tree_unroll_knob_range(lib):
     for v in (2, 1, 0):
         assert C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL, v) == C.CORTEX_OK
         assert C.cortex_get_knob(C.CORTEX_KNOB_TREE_UNROLL) == v
+
+
+# ---- the binding rejects tensors the library would misread (no GPU needed) ----
+
+def _cpu(n, dtype):
+    import torch
+    return torch.zeros(n, dtype=dtype)
+
+
+def test_binding_rejects_wrong_dtype_before_the_call():
+    import torch
+    # an int64 children array would be read as int32 pairs: a different tree
+    with pytest.raises(ValueError, match="children must be torch.int32"):
+        C.cortex_linearize(_cpu(20, torch.int64), 10, 2, None, None, None)
+    with pytest.raises(ValueError, match="x must be torch.float32"):
+        C._check_dag_args(256, 4, _cpu(4 * 256, torch.float16), None, None, None, None, None, None)
+
+
+def test_binding_rejects_short_and_strided_tensors():
+    import torch
+    with pytest.raises(ValueError, match="children holds 19 elements, needs at least 20"):
+        C.cortex_linearize(_cpu(19, torch.int32), 10, 2, None, None, None)
+    strided = torch.zeros(40, dtype=torch.int32)[::2]
+    with pytest.raises(ValueError, match="children must be contiguous"):
+        C.cortex_linearize(strided, 10, 2, None, None, None)
+    with pytest.raises(ValueError, match="N must be non-negative"):
+        C.cortex_linearize(_cpu(4, torch.int32), -2, 2, None, None, None)
+
+
+def test_binding_rejects_host_memory():
+    import torch
+    with pytest.raises(ValueError, match="children must be in device memory"):
+        C.cortex_linearize(_cpu(20, torch.int32), 10, 2, None, None, None)
+    with pytest.raises(ValueError, match="num_levels must be in device memory"):
+        C.Linearization.alloc(10, 2, device="cpu")
+
+
+def test_binding_checks_weight_and_table_sizes():
+    import torch
+    H, N = 64, 5
+    f32 = torch.float32
+    idx = _cpu(N, torch.int32)
+    # x_rows larger than the table: the buffer descriptor would cover memory past it
+    with pytest.raises(ValueError, match="x_table holds 640 elements, needs at least 704"):
+        C._check_tree_args(C.CORTEX_TREE_RNN, H, N, _cpu(10 * H, f32), 11, idx, None,
+                           {"W": _cpu(2 * H * H, f32), "b": _cpu(H, f32)}, _cpu(N * H, f32), None, None, None)
+    # an N-ary U holding one child's gates only
+    with pytest.raises(ValueError, match="U holds"):
+        C._check_tree_args(C.CORTEX_NARY_TREELSTM, H, N, _cpu(10 * H, f32), 10, idx, None,
+                           {"U": _cpu(5 * H * H, f32), "b": _cpu(5 * H, f32)}, _cpu(N * H, f32),
+                           _cpu(N * H, f32), None, None)
+    # MV-RNN: P must hold N matrices
+    with pytest.raises(ValueError, match="P holds"):
+        C._check_tree_args(C.CORTEX_MVRNN, H, N, _cpu(10 * H, f32), 10, idx, _cpu(10 * H * H, f32),
+                           {"W": _cpu(2 * H * H, f32), "W_M": _cpu(2 * H * H, f32)}, _cpu(N * H, f32),
+                           _cpu(N * H, f32), None, None)
+    # all sizes right: the first complaint is that the memory is on the host
+    with pytest.raises(ValueError, match="x_table must be in device memory"):
+        C._check_tree_args(C.CORTEX_TREE_RNN, H, N, _cpu(10 * H, f32), 10, idx, None,
+                           {"W": _cpu(2 * H * H, f32), "b": _cpu(H, f32)}, _cpu(N * H, f32), None,
+                           _cpu(1, torch.int32), _cpu(256, torch.uint8))

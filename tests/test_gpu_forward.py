@@ -46,7 +46,27 @@ def test_workload_parity(k, j):
     announce("forward workload %d seed %d (%s N=%d)" % (k, j, wl.name, wl.N))
     dw = run(wl)
     compare_lin(dw.lin_host(), cached_oracle_lin(k, j), wl.K)
-    compare_states(dw.states_by_node(), cached_oracle(k, j), wl.name)
+    got, ref = dw.states_by_node(), cached_oracle(k, j)
+    if wl.cell == I.CELL_MVRNN:
+        report_mvrnn_depth(got, ref, cached_oracle_lin(k, j), wl.name)
+    compare_states(got, ref, wl.name)
+
+
+def report_mvrnn_depth(got, ref, lin, label):
+    """Per-level max |P| and the level's max error relative to it, for P and
+    p (ungraded).  The matrix state shrinks about 0.65x per level at
+    W_M ~ U(+-0.1), so the absolute bound alone says little about the deep
+    levels; this prints how the relative error behaves there."""
+    height = lin["height"]
+    print("[mvrnn-depth] %s: level, nodes, max|P|, max|dP|/max|P|, max|p|, max|dp|/max|p|" % label)
+    for lvl in range(int(lin["num_levels"])):
+        sel = height == lvl
+        P_ref, P_got = ref["P"][sel], got["P"][sel]
+        p_ref, p_got = ref["h"][sel], got["h"][sel]
+        relP = float(np.abs(P_got - P_ref).max()) / max(float(np.abs(P_ref).max()), 1e-300)
+        relp = float(np.abs(p_got - p_ref).max()) / max(float(np.abs(p_ref).max()), 1e-300)
+        print("[mvrnn-depth] %2d %4d %.3e %.3e %.3e %.3e" % (lvl, int(sel.sum()), float(np.abs(P_ref).max()), relP,
+                                                           float(np.abs(p_ref).max()), relp), flush=True)
 
 
 SMALL = {
@@ -276,6 +296,18 @@ def test_tree_rnn_h64_lds_limit(n_leaves, unroll):
         C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL, 0)
 
 
+_ORACLE_MEMO = {}
+
+
+def _oracle_of(name, wl):
+    """fp64 oracle states of a schedule test's workload (computed once per
+    case name and workload: the parametrized modes share it)."""
+    key = (name, wl.name, wl.N)
+    if key not in _ORACLE_MEMO:
+        _ORACLE_MEMO[key] = O.forward_workload(wl)
+    return _ORACLE_MEMO[key]
+
+
 LEVEL_SYNC_CASES = {
     "treegru": (lambda: I.childsum_treegru_workload(44, batch=4, H=256), 0),
     "nary": (lambda: cached_workload(1, 0), 0),
@@ -306,6 +338,9 @@ def test_level_sync_modes_change_only_the_schedule(name, mode):
             dw.forward()
         return
     got = run(wl).states_by_node()
+    oracle = _oracle_of(name, wl)
+    compare_states(ref, oracle, "%s default" % name)
+    compare_states(got, oracle, "%s level sync %d" % (name, mode))
     for key in ref:
         assert np.array_equal(ref[key], got[key]), key
 
@@ -340,9 +375,12 @@ def test_ablations_change_only_the_schedule(name, bits):
             dw.forward()
         assert dw.status_code() == 0
         return
+    oracle = _oracle_of(name, wl)
+    compare_states(ref, oracle, "%s default" % name)
     for sync in (0, 2):
         C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, sync)
         got = run(wl).states_by_node()
+        compare_states(got, oracle, "%s ablate %d level sync %d" % (name, bits, sync))
         for key in ref:
             assert np.array_equal(ref[key], got[key]), (key, sync)
 
@@ -393,6 +431,9 @@ def test_treegru_phase_barrier_mode(name):
     ref = run(wl).states_by_node()
     C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, 3)
     got = run(wl).states_by_node()
+    oracle = _oracle_of(name, wl)
+    compare_states(ref, oracle, "%s default" % name)
+    compare_states(got, oracle, "%s phase barrier" % name)
     for key in ref:
         assert np.array_equal(ref[key], got[key]), key
 

@@ -20,7 +20,9 @@ def test_probe_mfma():
     assert C.cortex_probe_mfma(sink, 10) == C.CORTEX_OK
     torch.cuda.synchronize()
     assert bool(torch.isfinite(sink).all())
-    assert C.cortex_probe_mfma(None, 10) == C.CORTEX_E_INVAL
+    assert C.load().cortex_probe_mfma(None, 10, None) == C.CORTEX_E_INVAL
+    with pytest.raises(ValueError, match="sink"):
+        C.cortex_probe_mfma(None, 10)
     assert C.cortex_probe_mfma(sink, -1) == C.CORTEX_E_INVAL
 
 

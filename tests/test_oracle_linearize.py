@@ -95,8 +95,8 @@ def test_full_grid_workload_closed_form():
 
 
 def _paper_rows(children, K):
-    leaf_batch, internal = O.paper_linearize_trees(children, K)
-    return leaf_batch + [v for b in internal for v in b], [len(leaf_batch)] + [len(b) for b in internal]
+    batches = O.dfs_batches(children, K)
+    return [v for b in batches for v in b], [len(b) for b in batches]
 
 
 @pytest.mark.parametrize("k", [0, 1, 2, 3])
