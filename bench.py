@@ -6,16 +6,21 @@ cortex_tree_infer / cortex_dag_infer call on one stream (a single launch where
 the cell and batch have a fused instance) with the inputs already resident in
 HBM.
 
-Default workload: binary N-ary TreeLSTM, hidden 256, a batch of 10 random
-binary trees with 10-40 leaves each (seeded synthetic stand-in for the SST
-trees of the paper's TreeLSTM evaluation).
+Default workload: DAG-RNN, hidden 256, a batch of 64 image grids of 32 x 32
+nodes (65,536 nodes, 63 anti-diagonal levels), the largest configuration; the
+other four (TreeRNN H = 64 on one 32-leaf tree; binary N-ary TreeLSTM,
+child-sum TreeLSTM and MV-RNN on batches of 10 random trees) are measured in
+the same run under ``per_config``.
 
 Prints ONE JSON line with the contract fields plus:
   roofline      the step's dominant kernel's achieved algorithmic FLOP/s (or
                 GB/s) from its own HIP-event-timed launches, against the MI355X
                 nominal peak and against the rate measured on the GPU itself
-  cpu_baseline  the fp64 oracle timed on this host's cores over a bounded sample
+  cpu_baseline  the fp64 oracle on one host core: N over the median of 20
+                passes (3 for the 65,536-node batch)
   breakdown     latency percentiles and the linearize / forward split
+                (medians of single launches, averages of back-to-back ones)
+  per_config    the same figures, condensed, for every other configuration
 """
 from __future__ import annotations
 
@@ -190,28 +195,37 @@ def level_floor(stream, grid, levels):
             "note": "empty persistent launch + (levels - 1) x an empty level, 512-thread workgroups"}
 
 
-def cpu_baseline(wl, seconds):
-    """The fp64 oracle (linearize + recursive forward) on a bounded sample."""
+def cpu_baseline(wl, runs):
+    """The fp64 oracle (definitional linearization + recursive forward) timed
+    pass by pass on one host thread; the value is N over the median pass."""
     from oracle import cortex_oracle as O
     try:
         from threadpoolctl import threadpool_limits
         limiter = threadpool_limits(limits=1)
     except Exception:          # threadpoolctl missing: BLAS may use more threads
         limiter = None
-    runs = 0
-    t0 = time.perf_counter()
-    while True:
+    lin_s, fwd_s = [], []
+    for _ in range(runs):
+        t0 = time.perf_counter()
         O.linearize(wl.children, wl.K)
+        t1 = time.perf_counter()
         O.forward_workload(wl)
-        runs += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
+        t2 = time.perf_counter()
+        lin_s.append(t1 - t0)
+        fwd_s.append(t2 - t1)
     if limiter is not None:
         limiter.unregister()
-    return {"value": wl.N * runs / el, "unit": "nodes/s", "cores": 1, "kind": "oracle",
-            "sample": "%d full passes of the %d-node batch (linearize + forward, fp64, 1 thread) in %.1f s"
-                      % (runs, wl.N, el)}
+    total = [a + b for a, b in zip(lin_s, fwd_s)]
+    med = float(np.median(total))
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = os.cpu_count()
+    return {"value": wl.N / med, "unit": "nodes/s", "cores": 1, "kind": "oracle",
+            "sample": "median of %d full passes over the %d-node batch (linearize + forward, fp64, 1 thread "
+                      "of %s usable cores); %.1f s in all" % (runs, wl.N, affinity, sum(total)),
+            "median_pass_s": med, "median_linearize_s": float(np.median(lin_s)),
+            "median_forward_s": float(np.median(fwd_s))}
 
 
 # Cortex's own latencies on the paper's V100 GPU, in ms (the GPU rows of the
@@ -440,9 +454,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", type=int, default=1, help="0..4: tree_rnn, nary, childsum, mvrnn, dag")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--workload", type=int, default=4,
+                    help="headline configuration 0..4: tree_rnn, nary, childsum, mvrnn, dag (default: the "
+                         "64-grid DAG-RNN batch, the largest)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="measure the headline configuration only (no per_config entries)")
     ap.add_argument("--node-groups", type=int, default=0)
     ap.add_argument("--slice-units", type=int, default=0, help="hidden units per forward slice (0 = default)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -489,12 +506,53 @@ def main():
     if args.unroll:
         unroll_study(args)
         return
-    wl = I.make_workload(args.workload)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, args.node_groups)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, args.slice_units)
-    dw = DeviceWorkload(wl)
     stream = torch.cuda.current_stream()
+    peaks = measured_peaks(stream)
+    wl = I.make_workload(args.workload)
+    head = measure(wl, args, stream, peaks, full=True)
+    others = []
+    if not args.no_other_configs:
+        for k in range(len(I.WORKLOADS)):
+            if k != args.workload:
+                others.append(measure(I.make_workload(k), args, stream, peaks, full=False))
 
+    out = {
+        "metric": METRIC,
+        "value": head["nodes_per_s"],
+        "unit": "nodes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded)",
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "cpu_baseline": head["cpu_baseline"],
+        "level_floor": head["level_floor"],
+        "breakdown": head["breakdown"],
+        "per_config": others,
+    }
+    print(json.dumps(out))
+
+
+def measure(wl, args, stream, peaks, full):
+    """One configuration: K steps between two events (value = N / ms_per_step),
+    per-step latencies, the step's launches and the two separate calls timed
+    launch by launch (medians) and back to back (averages, as a kernel trace
+    reports them), the dominant kernel's roofline fraction and the oracle on
+    one host core.  full=False keeps the fields a per-configuration summary
+    needs."""
+    import torch
+    from paper_2011_01383_amd import cortex as C
+    from paper_2011_01383_amd.runner import DeviceWorkload
+
+    dw = DeviceWorkload(wl)
     for _ in range(args.warmup):
         dw.step()
     torch.cuda.synchronize()
@@ -508,7 +566,7 @@ def main():
     g0 = torch.cuda.Event(enable_timing=True)
     g1 = torch.cuda.Event(enable_timing=True)
     g0.record(stream)
-    for i in range(args.steps):
+    for _ in range(args.steps):
         dw.step()
     g1.record(stream)
     torch.cuda.synchronize()
@@ -517,21 +575,20 @@ def main():
     assert dw.status_code() == 0
     ms_per_step = total_ms / args.steps
 
-    # ---- latency distribution: a separate pass with an event pair around
-    #      every step (includes the events' own cost) ----
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
-        dw.step()
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
-    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    def per_launch_ms(fn, n):
+        """n calls, each between its own event pair (includes the events' cost)."""
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        fn()
+        torch.cuda.synchronize()
+        for a, b in ev:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in ev])
 
-    # ---- per-kernel timing: n launches back to back between two HIP events
-    #      on the launch stream (average launch duration, as a kernel trace
-    #      reports it), plus single-launch samples for percentiles ----
-    def time_back_to_back(fn, n):
+    def back_to_back_ms(fn, n):
+        """Average duration of n calls between two events on the launch stream."""
         for _ in range(5):            # host-side first-call work stays out of the average
             fn()
         a = torch.cuda.Event(enable_timing=True)
@@ -544,89 +601,89 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / n
 
+    step_ms = per_launch_ms(dw.step, args.steps)
     n_k = max(20, min(args.steps, 200))
     # the step's own launch(es): one cortex_tree_infer / cortex_dag_infer
     # call, a single fused kernel where the cell and batch have one (the
     # linearizer grid is then reported as 0); the two-call components are
     # timed beside it
-    step_avg_ms = time_back_to_back(dw.step, n_k)
+    step_avg_ms = back_to_back_ms(dw.step, n_k)
     grid_lin, grid_fwd = C.cortex_last_grid(0), C.cortex_last_grid(1)
     fused = grid_lin == 0
-    lin_avg_ms = time_back_to_back(dw.linearize, n_k)
-    fwd_avg_ms = time_back_to_back(dw.forward, n_k)
+    lin_avg_ms = back_to_back_ms(dw.linearize, n_k)
+    fwd_avg_ms = back_to_back_ms(dw.forward, n_k)
+    lin_ms = per_launch_ms(dw.linearize, n_k)
+    fwd_ms = per_launch_ms(dw.forward, n_k)
     assert dw.status_code() == 0
 
     flops, byts = algorithmic_work(wl)
     bound = bound_of(flops, byts)
     kern_ms = step_avg_ms if fused else fwd_avg_ms
-    fwd_avg_s = kern_ms / 1e3
-    if bound == "mfma":
-        achieved = flops / fwd_avg_s / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None}
-    else:
-        achieved = byts / fwd_avg_s / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": achieved / PEAK_HBM_GBS, "traffic": None}
-    peaks = measured_peaks(stream)
-    roof["peak_measured"] = peaks["fp32_mfma_tflops"] if bound == "mfma" else peaks["hbm_copy_gbs"]
-    roof["frac_of_measured"] = achieved / roof["peak_measured"]
-    roof["peak_measured_note"] = peaks["note"]
-    roof["traffic"] = measured_traffic(wl)
-    roof["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
-    roof["kernel"] = ("linearize + forward in one launch (%s)" if fused else "forward (%s)") % wl.cell
-    roof["kernel_avg_ms"] = kern_ms
-    roof["algorithmic_flops"] = flops
-    roof["algorithmic_bytes"] = byts
 
     def frac_at(ms):
         if bound == "mfma":
             return flops / (ms / 1e3) / 1e12 / PEAK_FP32_TFLOPS
         return byts / (ms / 1e3) / 1e9 / PEAK_HBM_GBS
 
-    lin_host = dw.lin_host()
-    floor = level_floor(stream, grid_fwd, int(lin_host["num_levels"]))
+    if bound == "mfma":
+        achieved = flops / (kern_ms / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_FP32_TFLOPS}
+        roof["peak_measured"] = peaks["fp32_mfma_tflops"]
+    else:
+        achieved = byts / (kern_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+        roof["peak_measured"] = peaks["hbm_copy_gbs"]
+    roof["traffic"] = measured_traffic(wl)
+    roof["frac_of_measured"] = achieved / roof["peak_measured"]
+    roof["peak_measured_note"] = peaks["note"]
+    roof["traffic_unit"] = "bytes per launch"
+    roof["traffic_source"] = ("profiles/hbm_counters_%s.md: rocprofv3 FETCH_SIZE and WRITE_SIZE passes, each scaled "
+                              "by its reading on a plain copy; used only while the forward sources hash as they did "
+                              "when the counters were taken (null otherwise)" % wl.name)
+    roof["kernel"] = ("linearize + forward in one launch (%s)" if fused else "forward (%s)") % wl.cell
+    roof["kernel_avg_ms"] = kern_ms
+    roof["algorithmic_flops"] = flops
+    roof["algorithmic_bytes"] = byts
 
+    lin_host = dw.lin_host()
+    levels = int(lin_host["num_levels"])
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, args.cpu_seconds)
-
-    out = {
-        "metric": METRIC,
-        "value": wl.N / (ms_per_step / 1e3),
-        "unit": "nodes/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic (seeded)",
-        "config": {"workload": wl.name, "cell": wl.cell, "hidden": wl.H, "nodes": wl.N,
-                   "levels": int(lin_host["num_levels"]), "max_arity": wl.K,
-                   "grid_linearize": grid_lin, "grid_forward": grid_fwd, "one_launch": fused},
-        "roofline": roof,
-        "cpu_baseline": cpu,
-        "level_floor": floor,
-        "breakdown": {
-            "latency_note": "percentiles from a second pass with an event pair around each step",
-            "latency_ms_p10": float(np.percentile(step_ms, 10)),
-            "latency_ms_p50": float(np.percentile(step_ms, 50)),
-            "latency_ms_p90": float(np.percentile(step_ms, 90)),
-            "step_launches_avg_ms": step_avg_ms,
-            "two_calls_note": "cortex_linearize and cortex_tree_forward / cortex_dag_forward timed on their own",
-            "linearize_kernel_avg_ms": lin_avg_ms,
-            "forward_kernel_avg_ms": fwd_avg_ms,
-            "roofline_frac_forward_only": frac_at(fwd_avg_ms),
-            "roofline_frac_end_to_end": frac_at(ms_per_step),
-            "measured_fp32_mfma_tflops": peaks["fp32_mfma_tflops"],
-            "measured_hbm_copy_gbs": peaks["hbm_copy_gbs"],
-            "host_wall_s": wall,
-        },
+        cpu = cpu_baseline(wl, 3 if wl.N > 20000 else 20)
+    config = {"workload": wl.name, "cell": wl.cell, "hidden": wl.H, "nodes": wl.N, "levels": levels,
+              "max_arity": wl.K, "grid_linearize": grid_lin, "grid_forward": grid_fwd, "one_launch": fused}
+    res = {"config": config, "ms_per_step": ms_per_step, "nodes_per_s": wl.N / (ms_per_step / 1e3),
+           "latency_ms_p50": float(np.percentile(step_ms, 50)), "roofline": roof, "cpu_baseline": cpu}
+    if not full:
+        res["roofline"] = {k: roof[k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic", "kernel",
+                                                "kernel_avg_ms")}
+        res["linearize_ms_median"] = float(np.median(lin_ms))
+        res["forward_ms_median"] = float(np.median(fwd_ms))
+        return res
+    res["level_floor"] = level_floor(stream, grid_fwd, levels)
+    res["breakdown"] = {
+        "latency_note": "percentiles from a second pass with an event pair around each step (includes the "
+                        "events' own cost)",
+        "latency_ms_p10": float(np.percentile(step_ms, 10)),
+        "latency_ms_p50": float(np.percentile(step_ms, 50)),
+        "latency_ms_p90": float(np.percentile(step_ms, 90)),
+        "nodes_per_s_at_p50": wl.N / (float(np.percentile(step_ms, 50)) / 1e3),
+        "step_launches_avg_ms": step_avg_ms,
+        "two_calls_note": "cortex_linearize and cortex_tree_forward / cortex_dag_forward on their own: medians "
+                          "of launches each between its own event pair, and averages of back-to-back launches",
+        "linearize_ms_median": float(np.median(lin_ms)),
+        "forward_ms_median": float(np.median(fwd_ms)),
+        "linearize_kernel_avg_ms": lin_avg_ms,
+        "forward_kernel_avg_ms": fwd_avg_ms,
+        "roofline_frac_forward_only": frac_at(fwd_avg_ms),
+        "roofline_frac_end_to_end": frac_at(ms_per_step),
+        "measured_fp32_mfma_tflops": peaks["fp32_mfma_tflops"],
+        "measured_hbm_copy_gbs": peaks["hbm_copy_gbs"],
+        "host_wall_s": wall,
     }
-    print(json.dumps(out))
+    return res
 
 
 if __name__ == "__main__":

@@ -82,6 +82,7 @@ extern "C" {
 #define CORTEX_ST_BARRIER_TIMEOUT 3  /* a barrier or per-datum wait passed its limit */
 #define CORTEX_ST_BAD_LINEARIZATION 4 /* forward was handed an inconsistent linearization */
 #define CORTEX_ST_INPUT_RANGE 5      /* an input index outside [-1, rows of the input table) */
+#define CORTEX_ST_EPOCH_WRAP 6       /* the forward workspace has served 2^32 - 1 launches: zero it */
 
 /* Cells (Sec. 7.1, Table "Models and datasets"). */
 #define CORTEX_TREE_RNN 0            /* h = tanh(W [h_l; h_r] + b); leaf h = x */
@@ -251,7 +252,7 @@ int cortex_dag_infer(int32_t H, const int32_t *d_children, const cortex_lin_t *l
  *                                   H = 64, takes one group per 16 nodes, at
  *                                   most one per compute unit)
  *   CORTEX_KNOB_BARRIER_TIMEOUT_US  spin limit of one barrier or per-datum wait in
- *                                   microseconds (default 5,000,000; 0 makes every
+ *                                   microseconds (default 200,000: 0.2 s; 0 makes every
  *                                   wait time out at once, for tests of that path)
  *   CORTEX_KNOB_COOPERATIVE         1 = always use the cooperative launch
  *                                   (0 = only when the grid exceeds one

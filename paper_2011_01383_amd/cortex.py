@@ -30,6 +30,7 @@ CORTEX_ST_CYCLE = 2
 CORTEX_ST_BARRIER_TIMEOUT = 3
 CORTEX_ST_BAD_LINEARIZATION = 4
 CORTEX_ST_INPUT_RANGE = 5
+CORTEX_ST_EPOCH_WRAP = 6
 
 CORTEX_TREE_RNN = 0
 CORTEX_NARY_TREELSTM = 1

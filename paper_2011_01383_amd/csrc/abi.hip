@@ -9,7 +9,12 @@
 namespace cortex {
 
 constexpr int kKnobs = 8;
-static std::atomic<int64_t> g_knobs[kKnobs] = {{0}, {0}, {5000000}, {0}, {0}, {0}, {0}, {0}};
+// The default spin limit of one wait, 0.2 s, is about 10^4 times the longest
+// level or linearizer phase measured on the largest batch here (tens of
+// microseconds): a wait that long means the grid is not co-resident (a GPU
+// shared with other persistent work), and the launch then ends with a status
+// instead of holding the GPU.
+static std::atomic<int64_t> g_knobs[kKnobs] = {{0}, {0}, {200000}, {0}, {0}, {0}, {0}, {0}};
 static std::atomic<int32_t> g_last_grid[2] = {{0}, {0}};
 
 int64_t knob(int32_t which) {

@@ -12,26 +12,33 @@ namespace cortex {
 
 // ---------------------------------------------------------------------------
 // Workspace header of a persistent launch.
-//   line 0            the barrier generation (written by workgroup 0 only)
+//   line 0, word 0    the barrier generation (written by workgroup 0 only)
+//   line 0, word 16   the staging epoch: the tag of the last forward launch on
+//                     this workspace that ended normally (see launch tags below)
 //   arrive[kMaxGrid]  one arrival word per workgroup (written by its owner only)
 //   slot[2][kMaxGrid] per-workgroup values a kernel exchanges between barriers,
 //                     double-buffered by round parity (x2 for two values)
+//   entered[kMaxGrid] the tag each workgroup of the current forward launch read
 // Nothing here needs resetting between launches: barrier epochs are derived
 // from the generation, which only grows, so old arrival words never match a
 // future epoch.  After a launch that ends with a non-zero status the caller
-// must zero the workspace again (the abort can leave arrival words ahead).
+// must zero the workspace again (the abort can leave arrival words ahead, and
+// the staging epoch is not advanced).
 // ---------------------------------------------------------------------------
 constexpr int kMaxGrid = 4096;
-constexpr size_t kSyncBytes = 128 + sizeof(unsigned int) * (size_t)kMaxGrid * (1 + 4);
+constexpr int kEpochWord = 16;
+constexpr size_t kSyncBytes = 128 + sizeof(unsigned int) * (size_t)kMaxGrid * (1 + 4 + 1);
 
 struct SyncWords {
   unsigned int *base;
   __device__ unsigned int *gen() const { return base; }
+  __device__ unsigned int *epoch() const { return base + kEpochWord; }
   __device__ unsigned int *arrive(int b) const { return base + 32 + b; }
   // value v (0 or 1) of round parity p for workgroup b
   __device__ unsigned int *slot(int v, int p, int b) const {
     return base + 32 + kMaxGrid + ((v * 2 + p) * kMaxGrid) + b;
   }
+  __device__ unsigned int *entered(int b) const { return base + 32 + 5 * kMaxGrid + b; }
 };
 
 __device__ __forceinline__ int load_status(const int32_t *status) {
@@ -123,6 +130,61 @@ struct TagBuf {
     __builtin_amdgcn_raw_buffer_store_b64(w, r, e * 8u, 0, kScopeDevice);
   }
 };
+
+// ---------------------------------------------------------------------------
+// Launch tags.  A pair in the staging is this launch's value only if no
+// earlier launch on the same workspace wrote that tag, so tags come from the
+// workspace itself, not from the host: every workgroup reads the staging
+// epoch E at entry and uses tag = E + 1 (all workgroups read the same E:
+// nothing changes it during the launch), and records that tag in its entered
+// word.  At its normal exit workgroup 0 waits until every workgroup of the
+// launch has entered, then stores E + 1 as the new epoch, which the next
+// launch on the stream reads.  Launches enqueued by different copies of the
+// library, or by different processes, on one workspace therefore never reuse
+// a tag, as long as they are ordered (the ABI already forbids overlapping
+// calls on one workspace).  A zeroed workspace has E = 0 and holds tag 0
+// only, which no launch uses; a workspace whose epoch reached 0xFFFFFFFF has
+// no tag left and reports CORTEX_ST_EPOCH_WRAP (zero it to continue).  A
+// launch that ends with an error does not advance the epoch; the ABI asks for
+// the workspace to be zeroed then.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t launch_tag(const unsigned int *sync) {
+  return ld_agent(SyncWords{(unsigned int *)sync}.epoch()) + 1u;
+}
+
+// After the entry loads: false (and CORTEX_ST_EPOCH_WRAP) when the epoch has
+// no tag left; otherwise thread 0 records the workgroup's tag.
+__device__ __forceinline__ bool mark_entered(unsigned int *sync, uint32_t tag, int32_t *status) {
+  if (tag == 0u) {
+    if (threadIdx.x == 0) raise_status(status, CORTEX_ST_EPOCH_WRAP);
+    return false;
+  }
+  if (threadIdx.x == 0) st_agent(SyncWords{sync}.entered(blockIdx.x), tag);
+  return true;
+}
+
+// At the normal end of a launch that retires its tag, reached by every
+// thread of every workgroup: workgroup 0 waits (bounded) for every
+// workgroup's entered word, then publishes the tag as the epoch.  Nothing is
+// published after an error anywhere in the launch.
+__device__ __forceinline__ void retire_tag(unsigned int *sync, uint32_t tag, int32_t *status, uint64_t timeout_ticks) {
+  if (blockIdx.x != 0) return;
+  const SyncWords sw{sync};
+  int ok = 1;
+  for (int b = (int)threadIdx.x; b < (int)gridDim.x && ok; b += (int)blockDim.x) {
+    const uint64_t t0 = wall_clock64();
+    while (ld_agent(sw.entered(b)) != tag) {
+      if (load_status(status) != 0) { ok = 0; break; }
+      if (wall_clock64() - t0 > timeout_ticks) {
+        raise_status(status, CORTEX_ST_BARRIER_TIMEOUT);
+        ok = 0;
+        break;
+      }
+    }
+  }
+  ok = __syncthreads_and(ok);
+  if (ok && threadIdx.x == 0 && load_status(status) == 0) st_agent(sw.epoch(), tag);
+}
 
 // Read-only input rows (embedding tables, DAG inputs) through the ordinary
 // cache hierarchy; out-of-range offsets read zeros.  Offsets are bytes.

@@ -85,7 +85,8 @@ struct FwdArgs {
   unsigned int *sync;
   uint64_t timeout;
   uint64_t *trace;
-  uint32_t tag;                 // this launch's staging tag
+  int32_t retire;               // 1: publish this launch's tag as the workspace's staging epoch at the end
+                                // (0 for all but the last of a sequence of per-level launches)
   void *hs, *cs;                // tagged staging of h and c (workspace)
   int32_t level_lo, level_hi;   // levels this launch runs (all of them unless one launch per level)
   int32_t level_barrier;        // 1: a device-wide barrier closes every level (instead of per-datum waits alone);
@@ -789,7 +790,7 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
   const int slice = blockIdx.x % a.S, group = blockIdx.x / a.S, Q = a.Q;
   const int hbase = slice * J;
   const int N = a.N;
-  const uint32_t tag = a.tag;
+  const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
   const TagBuf hs(a.hs, (uint32_t)N * H * 8);
   const TagBuf cs(a.cs, kLstm ? (uint32_t)N * H * 8 : 0u);
   // plain operand rows: the input table (leaf children) or the DAG inputs
@@ -832,6 +833,7 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
     if (!setup_sources<CELL, kCached>(a, pf, cache, L, off, codes, xrow)) return;
   }
   CORTEX_TRACE_KERNEL(2);
+  if (!mark_entered(a.sync, tag, a.status)) return;
   const int off1 = off[1];
   int gave_up = 0;
 
@@ -1088,6 +1090,7 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
     if (a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
   }
   CORTEX_TRACE_KERNEL(3);
+  if (a.retire) retire_tag(a.sync, tag, a.status, a.timeout);
 }
 
 // ---------------------------------------------------------------------------
@@ -1277,7 +1280,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   const int Q = a.Q;
   const int hbase = slice * J;
   const int N = a.N;
-  const uint32_t tag = a.tag;
+  const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
   const TagBuf hs(a.hs, (uint32_t)N * H * 8);
   const InBuf xin(a.x, (uint32_t)N * H * 4);
   const int rslot = wave >> 2;                 // child slot of this wave's recurrent columns
@@ -1396,6 +1399,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     }
   }
   CORTEX_TRACE_KERNEL(2);
+  if (!mark_entered(a.sync, tag, a.status)) return;
   int gave_up = 0;
 
   struct Ops {
@@ -1556,6 +1560,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     }
   }
   CORTEX_TRACE_KERNEL(3);
+  if (a.retire) retire_tag(a.sync, tag, a.status, a.timeout);
 }
 
 // ---------------------------------------------------------------------------
@@ -1593,7 +1598,7 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
   const int slice = blockIdx.x % a.S, group = blockIdx.x / a.S, Q = a.Q;
   const int hbase = slice * J;
   const int N = a.N, K = a.K;
-  const uint32_t tag = a.tag;
+  const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
   const TagBuf hs(a.hs, (uint32_t)N * H * 8);
   const TagBuf cs(a.cs, (uint32_t)N * H * 8);
   const InBuf xin(a.x_table, (uint32_t)a.x_rows * H * 4);
@@ -1623,6 +1628,7 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
     if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
   }
   CORTEX_TRACE_KERNEL(2);
+  if (!mark_entered(a.sync, tag, a.status)) return;
   int gave_up = 0;
 
   struct TileOps {
@@ -1905,6 +1911,7 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
     if (a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
   }
   CORTEX_TRACE_KERNEL(3);
+  if (a.retire) retire_tag(a.sync, tag, a.status, a.timeout);
 }
 
 // ---------------------------------------------------------------------------
@@ -2212,7 +2219,7 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
   const int slice = blockIdx.x % a.S, group = blockIdx.x / a.S, Q = a.Q;
   const int hbase = slice * J;
   const int N = a.N, K = a.K;
-  const uint32_t tag = a.tag;
+  const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
   const TagBuf hs(a.hs, (uint32_t)N * H * 8);
   const TagBuf ms(a.cs, (uint32_t)N * H * 8);
   const InBuf xin(a.x_table, (uint32_t)a.x_rows * H * 4);
@@ -2258,6 +2265,7 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
     if (!setup_structure<kCached, true, false>(a, cache, st, L)) return;
   }
   CORTEX_TRACE_KERNEL(2);
+  if (!mark_entered(a.sync, tag, a.status)) return;
   int gave_up = 0;
 
   // ---- level 0: leaves (m = 0, h~ = 0): h = (1 - z) tanh(W_h x + b_h) ----
@@ -2586,6 +2594,7 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
     if (a.level_barrier && !grid_sync<false>(SyncWords{a.sync}, a.status, a.timeout)) return;
   }
   CORTEX_TRACE_KERNEL(3);
+  if (a.retire) retire_tag(a.sync, tag, a.status, a.timeout);
 }
 
 // Validated level bounds; false (and a status) when the linearization is broken.
@@ -2658,7 +2667,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
   const int rblk = blockIdx.x % RB, ngroup = blockIdx.x / RB, ngroups = gridDim.x / RB;
   const int N = a.N;
   const bool cached = kFused || N <= M::kCacheRows;
-  const uint32_t tag = a.tag;
+  const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
   const TagBuf hs(a.hs, (uint32_t)N * D * 8);
   const TagBuf ps(a.cs, (uint32_t)N * D * D * 8);
   const InBuf xv(a.x_table, a.x_table ? (uint32_t)a.x_rows * D * 4 : 0u);
@@ -2733,6 +2742,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
     return;
   }
+  if (!mark_entered(a.sync, tag, a.status)) return;
   int r0, r1;
   auto bounds = [&](int l) -> bool {
     if constexpr (kFused) {
@@ -2918,6 +2928,7 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
       __syncthreads();
     }
   }
+  if (a.retire) retire_tag(a.sync, tag, a.status, a.timeout);
 }
 
 // ---------------------------------------------------------------------------
@@ -3145,15 +3156,6 @@ static size_t second_staging_bytes(int32_t cell, int32_t N, int32_t H) {
   if (cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) return staging_bytes(N, H) + keep_bytes(N, H);
   return staging_bytes(N, H);
 }
-static std::atomic<uint32_t> g_tag{0};
-
-// A tag no earlier launch used (0 never: a zeroed workspace holds tag 0).
-static uint32_t next_tag() {
-  uint32_t t = g_tag.fetch_add(1) + 1;
-  if (t == 0) t = g_tag.fetch_add(1) + 1;
-  return t;
-}
-
 // fused_children != nullptr: the fused instance, which linearizes the batch
 // itself and writes *lin; where there is none, or it does not fit one compute
 // unit, nothing is enqueued and *launched stays false.
@@ -3215,7 +3217,7 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   a.hs = staged >= 1 ? stage : nullptr;
   a.cs = staged >= 2 ? stage + staging_bytes(lin->num_nodes, H) : nullptr;   // c, or P for MV-RNN
   a.keep = inst.phase_barrier_ok ? (float *)(stage + 2 * staging_bytes(lin->num_nodes, H)) : nullptr;
-  a.tag = next_tag();
+  a.retire = 1;                 // the tag itself comes from the workspace header (launch_tag)
   a.level_lo = 0;
   a.level_hi = 0x7fffffff;
   a.level_barrier = 0;
@@ -3242,8 +3244,9 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   }
   if (sync_mode != 2) return launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
   // one launch per level (ablation): L is read back first; every launch
-  // reloads weights and structure and keeps the launch tag, so a level
-  // reads what the previous launches staged
+  // reloads weights and structure and reads the same staging epoch (only the
+  // last one advances it), so all use one tag and a level reads what the
+  // previous launches staged
   int32_t L = 0;
   if (hipMemcpyAsync(&L, lin->num_levels, sizeof(L), hipMemcpyDeviceToHost, (hipStream_t)stream) != hipSuccess ||
       hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
@@ -3252,6 +3255,7 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   for (int32_t l = 0; l < L; ++l) {
     a.level_lo = l;
     a.level_hi = l + 1;
+    a.retire = l == L - 1;
     const int rc = launch_persistent(inst.fn, (int)G, inst.threads, dyn, a, stream);
     if (rc != CORTEX_OK) return rc;
   }

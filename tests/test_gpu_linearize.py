@@ -18,7 +18,7 @@ def _gpu():
     need_gpu()
     yield
     C.cortex_set_knob(C.CORTEX_KNOB_LIN_BLOCKS, 0)
-    C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 5000000)
+    C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 200000)
 
 
 def gpu_linearize(children, K, blocks=0):
@@ -176,7 +176,7 @@ def test_forced_barrier_timeout_then_recovery():
         seen.add(st)
     assert seen <= {0, C.CORTEX_ST_BARRIER_TIMEOUT}
     assert C.CORTEX_ST_BARRIER_TIMEOUT in seen
-    C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 5000000)
+    C.cortex_set_knob(C.CORTEX_KNOB_BARRIER_TIMEOUT_US, 200000)
     # after an error the ABI asks for a zeroed workspace; then it is reusable
     lin, status, ws, d_children = keep
     status.zero_()
