@@ -209,6 +209,41 @@ int cortex_tree_infer(int32_t cell, int32_t H, const int32_t *d_children, const 
                       size_t ws_bytes, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * cortex_tree_infer with the workspace taken from a library-owned array in
+ * device memory instead of a caller's buffer.  The caller still passes the
+ * linearization arrays, inputs, weights, outputs and status word, with the
+ * meanings of cortex_tree_infer; the results are bitwise those of
+ * cortex_tree_infer on the same inputs.
+ *   - The array is CORTEX_NOALLOC_SCRATCH_BYTES per GPU, held from the first
+ *     call on that GPU until the process ends.  The call allocates nothing:
+ *     no hipMalloc, no hipFree, no allocating library routine.
+ *   - Size limits (each checked on the host): the linearizer workspace
+ *     (cortex_linearize_workspace_bytes, needed when the batch takes two
+ *     launches) at most 2 MiB; N * H at most 2,097,152 for the h staging;
+ *     the second state's staging (c and the TreeGRU reset sums: N * H; P of
+ *     MV-RNN: N * H * H) at most 4,194,304 elements; the TreeGRU phase values
+ *     (N * H * 3 floats) at most 8 MiB.  A batch beyond them returns
+ *     CORTEX_E_WORKSPACE and enqueues nothing.  Other host errors are those of
+ *     cortex_tree_infer, also with nothing enqueued.
+ *   - Each call enqueues, before the path's own launches, one small kernel
+ *     that prepares the array (it clears its barrier words and advances its
+ *     staging epoch; the first call on a GPU clears the whole array).  So a
+ *     call after one that ended with a non-zero status needs no reset beyond
+ *     setting *d_status back to 0.
+ *   - Every call on a GPU shares that GPU's array, which keeps the last
+ *     call's contents: calls that overlap in time on one GPU (other streams,
+ *     other threads) race and give wrong results.  Order them, e.g. on one
+ *     stream.
+ */
+#define CORTEX_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+int cortex_tree_infer_noalloc(int32_t cell, int32_t H, const int32_t *d_children, const cortex_lin_t *lin,
+                              const float *d_x_table, int32_t x_rows, const int32_t *d_x_index,
+                              const float *d_leaf_mat, const cortex_weights_t *w, float *d_h, float *d_c_or_P,
+                              int32_t *d_status, void *stream);
+
+/*
  * Forward pass of the DAG-RNN cell (recursive part of DAG-RNN, Sec. 7.1):
  *   h(v) = tanh(W x(v) + U_0 h(slot 0) + U_1 h(slot 1) + b)
  * (for image grids slot 0 is the node above, slot 1 the node to the left).

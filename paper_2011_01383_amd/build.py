@@ -30,7 +30,7 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
 ]
-SOURCES = ["abi.hip", "linearize.hip", "forward.hip", "probe.hip"]
+SOURCES = ["abi.hip", "linearize.hip", "forward.hip", "probe.hip", "noalloc.hip"]
 # packed two-lane fp32 arithmetic, which this library must not contain
 PACKED_FP32 = ("v_pk_add_f32", "v_pk_mul_f32", "v_pk_fma_f32")
 LLVM_BIN = "/opt/rocm/llvm/bin"

@@ -55,6 +55,7 @@ CELL_IDS = {"tree_rnn": CORTEX_TREE_RNN, "nary_treelstm": CORTEX_NARY_TREELSTM,
 EXPORTED = [
     "cortex_linearize_workspace_bytes", "cortex_linearize", "cortex_forward_workspace_bytes",
     "cortex_tree_forward", "cortex_dag_forward", "cortex_tree_infer_workspace_bytes", "cortex_tree_infer",
+    "cortex_tree_infer_noalloc",
     "cortex_dag_infer_workspace_bytes", "cortex_dag_infer",
     "cortex_set_knob", "cortex_get_knob",
     "cortex_last_grid", "cortex_version",
@@ -103,6 +104,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cortex_tree_infer.argtypes = [I32, I32, P, ctypes.POINTER(cortex_lin_t), P, I32, P, P,
                                       ctypes.POINTER(cortex_weights_t), P, P, P, P, SZ, P]
     lib.cortex_tree_infer.restype = ctypes.c_int
+    lib.cortex_tree_infer_noalloc.argtypes = [I32, I32, P, ctypes.POINTER(cortex_lin_t), P, I32, P, P,
+                                              ctypes.POINTER(cortex_weights_t), P, P, P, P]
+    lib.cortex_tree_infer_noalloc.restype = ctypes.c_int
     lib.cortex_dag_infer_workspace_bytes.argtypes = [I32, I32, I32]
     lib.cortex_dag_infer_workspace_bytes.restype = SZ
     lib.cortex_dag_infer.argtypes = [I32, P, ctypes.POINTER(cortex_lin_t), P, P, P, P, P, P, P, SZ, P]
@@ -178,6 +182,9 @@ _WEIGHT_ELEMS = {
 }
 
 
+_NO_WS = object()        # the entry point takes no workspace
+
+
 def _check_tree_args(cell: int, H: int, N: int, x_table, x_rows: int, x_index, leaf_mat, weights: dict, h,
                      c_or_P, status, ws) -> None:
     if cell not in _WEIGHT_ELEMS:
@@ -195,7 +202,9 @@ def _check_tree_args(cell: int, H: int, N: int, x_table, x_rows: int, x_index, l
         specs.append((c_or_P, "c", f32, N * H, False))
     elif cell == CORTEX_MVRNN:
         specs.append((c_or_P, "P", f32, N * H * H, False))
-    specs += [(status, "status", i32, 1, False), (ws, "ws", None, 1, False)]
+    specs.append((status, "status", i32, 1, False))
+    if ws is not _NO_WS:
+        specs.append((ws, "ws", None, 1, False))
     _need_all(specs)
 
 
@@ -284,6 +293,21 @@ def cortex_tree_infer(cell: int, H: int, children: torch.Tensor, lin: "Lineariza
     return load().cortex_tree_infer(cell, H, _ptr(children), ctypes.byref(lin.struct), _ptr(x_table), x_rows,
                                     _ptr(x_index), _ptr(leaf_mat), ctypes.byref(w), _ptr(h), _ptr(c_or_P),
                                     _ptr(status), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
+
+
+def cortex_tree_infer_noalloc(cell: int, H: int, children: torch.Tensor, lin: "Linearization",
+                              x_table: Optional[torch.Tensor], x_rows: int, x_index: torch.Tensor,
+                              leaf_mat: Optional[torch.Tensor], W=None, U=None, b=None, W_M=None,
+                              h: torch.Tensor = None, c_or_P: Optional[torch.Tensor] = None,
+                              status: torch.Tensor = None, stream=None) -> int:
+    _check_lin(lin, lin.N, lin.K)
+    _need(children, "children", torch.int32, lin.N * lin.K)
+    _check_tree_args(cell, H, lin.N, x_table, x_rows, x_index, leaf_mat, {"W": W, "U": U, "b": b, "W_M": W_M},
+                     h, c_or_P, status, _NO_WS)
+    w = cortex_weights_t(_ptr(W), _ptr(U), _ptr(b), _ptr(W_M))
+    return load().cortex_tree_infer_noalloc(cell, H, _ptr(children), ctypes.byref(lin.struct), _ptr(x_table), x_rows,
+                                            _ptr(x_index), _ptr(leaf_mat), ctypes.byref(w), _ptr(h), _ptr(c_or_P),
+                                            _ptr(status), _stream(stream))
 
 
 def cortex_dag_infer_workspace_bytes(N: int, K: int, H: int) -> int:

@@ -54,4 +54,25 @@ int launch_persistent(Kernel kernel, int grid, int threads, size_t dyn_lds, cons
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Where a forward launch keeps its workspace header, its tagged staging of h
+// and of the second state, and the TreeGRU phase values.
+struct FwdRegions {
+  void *header;
+  void *hs, *cs;
+  float *keep;
+};
+
+// Internal entry points shared by the C entry points (dry_run: every host
+// check, nothing enqueued).
+int linearize_impl(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin, int32_t *d_status,
+                   void *d_ws, size_t ws_bytes, void *stream, bool dry_run);
+int tree_infer_impl(int32_t cell, int32_t H, const int32_t *d_children, const cortex_lin_t *lin,
+                    const float *d_x_table, int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
+                    const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status, void *lin_ws,
+                    size_t lin_ws_bytes, void *fwd_ws, size_t fwd_ws_bytes, const FwdRegions *fixed, void *stream,
+                    bool dry_run);
+bool fixed_regions(int32_t cell, int32_t N, int32_t H, void *header, size_t header_cap, void *hs, size_t hs_cap,
+                   void *cs, size_t cs_cap, void *keep, size_t keep_cap, FwdRegions &out);
+size_t forward_header_bytes();
+
 }  // namespace cortex

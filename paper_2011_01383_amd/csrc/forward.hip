@@ -3141,6 +3141,7 @@ static bool pick_fused(int cell, int H, int32_t N, int32_t K, Instance &out) {
 static size_t staging_bytes(int32_t N, int32_t H) { return align_up((size_t)N * H * 8, 256); }
 static size_t staging_offset() { return align_up(kSyncBytes + kTraceBytes, 256); }
 size_t trace_offset() { return kSyncBytes; }
+size_t forward_header_bytes() { return staging_offset(); }
 static int staged_tensors(int32_t cell) {
   if (cell == CORTEX_NARY_TREELSTM || cell == CORTEX_CHILDSUM_TREELSTM || cell == CORTEX_MVRNN ||
       cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU)
@@ -3156,18 +3157,47 @@ static size_t second_staging_bytes(int32_t cell, int32_t N, int32_t H) {
   if (cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) return staging_bytes(N, H) + keep_bytes(N, H);
   return staging_bytes(N, H);
 }
+// Where a forward launch keeps its header (barrier words, staging epoch,
+// entered words; then the trace area in trace builds), its tagged staging of
+// h and of the second state (c, P or the TreeGRU reset sums m) and the
+// TreeGRU phase values.  The staging regions must only ever have held tagged
+// pairs written through this header's epoch, so that every tag in them is at
+// most the epoch.
+static size_t regions_bytes(int32_t cell, int32_t N, int32_t H, size_t &hs_off, size_t &cs_off, size_t &keep_off) {
+  const int staged = staged_tensors(cell == CELL_DAG ? -1 : cell);
+  hs_off = staging_offset();
+  cs_off = hs_off + (staged >= 1 ? staging_bytes(N, H) : 0);
+  keep_off = cs_off + (staged >= 2 ? (cell == CORTEX_MVRNN ? align_up((size_t)N * H * H * 8, 256) : staging_bytes(N, H))
+                                   : 0);
+  return cortex_forward_workspace_bytes(cell == CELL_DAG ? -1 : cell, N, H);
+}
+
+// The regions of a caller's workspace: header, h staging, second staging,
+// then the TreeGRU phase values, back to back.
+static FwdRegions workspace_regions(void *d_ws, int32_t cell, int32_t N, int32_t H) {
+  size_t hs_off, cs_off, keep_off;
+  regions_bytes(cell, N, H, hs_off, cs_off, keep_off);
+  char *base = (char *)d_ws;
+  const int staged = staged_tensors(cell == CELL_DAG ? -1 : cell);
+  return FwdRegions{d_ws, staged >= 1 ? base + hs_off : nullptr, staged >= 2 ? base + cs_off : nullptr,
+                    (float *)(base + keep_off)};
+}
+
 // fused_children != nullptr: the fused instance, which linearizes the batch
 // itself and writes *lin; where there is none, or it does not fit one compute
-// unit, nothing is enqueued and *launched stays false.
+// unit, nothing is enqueued and *launched stays false.  fixed != nullptr: the
+// regions come from the caller (ws_bytes is then not checked).
 static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, void *d_ws, size_t ws_bytes,
-                          void *stream, const int32_t *fused_children = nullptr, bool *launched = nullptr) {
+                          void *stream, const int32_t *fused_children = nullptr, bool *launched = nullptr,
+                          const FwdRegions *fixed = nullptr, bool dry_run = false) {
   if (launched) *launched = false;
   // state and staging arrays are addressed with 32-bit byte offsets
   const uint64_t state_bytes = (uint64_t)lin->num_nodes * H * (cell == CORTEX_MVRNN ? H : 1) * 8;
   const uint64_t table_bytes = (uint64_t)(a.x_rows > 0 ? a.x_rows : 0) * H * (cell == CORTEX_MVRNN ? H : 1) * 4;
   if (state_bytes > 0x7fffffffull || table_bytes > 0x7fffffffull) return CORTEX_E_TOO_LARGE;
-  if (ws_bytes < cortex_forward_workspace_bytes(cell == CELL_DAG ? -1 : cell, lin->num_nodes, H))
+  if (!fixed && ws_bytes < cortex_forward_workspace_bytes(cell == CELL_DAG ? -1 : cell, lin->num_nodes, H))
     return CORTEX_E_WORKSPACE;
+  const FwdRegions reg = fixed ? *fixed : workspace_regions(d_ws, cell, lin->num_nodes, H);
   size_t dyn = 0;
   bool cached = false;
   Instance inst;
@@ -3209,14 +3239,12 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   if (G > cap || G > kMaxGrid) return CORTEX_E_TOO_LARGE;
   a.S = S;
   a.Q = (int32_t)q;
-  a.sync = (unsigned int *)d_ws;
-  a.trace = (uint64_t *)((char *)d_ws + kSyncBytes);
+  a.sync = (unsigned int *)reg.header;
+  a.trace = (uint64_t *)((char *)reg.header + kSyncBytes);
   a.timeout = barrier_timeout_ticks();
-  const int staged = staged_tensors(cell == CELL_DAG ? -1 : cell);
-  char *stage = (char *)d_ws + staging_offset();
-  a.hs = staged >= 1 ? stage : nullptr;
-  a.cs = staged >= 2 ? stage + staging_bytes(lin->num_nodes, H) : nullptr;   // c, or P for MV-RNN
-  a.keep = inst.phase_barrier_ok ? (float *)(stage + 2 * staging_bytes(lin->num_nodes, H)) : nullptr;
+  a.hs = reg.hs;
+  a.cs = reg.cs;                                     // c, P for MV-RNN, or the TreeGRU reset sums
+  a.keep = inst.phase_barrier_ok ? reg.keep : nullptr;
   a.retire = 1;                 // the tag itself comes from the workspace header (launch_tag)
   a.level_lo = 0;
   a.level_hi = 0x7fffffff;
@@ -3227,6 +3255,10 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
     return CORTEX_E_INVAL;
   const int64_t ablate = knob(CORTEX_KNOB_ABLATE);
   if (ablate & ~(int64_t)inst.ablate_bits) return CORTEX_E_INVAL;
+  if (dry_run) {                      // every host check passed; enqueue nothing
+    if (fused_children) *launched = true;
+    return CORTEX_OK;
+  }
   a.ablate = (int32_t)ablate;
   set_last_grid(1, (int32_t)G);
   if (sync_mode == 1) a.level_barrier = 1;
@@ -3322,17 +3354,71 @@ static int tree_args(int32_t cell, const cortex_lin_t *lin, const float *d_x_tab
   return CORTEX_OK;
 }
 
-extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,
-                                   int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
-                                   const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status,
-                                   void *d_ws, size_t ws_bytes, void *stream) {
+namespace cortex {
+
+static int tree_forward_impl(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,
+                             int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
+                             const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status, void *d_ws,
+                             size_t ws_bytes, void *stream, const FwdRegions *fixed, bool dry_run) {
   if (!lin_ok(lin) || !w || !d_status || x_rows < 0) return CORTEX_E_INVAL;
   if (cell < CORTEX_TREE_RNN || cell > CORTEX_SIMPLE_TREEGRU) return CORTEX_E_INVAL;
   if (lin->num_nodes == 0) return CORTEX_OK;
   FwdArgs a;
   const int rc = tree_args(cell, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status, d_ws, a);
   if (rc != CORTEX_OK) return rc;
-  return launch_forward(cell, H, lin, a, d_ws, ws_bytes, stream);
+  return launch_forward(cell, H, lin, a, d_ws, ws_bytes, stream, nullptr, nullptr, fixed, dry_run);
+}
+
+// The whole path of a tree batch: one fused launch where there is an
+// instance for it, else the linearizer then the forward.  lin_ws / fwd_ws are
+// the two workspaces (fixed: the forward's regions, placed by the caller).
+// dry_run: every host check, nothing enqueued.
+int tree_infer_impl(int32_t cell, int32_t H, const int32_t *d_children, const cortex_lin_t *lin,
+                    const float *d_x_table, int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
+                    const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status, void *lin_ws,
+                    size_t lin_ws_bytes, void *fwd_ws, size_t fwd_ws_bytes, const FwdRegions *fixed, void *stream,
+                    bool dry_run) {
+  const int32_t N = lin->num_nodes, K = lin->max_arity;
+  if (N == 0) return linearize_impl(d_children, 0, K, lin, d_status, lin_ws, lin_ws_bytes, stream, dry_run);
+  if (!d_children) return CORTEX_E_INVAL;
+  FwdArgs a;
+  int rc = tree_args(cell, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status, fwd_ws, a);
+  if (rc != CORTEX_OK) return rc;
+  // one launch where a fused instance exists and fits; else the two calls
+  bool launched = false;
+  rc = launch_forward(cell, H, lin, a, fwd_ws, fwd_ws_bytes, stream, d_children, &launched, fixed, dry_run);
+  if (rc != CORTEX_OK || launched) return rc;
+  rc = linearize_impl(d_children, N, K, lin, d_status, lin_ws, lin_ws_bytes, stream, dry_run);
+  if (rc != CORTEX_OK) return rc;
+  return tree_forward_impl(cell, H, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status,
+                           fwd_ws, fwd_ws_bytes, stream, fixed, dry_run);
+}
+
+// Regions of the forward for a workspace placed by the library (the
+// allocation-free entry point): the header and each staging region at their
+// own fixed offsets, whatever the batch, so a region only ever holds its own
+// kind of data.
+bool fixed_regions(int32_t cell, int32_t N, int32_t H, void *header, size_t header_cap, void *hs, size_t hs_cap,
+                   void *cs, size_t cs_cap, void *keep, size_t keep_cap, FwdRegions &out) {
+  size_t hs_off, cs_off, keep_off;
+  regions_bytes(cell, N, H, hs_off, cs_off, keep_off);
+  const int staged = staged_tensors(cell);
+  const size_t need_hs = staged >= 1 ? cs_off - hs_off : 0;
+  const size_t need_cs = staged >= 2 ? keep_off - cs_off : 0;
+  const size_t need_keep = (cell == CORTEX_CHILDSUM_TREEGRU || cell == CORTEX_SIMPLE_TREEGRU) ? keep_bytes(N, H) : 0;
+  if (hs_off > header_cap || need_hs > hs_cap || need_cs > cs_cap || need_keep > keep_cap) return false;
+  out = FwdRegions{header, staged >= 1 ? hs : nullptr, staged >= 2 ? cs : nullptr, (float *)keep};
+  return true;
+}
+
+}  // namespace cortex
+
+extern "C" int cortex_tree_forward(int32_t cell, int32_t H, const cortex_lin_t *lin, const float *d_x_table,
+                                   int32_t x_rows, const int32_t *d_x_index, const float *d_leaf_mat,
+                                   const cortex_weights_t *w, float *d_h, float *d_c_or_P, int32_t *d_status,
+                                   void *d_ws, size_t ws_bytes, void *stream) {
+  return tree_forward_impl(cell, H, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status, d_ws,
+                           ws_bytes, stream, nullptr, false);
 }
 
 extern "C" int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, const float *d_W,
@@ -3370,22 +3456,14 @@ extern "C" int cortex_tree_infer(int32_t cell, int32_t H, const int32_t *d_child
   if (N == 0) return cortex_linearize(d_children, 0, K, lin, d_status, d_ws, ws_bytes, stream);
   if (!d_children) return CORTEX_E_INVAL;
   FwdArgs a;
-  int rc = tree_args(cell, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status, d_ws, a);
+  const int rc = tree_args(cell, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status, d_ws, a);
   if (rc != CORTEX_OK) return rc;
   const size_t need = cortex_tree_infer_workspace_bytes(cell, N, K, H);
   if (need == 0) return CORTEX_E_INVAL;
   if (ws_bytes < need) return CORTEX_E_WORKSPACE;
   const size_t lw = align_up(cortex_linearize_workspace_bytes(N, K), 256);
-  void *fws = (char *)d_ws + lw;
-  const size_t fws_bytes = ws_bytes - lw;
-  // one launch where a fused instance exists and fits; else the two calls
-  bool launched = false;
-  rc = launch_forward(cell, H, lin, a, fws, fws_bytes, stream, d_children, &launched);
-  if (rc != CORTEX_OK || launched) return rc;
-  rc = cortex_linearize(d_children, N, K, lin, d_status, d_ws, lw, stream);
-  if (rc != CORTEX_OK) return rc;
-  return cortex_tree_forward(cell, H, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P, d_status,
-                             fws, fws_bytes, stream);
+  return tree_infer_impl(cell, H, d_children, lin, d_x_table, x_rows, d_x_index, d_leaf_mat, w, d_h, d_c_or_P,
+                         d_status, d_ws, lw, (char *)d_ws + lw, ws_bytes - lw, nullptr, stream, false);
 }
 
 extern "C" size_t cortex_dag_infer_workspace_bytes(int32_t N, int32_t K, int32_t H) {

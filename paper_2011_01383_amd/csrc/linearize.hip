@@ -359,6 +359,8 @@ __global__ void __launch_bounds__(kSmallThreads) linearize_small_kernel(LinArgs 
 
 static size_t lin_tiles(int32_t N) { return (size_t)(N + kTile - 1) / kTile; }
 
+__global__ void write_zero_kernel(int32_t *p) { *p = 0; }
+
 }  // namespace cortex
 
 using namespace cortex;
@@ -371,13 +373,23 @@ extern "C" size_t cortex_linearize_workspace_bytes(int32_t N, int32_t K) {
   return b;
 }
 
-extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin,
-                                int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream) {
+namespace cortex {
+
+// dry_run: every host check of the call, nothing enqueued.
+int linearize_impl(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin, int32_t *d_status,
+                   void *d_ws, size_t ws_bytes, void *stream, bool dry_run) {
   if (!lin || !d_status || N < 0 || K < 1 || K > 4) return CORTEX_E_INVAL;
   if (lin->num_nodes != N || lin->max_arity != K || !lin->num_levels) return CORTEX_E_INVAL;
   if (N == 0) {
-    return hipMemsetAsync(lin->num_levels, 0, sizeof(int32_t), (hipStream_t)stream) == hipSuccess
-               ? CORTEX_OK : CORTEX_E_HIP;
+    if (dry_run) return CORTEX_OK;
+    // an empty batch has no levels; a one-lane kernel (not a memset node, so
+    // the call can be captured into a graph) writes L = 0
+    int32_t *p = lin->num_levels;
+    void *kargs[] = {(void *)&p};
+    return hipLaunchKernel((const void *)write_zero_kernel, dim3(1), dim3(1), kargs, 0, (hipStream_t)stream) ==
+                   hipSuccess
+               ? CORTEX_OK
+               : CORTEX_E_HIP;
   }
   if (!d_children || !lin->height || !lin->level_offsets || !lin->level_nodes || !lin->node_row ||
       !lin->child_rows || !d_ws)
@@ -399,6 +411,7 @@ extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K,
     s.status = d_status;
     s.sync = (unsigned int *)d_ws;
     if (cached_occupancy((const void *)linearize_small_kernel, kSmallThreads, small_lds) <= 0) return CORTEX_E_HIP;
+    if (dry_run) return CORTEX_OK;
     set_last_grid(0, 1);
     return launch_persistent(linearize_small_kernel, 1, kSmallThreads, small_lds, s, stream);
   }
@@ -414,6 +427,7 @@ extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K,
     if (g_min > cap) return CORTEX_E_TOO_LARGE;
     g = cap;
   }
+  if (dry_run) return CORTEX_OK;
   LinArgs a;
   a.children = d_children;
   a.N = N;
@@ -438,4 +452,11 @@ extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K,
   a.timeout = barrier_timeout_ticks();
   set_last_grid(0, (int32_t)g);
   return launch_persistent(linearize_kernel, (int)g, kLinThreads, 0, a, stream);
+}
+
+}  // namespace cortex
+
+extern "C" int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin,
+                                int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream) {
+  return linearize_impl(d_children, N, K, lin, d_status, d_ws, ws_bytes, stream, false);
 }
