@@ -322,6 +322,22 @@ __device__ __forceinline__ floatx4 mfma_k16(float4 a4, float4 b4, floatx4 c) {
   return c;
 }
 
+// Four output tiles sharing one A fragment: the same four k steps as
+// mfma_k16 for each tile, issued step-major so that consecutive MFMAs write
+// different accumulators (no back-to-back dependence); every accumulator
+// still adds its products in the order mfma_k16 adds them.
+template <int NT>
+__device__ __forceinline__ void mfma_k16_xn(float4 a4, const float4 (&b4)[NT], floatx4 (&c)[NT]) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) c[nt] = mfma16x16x4(a4.x, b4[nt].x, c[nt]);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) c[nt] = mfma16x16x4(a4.y, b4[nt].y, c[nt]);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) c[nt] = mfma16x16x4(a4.z, b4[nt].z, c[nt]);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) c[nt] = mfma16x16x4(a4.w, b4[nt].w, c[nt]);
+}
+
 // ---------------------------------------------------------------------------
 // Gate nonlinearities from their definitions, on the hardware base-2
 // exponential and reciprocal (v_exp_f32, v_rcp_f32, about 1 ulp each):

@@ -1202,27 +1202,40 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
 // Fewer, wider slices than the kernel above: every slice re-reads the child
 // rows it contracts, so four slices move a quarter of the operand bytes of
 // sixteen.  Each wave keeps its 64 recurrent columns x 64 units of U_0 / U_1
-// in registers for the whole launch and the input weights W sit in LDS.  Per
-// 16-row tile, wave w contracts input columns [32w, 32w+32) first — they do
-// not depend on any child — and only then waits for the children and
-// contracts recurrent columns [64w, 64w+64) of [h(slot 0) | h(slot 1)]; the
-// eight partial sums meet in LDS.  When the grid is a multiple of 32, the
-// four slices of node group q are workgroups 32m + r + 8s (r = q mod 8,
-// m = q div 8, s = 0..3), which round-robin dispatch places on one XCD, so
-// the input row of a node is fetched into one L2 once.
+// in registers for the whole launch and the input weights W sit in LDS.  When
+// the grid is a multiple of 32, the four slices of node group q are
+// workgroups 32m + r + 8s (r = q mod 8, m = q div 8, s = 0..3), which
+// round-robin dispatch places on one XCD, so the input row of a node is
+// fetched into one L2 once.
 //
-// At entry each workgroup lists its own tiles of every level (the tiles u of
-// level l with u = q - l mod Q) with their operand sources in LDS, so the
-// level loop never goes back to the linearization in memory, and the next
-// tile's operands, in the same level or the next, are requested while the
-// current tile is contracted.  A group whose list does not fit the LDS
-// budget walks the levels instead, staging each chunk of tiles' sources.
+// Work is done in steps: a step is up to two of the group's 16-row tiles of
+// one level (group q owns the tiles u of level l with u = q - l mod Q, so a
+// level of up to 2Q tiles is one step per group).  The tiles of a step share
+// one wait, one cross-wave reduction and one epilogue, and every weight
+// fragment is read once for both tiles.  Per step, wave w
+//   1. requests the child-state fragments of its recurrent columns
+//      [64w, 64w+64) of [h(slot 0) | h(slot 1)] for every row of the step,
+//   2. contracts input columns [32w, 32w+32) (requested one step earlier;
+//      they depend on no child) while those loads are in flight,
+//   3. requests the next step's input fragments,
+//   4. waits until every fragment it read carries this launch's tag,
+//   5. contracts the recurrent columns;
+// the eight partial sums then meet in LDS and the workgroup applies tanh and
+// writes the step's rows.  At entry each workgroup lists its steps of every
+// level with their operand sources in LDS, so the level loop never goes back
+// to the linearization in memory; a group whose list does not fit walks the
+// levels instead, staging one step's sources at a time.
 // ---------------------------------------------------------------------------
 constexpr int kDagH = 256, kDagJ = 64, kDagS = kDagH / kDagJ;
 constexpr int kDagWideMinRows = 12288;             // default choice of this kernel (measured crossover)
-constexpr int kDagTileInts = 4 + kTileM * 3;        // level, level start, first row, level end, codes[16][3]
-constexpr int kDagTileCap = 240;                    // tiles per workgroup list (dynamic LDS)
-constexpr size_t kDagListBytes = (size_t)kDagTileCap * kDagTileInts * sizeof(int);
+constexpr int kDagStepTiles = 2;                   // tiles per step
+constexpr int kDagStepRows = kDagStepTiles * kTileM;
+// level, level start, first row of tile 0, first row of tile 1 (-1: none),
+// level end, then codes[32][3]: -2 - node id (input row) or -1, child rows
+constexpr int kDagStepHead = 5;
+constexpr int kDagStepInts = kDagStepHead + kDagStepRows * 3;
+constexpr int kDagStepCap = 60;                    // steps per workgroup list (dynamic LDS)
+constexpr size_t kDagListBytes = (size_t)kDagStepCap * kDagStepInts * sizeof(int);
 
 // Exclusive prefix sum of one value per thread over the workgroup; wsum
 // holds kFwdWaves + 1 ints of LDS.  Returns the exclusive sum, *total the sum.
@@ -1252,24 +1265,60 @@ __device__ __forceinline__ int block_excl_scan(int v, int *wsum, int *total) {
   return ex;
 }
 
+// Tiles of group `group` at a level of ntile tiles: u = uf, uf + Q, ...;
+// returns their count.
+__device__ __forceinline__ int dag_group_tiles(int group, int l, int Q, int ntile, int &uf) {
+  uf = ((group - l) % Q + Q) % Q;
+  return uf < ntile ? (ntile - 1 - uf) / Q + 1 : 0;
+}
+
+// Operand sources of row slot (t, i) of a step record; validates them as the
+// forward requires (a child lies below its row's level).  Returns false when
+// the linearization is inconsistent.
+__device__ __forceinline__ bool dag_fill_codes(const FwdArgs &a, int *st, int slot) {
+  const int t = slot / kTileM, i = slot % kTileM;
+  const int base = st[2 + t], lstart = st[1], lend = st[4];
+  const int row = base + i;
+  int *cd = &st[kDagStepHead + slot * 3];
+  bool ok = true;
+  int v = -1, c0 = -1, c1 = -1;
+  if (base >= 0 && row < lend) {
+    v = a.level_nodes[row];
+    c0 = a.child_rows[(size_t)row * 2];
+    c1 = a.child_rows[(size_t)row * 2 + 1];
+    if (v < 0 || v >= a.N) ok = false;
+  }
+  cd[0] = (v >= 0 && v < a.N) ? -2 - v : -1;
+  if (c0 < -1 || c0 >= lstart) {
+    ok = false;
+    c0 = -1;
+  }
+  if (c1 < -1 || c1 >= lstart) {
+    ok = false;
+    c1 = -1;
+  }
+  cd[1] = c0;
+  cd[2] = c1;
+  return ok;
+}
+
 __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   constexpr int H = kDagH, J = kDagJ, NT = J / 16;
   constexpr int KX = H / kFwdWaves, NBX = KX / 16;          // input columns per wave, 16-blocks
   constexpr int KR = 2 * H / kFwdWaves, NBR = KR / 16;      // recurrent columns per wave, 16-blocks
   constexpr int LDX = H + 4;                                // W row stride in LDS
   constexpr int LDC = J + 4;                                // partial-sum row stride
-  constexpr int EPI = kTileM * J / kFwdThreads;             // outputs per thread per tile
-  constexpr int TI = kDagTileInts;
-  constexpr int R = 4;                                      // listed rows loaded per thread per round
-  static_assert(NBX * 16 == KX && NBR * 16 == KR && EPI * kFwdThreads == kTileM * J, "tiling");
+  constexpr int MT = kDagStepTiles;
+  constexpr int SI = kDagStepInts;
+  constexpr int EPI = MT * kTileM * J / kFwdThreads;        // outputs per thread per full step
+  static_assert(NBX * 16 == KX && NBR * 16 == KR && EPI * kFwdThreads == MT * kTileM * J, "tiling");
   static_assert(KR == 64 && H % KR == 0, "a wave's recurrent columns lie in one child slot");
 
   __shared__ __attribute__((aligned(16))) float Wx_s[J * LDX];
-  __shared__ __attribute__((aligned(16))) float C_s[kFwdWaves * kTileM * LDC];
+  __shared__ __attribute__((aligned(16))) float C_s[kFwdWaves * MT * kTileM * LDC];
   __shared__ float bias_s[J];
-  __shared__ ChunkSrc chunk;
   __shared__ int wsum[kFwdWaves + 1];
-  extern __shared__ int list[];               // [kDagTileCap][kDagTileInts]
+  extern __shared__ int list[];               // [kDagStepCap][kDagStepInts]
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
@@ -1321,28 +1370,29 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   }
   CORTEX_TRACE_KERNEL(1);
 
-  // ---- this group's tiles of every level, one level per thread per round ----
+  // ---- this group's steps of every level, one level per thread per round ----
   int total = 0, bad = 0;
   for (int lb = 0; lb < L; lb += kFwdThreads) {
     const int l = lb + tid;
-    int cnt = 0, r0 = 0, r1 = 0, uf = 0;
+    int nst = 0, r0 = 0, r1 = 0, uf = 0, cnt = 0;
     if (l < L) {
       r0 = a.level_offsets[l];
       r1 = a.level_offsets[l + 1];
       const bool ok = r0 >= 0 && r1 >= r0 && r1 <= N && (l != 0 || r0 == 0) && (l != L - 1 || r1 == N);
       if (!ok) bad = 1;
       const int ntile = (ok && l >= a.level_lo && l < a.level_hi) ? (r1 - r0 + kTileM - 1) / kTileM : 0;
-      uf = ((group - l) % Q + Q) % Q;
-      cnt = uf < ntile ? (ntile - 1 - uf) / Q + 1 : 0;
+      cnt = dag_group_tiles(group, l, Q, ntile, uf);
+      nst = (cnt + MT - 1) / MT;
     }
     int round_total;
-    const int pos = total + block_excl_scan(cnt, wsum, &round_total);
-    for (int j = 0; j < cnt && pos + j < kDagTileCap; ++j) {
-      int *t = &list[(pos + j) * TI];
-      t[0] = l;
-      t[1] = r0;
-      t[2] = r0 + kTileM * (uf + j * Q);
-      t[3] = r1;
+    const int pos = total + block_excl_scan(nst, wsum, &round_total);
+    for (int j = 0; j < nst && pos + j < kDagStepCap; ++j) {
+      int *st = &list[(pos + j) * SI];
+      st[0] = l;
+      st[1] = r0;
+      st[2] = r0 + kTileM * (uf + (MT * j) * Q);
+      st[3] = MT * j + 1 < cnt ? r0 + kTileM * (uf + (MT * j + 1) * Q) : -1;
+      st[4] = r1;
     }
     total += round_total;
   }
@@ -1351,48 +1401,10 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
     return;
   }
-  const bool listed = total <= kDagTileCap;
+  const bool listed = total <= kDagStepCap;
   if (listed) {
-    // operand sources of every listed row: code 0 = -2 - node id (its input
-    // row), codes 1 and 2 = child rows, which must lie below the row's level
-    for (int base = 0; base < total * kTileM; base += R * kFwdThreads) {
-      int v[R], c[R][2];
-#pragma unroll
-      for (int k = 0; k < R; ++k) {
-        const int idx = base + k * kFwdThreads + tid;
-        v[k] = -1;
-        c[k][0] = c[k][1] = -1;
-        if (idx < total * kTileM) {
-          const int *t = &list[(idx / kTileM) * TI];
-          const int row = t[2] + idx % kTileM;
-          if (row < t[3]) {
-            v[k] = a.level_nodes[row];
-            c[k][0] = a.child_rows[(size_t)row * 2];
-            c[k][1] = a.child_rows[(size_t)row * 2 + 1];
-          }
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < R; ++k) {
-        const int idx = base + k * kFwdThreads + tid;
-        if (idx < total * kTileM) {
-          int *t = &list[(idx / kTileM) * TI];
-          const int row = t[2] + idx % kTileM, lstart = t[1];
-          int *cd = &t[4 + (idx % kTileM) * 3];
-          if (row < t[3] && (v[k] < 0 || v[k] >= N)) bad = 1;
-          cd[0] = (v[k] >= 0 && v[k] < N) ? -2 - v[k] : -1;
-#pragma unroll
-          for (int s = 0; s < 2; ++s) {
-            int ch = c[k][s];
-            if (ch < -1 || ch >= lstart) {
-              bad = 1;
-              ch = -1;
-            }
-            cd[1 + s] = ch;
-          }
-        }
-      }
-    }
+    for (int idx = tid; idx < total * kDagStepRows; idx += kFwdThreads)
+      if (!dag_fill_codes(a, &list[(idx / kDagStepRows) * SI], idx % kDagStepRows)) bad = 1;
     if (__syncthreads_or(bad)) {
       raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
       return;
@@ -1402,70 +1414,85 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   if (!mark_entered(a.sync, tag, a.status)) return;
   int gave_up = 0;
 
-  struct Ops {
-    u32x4 xv[NBX];     // input fragments (plain)
-    Frag hv[NBR];      // child-state fragments (staged pairs)
-    int cr;            // child row of this lane's tile row, -1 = none
-  };
-  // Operands of the tile whose rows start at rowbase (rows < rend live) and
-  // whose sources are cd[16][3].
-  auto issue = [&](const int *cd, int rowbase, int rend, Ops &t) __attribute__((always_inline)) {
-    int xc = -1, cr = -1;
-    if (rowbase + i16 < rend) {
-      xc = cd[i16 * 3];
-      cr = cd[i16 * 3 + 1 + rslot];
-    }
-    // one base offset per operand: the blocks and halves add constants,
-    // which the loads take as immediate offsets (an absent source stays
-    // beyond the buffer with them)
-    const uint32_t xo = xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 4 * g4) * 4) : kNoSource;
-    const uint32_t ho = cr >= 0 ? (uint32_t)(cr * H + rcol + 4 * g4) * 8u : kNoSource;
-    t.cr = cr;
+  // input fragments of a step's rows (tile t, row i16): x[node][xcol + 16 b + 4 g4 .. +3]
+  auto issue_x = [&](const int *st, u32x4 (&xv)[MT][NBX]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int b = 0; b < NBX; ++b) t.xv[b] = xin.load4(xo + 64u * b);
+    for (int t = 0; t < MT; ++t) {
+      const int base = st[2 + t];
+      const int xc = (base >= 0 && base + i16 < st[4]) ? st[kDagStepHead + (t * kTileM + i16) * 3] : -1;
+      const uint32_t xo = xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 4 * g4) * 4) : kNoSource;
 #pragma unroll
-    for (int b = 0; b < NBR; ++b) {
-      t.hv[b].lo = hs.load2_at(ho + 128u * b);
-      t.hv[b].hi = hs.load2_at(ho + 128u * b + 16u);
+      for (int b = 0; b < NBX; ++b) xv[t][b] = xin.load4(xo + 64u * b);
     }
   };
-  auto ready = [&](const Ops &t) __attribute__((always_inline)) -> bool {
-    bool r = true;
+
+  // One step.  xc: its input fragments (requested earlier); nst: the next
+  // step (nullptr: none), whose input fragments go to xn.  Returns true when
+  // the kernel must stop.
+  auto run_step = [&](const int *st, const u32x4 (&xc)[MT][NBX], const int *nst,
+                      u32x4 (&xn)[MT][NBX]) __attribute__((always_inline)) -> bool {
+    const int l = st[0], lend = st[4];
+    const bool two = st[3] >= 0;
+    // 1. child-state fragments of every row of the step
+    Frag hv[MT][NBR];
+    int cr[MT];
 #pragma unroll
-    for (int b = 0; b < NBR; ++b) r = r && t.hv[b].ready(tag);
-    return t.cr < 0 || r;
-  };
-  // One tile: input part, wait, request the next tile's operands (ncd !=
-  // nullptr), recurrent part, epilogue.  Returns true when the kernel must stop.
-  auto process = [&](int l, int rowbase, int rend, Ops &t, const int *ncd, int nrow, int nrend,
-                     Ops &tn) __attribute__((always_inline)) -> bool {
-    (void)l;
-    floatx4 acc[2][NT];
+    for (int t = 0; t < MT; ++t) {
+      const int base = st[2 + t];
+      cr[t] = (base >= 0 && base + i16 < lend) ? st[kDagStepHead + (t * kTileM + i16) * 3 + 1 + rslot] : -1;
+      const uint32_t ho = cr[t] >= 0 ? (uint32_t)(cr[t] * H + rcol + 4 * g4) * 8u : kNoSource;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[0][nt] = acc[1][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int b = 0; b < NBR; ++b) {
+        hv[t][b].lo = hs.load2_at(ho + 128u * b);
+        hv[t][b].hi = hs.load2_at(ho + 128u * b + 16u);
+      }
+    }
+    // 2. input part; one weight fragment serves both tiles
+    floatx4 acc[MT][NT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[t][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
     const float *bx = &Wx_s[i16 * LDX + xcol + 4 * g4];
 #pragma unroll
     for (int b = 0; b < NBX; ++b) {
-      const float4 av = as_float4(t.xv[b]);
+      float4 wv[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        acc[b & 1][nt] = mfma_k16(av, *(const float4 *)(bx + nt * 16 * LDX + 16 * b), acc[b & 1][nt]);
+      for (int nt = 0; nt < NT; ++nt) wv[nt] = *(const float4 *)(bx + nt * 16 * LDX + 16 * b);
+      mfma_k16_xn<NT>(as_float4(xc[0][b]), wv, acc[0]);
+      if (two) mfma_k16_xn<NT>(as_float4(xc[1][b]), wv, acc[1]);
     }
+    // 3. the next step's input fragments, in flight through this step
+    if (nst) issue_x(nst, xn);
     CORTEX_TRACE_POINT(l, 1);
-    if (!gave_up && !ready(t)) {
+    // 4. wait for the children
+    auto ready = [&]() __attribute__((always_inline)) -> bool {
+      bool r = true;
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        bool rt = true;
+#pragma unroll
+        for (int b = 0; b < NBR; ++b) rt = rt && hv[t][b].ready(tag);
+        r = r && (cr[t] < 0 || rt);
+      }
+      return r;
+    };
+    if (!gave_up && !ready()) {
       const uint64_t t0 = wall_clock64();
       for (;;) {
         __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-        for (int b = 0; b < NBR; ++b) {
-          if (!t.hv[b].ready(tag)) {
-            const uint32_t so = (uint32_t)(t.cr * H + rcol + 16 * b + 4 * g4) * 8u;
-            t.hv[b].lo = hs.load2_at(so);
-            t.hv[b].hi = hs.load2_at(so + 16u);
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+          for (int b = 0; b < NBR; ++b) {
+            if (cr[t] >= 0 && !hv[t][b].ready(tag)) {
+              const uint32_t so = (uint32_t)(cr[t] * H + rcol + 16 * b + 4 * g4) * 8u;
+              hv[t][b].lo = hs.load2_at(so);
+              hv[t][b].hi = hs.load2_at(so + 16u);
+            }
           }
-        }
         const int stv = load_status(a.status);
-        if (ready(t)) break;
+        if (ready()) break;
         if (stv != 0) {
           gave_up = 1;
           break;
@@ -1478,83 +1505,95 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       }
     }
     CORTEX_TRACE_POINT(l, 2);
-    if (ncd) issue(ncd, nrow, nrend, tn);      // in flight during the recurrent part
+    // 5. recurrent part
 #pragma unroll
     for (int b = 0; b < NBR; ++b) {
-      const float4 av = t.hv[b].value(true);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[b & 1][nt] = mfma_k16(av, wr[b][nt], acc[b & 1][nt]);
+      mfma_k16_xn<NT>(hv[0][b].value(true), wr[b], acc[0]);
+      if (two) mfma_k16_xn<NT>(hv[1][b].value(true), wr[b], acc[1]);
     }
     CORTEX_TRACE_WAVE(l);
-    // the next tile's loads stay in flight through this tile's epilogue
-    // (vector memory operations retire in order, so its first use waits
-    // for them alone)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int t = 0; t < MT; ++t)
+      if (t == 0 || two)
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        C_s[(wave * kTileM + 4 * g4 + v) * LDC + nt * 16 + i16] = acc[0][nt][v] + acc[1][nt][v];
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            C_s[((wave * MT + t) * kTileM + 4 * g4 + v) * LDC + nt * 16 + i16] = acc[t][nt][v];
     __syncthreads();
     CORTEX_TRACE_POINT(l, 3);
+    // every output of the thread first, then the stores: a store's data
+    // registers are not reused while earlier stores are in flight
+    const int outs = (two ? MT : 1) * kTileM * J;
+    float hv_out[EPI];
+    uint32_t el[EPI];
 #pragma unroll
     for (int e = 0; e < EPI; ++e) {
-      const int p = tid + e * kFwdThreads, i = p / J, j = p % J;
-      const int row = rowbase + i;
+      const int p = tid + e * kFwdThreads;
+      const int t = p / (kTileM * J), i = (p / J) % kTileM, j = p % J;
+      const int row = st[2 + t] + i;
       float sum = bias_s[j];
 #pragma unroll
-      for (int w = 0; w < kFwdWaves; ++w) sum += C_s[(w * kTileM + i) * LDC + j];
-      if (row < rend) {
-        const uint32_t el = (uint32_t)(row * H + hbase + j);
-        const float hv = tanh_f(sum);
-        hs.store1(el, hv, tag);
-        a.h[el] = hv;
+      for (int w = 0; w < kFwdWaves; ++w) sum += C_s[((w * MT + t) * kTileM + i) * LDC + j];
+      hv_out[e] = tanh_f(sum);
+      el[e] = (p < outs && row < lend) ? (uint32_t)(row * H + hbase + j) : 0xFFFFFFFFu;
+    }
+#pragma unroll
+    for (int e = 0; e < EPI; ++e) {
+      if (el[e] != 0xFFFFFFFFu) {
+        hs.store1(el[e], hv_out[e], tag);
+        a.h[el[e]] = hv_out[e];
       }
     }
     CORTEX_TRACE_POINT(l, 4);
     return __syncthreads_or(gave_up) != 0;
   };
 
-  Ops ta, tb;
+  u32x4 xa[MT][NBX], xb[MT][NBX];
   if (listed) {
-    // one flat pass over this group's tiles, level after level
-    auto tile = [&](int e) __attribute__((always_inline)) -> const int * { return &list[e * TI]; };
-    if (total > 0) issue(tile(0) + 4, tile(0)[2], tile(0)[3], ta);
-    for (int e = 0; e < total;) {
-#pragma unroll
-      for (int ph = 0; ph < 2; ++ph) {
-        const int *t = tile(e);
-        const bool more = e + 1 < total;
-        const int *tn = more ? tile(e + 1) : nullptr;
-        if (e == 0 || tile(e - 1)[0] != t[0]) CORTEX_TRACE_POINT(t[0], 0);
-        const bool stop = process(t[0], t[2], t[3], ph ? tb : ta, more ? tn + 4 : nullptr, more ? tn[2] : 0,
-                                  more ? tn[3] : 0, ph ? ta : tb);
-        if (!more || tn[0] != t[0]) CORTEX_TRACE_POINT(t[0], 5);
-        if (stop) return;
-        if (++e >= total) break;
-      }
+    // one flat pass over this group's steps, level after level
+    auto step = [&](int e) __attribute__((always_inline)) -> const int * { return &list[e * SI]; };
+    // two steps per iteration, written out, so each step's input fragments
+    // stay in fixed registers (xa, xb) rather than being selected at run time
+    if (total > 0) issue_x(step(0), xa);
+    for (int e = 0; e < total; e += 2) {
+      CORTEX_TRACE_POINT(step(e)[0], 0);
+      if (run_step(step(e), xa, e + 1 < total ? step(e + 1) : nullptr, xb)) return;
+      CORTEX_TRACE_POINT(step(e)[0], 5);
+      if (e + 1 >= total) break;
+      CORTEX_TRACE_POINT(step(e + 1)[0], 0);
+      if (run_step(step(e + 1), xb, e + 2 < total ? step(e + 2) : nullptr, xa)) return;
+      CORTEX_TRACE_POINT(step(e + 1)[0], 5);
     }
   } else {
-    // the list does not fit: walk the levels, staging each chunk of tiles' sources
+    // the list does not fit: walk the levels, staging one step's sources at
+    // a time in the first list entry
+    int *st = list;
     const int *off = a.level_offsets;
     for (int l = a.level_lo; l < L && l < a.level_hi; ++l) {
       CORTEX_TRACE_POINT(l, 0);
       const int r0 = off[l], r1 = off[l + 1];
-      const int ntile = (r1 - r0 + kTileM - 1) / kTileM;
-      for (int u0 = ((group - l) % Q + Q) % Q; u0 < ntile; u0 += Q * kChunkTiles) {
-        const int u_last = min(ntile - 1, u0 + Q * (kChunkTiles - 1));
-        __syncthreads();                // the previous chunk's codes are no longer read
-        stage_chunk_codes<CELL_DAG>(a, chunk, u0, (u_last - u0) / Q + 1, Q, r0, r1, 0);
-        __syncthreads();
-        issue(&chunk.code[0][0][0], r0 + u0 * kTileM, r1, ta);
-        for (int u = u0, k = 0;; ++k) {
-          const bool more = u + Q <= u_last;
-          const int *ncd = more ? &chunk.code[k + 1][0][0] : nullptr;
-          const bool stop = process(l, r0 + u * kTileM, r1, (k & 1) ? tb : ta, ncd, r0 + (u + Q) * kTileM, r1,
-                                    (k & 1) ? ta : tb);
-          if (stop) return;
-          u += Q;
-          if (!more) break;
+      int uf;
+      const int cnt = dag_group_tiles(group, l, Q, (r1 - r0 + kTileM - 1) / kTileM, uf);
+      for (int k = 0; k < cnt; k += MT) {
+        __syncthreads();                // the previous step's sources are no longer read
+        if (tid == 0) {
+          st[0] = l;
+          st[1] = r0;
+          st[2] = r0 + kTileM * (uf + k * Q);
+          st[3] = k + 1 < cnt ? r0 + kTileM * (uf + (k + 1) * Q) : -1;
+          st[4] = r1;
         }
+        __syncthreads();
+        int bad_codes = 0;
+        for (int s = tid; s < kDagStepRows; s += kFwdThreads)
+          if (!dag_fill_codes(a, st, s)) bad_codes = 1;
+        if (__syncthreads_or(bad_codes)) {
+          raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+          return;
+        }
+        issue_x(st, xa);
+        if (run_step(st, xa, nullptr, xb)) return;
       }
       CORTEX_TRACE_POINT(l, 5);
     }

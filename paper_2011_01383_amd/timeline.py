@@ -35,7 +35,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 TRACE_LIB = os.path.join(HERE, "libcortex_trace.so")
 
-SYNC_BYTES = 128 + 4 * 4096 * 5          # barrier words ahead of the timeline
+SYNC_BYTES = 128 + 4 * 4096 * 6          # workspace header (barrier, epoch and entered words) ahead of the timeline
 TRACE_BLOCKS, TRACE_LEVELS, TRACE_SLOTS = 256, 64, 16
 TICKS_PER_US = 100.0
 
@@ -122,6 +122,7 @@ def main():
     ap.add_argument("--json", default=None)
     ap.add_argument("--markdown", default=None)
     ap.add_argument("--npy", default=None, help="also save the raw stamps, uint64 [256, 64, 16]")
+    ap.add_argument("--lib", default=TRACE_LIB, help="trace build of the library to load")
     ap.add_argument("--two-calls", action="store_true",
                     help="trace cortex_linearize, then the forward entry point, instead of the step's launch")
     args = ap.parse_args()
@@ -131,9 +132,9 @@ def main():
     from . import inputs as I
     from .runner import DeviceWorkload
 
-    if not os.path.exists(TRACE_LIB):
-        raise RuntimeError("%s is not built; run python -m paper_2011_01383_amd.build --trace" % TRACE_LIB)
-    C.load(TRACE_LIB)
+    if not os.path.exists(args.lib):
+        raise RuntimeError("%s is not built; run python -m paper_2011_01383_amd.build --trace" % args.lib)
+    C.load(args.lib)
     torch.cuda.set_device(0)
     wl = I.make_workload(args.workload)
     dw = DeviceWorkload(wl)
