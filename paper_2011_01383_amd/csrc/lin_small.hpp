@@ -98,6 +98,66 @@ __device__ __forceinline__ bool height_sweep(const int (&lc)[PER][4], const int 
   return changed;
 }
 
+// Dataflow pre-pass before the sweeps: a node's height is computed once,
+// when every child it has inside the block is final (hs[c] >= 0; hs holds -1
+// for a node not yet computed), as 1 + max over those children and the
+// outside lower bounds ext.  Waves run without barriers and each retries its
+// pending nodes until all are done, so a chain of dependences advances about
+// one node per retry of the wave that holds the next node; a retry requests
+// every child height of the thread's nodes at once (one LDS round trip).  A
+// cycle (or a very long chain) leaves nodes pending; after max_tries retries
+// the pass gives up and leaves them at 0.  Every computed value is the height
+// given ext, which is at most the true height, so the sweeps that follow
+// start from valid lower bounds and confirm (or finish) the fixed point.
+// Returns after a workgroup barrier.
+template <int PER, int THREADS, int KS>
+__device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
+                                int max_tries) {
+  const int wave_first = (int)(threadIdx.x & ~63u);
+  bool pending[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) pending[j] = (int)threadIdx.x + j * THREADS < n;
+  for (int tries = 0; tries < max_tries; ++tries) {
+    bool left = false;
+    int hvs[PER][KS];
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) hvs[j][s] = lds_load(&hs[lc[j][s] >= 0 ? lc[j][s] : 0]);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      if (wave_first + j * THREADS >= n) break;
+      bool ready = true;
+      int m = -1;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if (lc[j][s] >= 0) {
+          ready = ready && hvs[j][s] >= 0;
+          m = max(m, hvs[j][s]);
+        }
+        m = max(m, ext[j][s]);
+      }
+      if (pending[j] && ready) {
+        myh[j] = m + 1;
+        lds_store(&hs[(int)threadIdx.x + j * THREADS], m + 1);
+        pending[j] = false;
+      }
+      left = left || pending[j];
+    }
+    if (!__any(left)) break;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int i = (int)threadIdx.x + j * THREADS;
+    if (i < n && pending[j]) {
+      myh[j] = 0;
+      lds_store(&hs[i], 0);
+    }
+  }
+  __syncthreads();
+}
+
 // Sweeps to the fixed point over child slots [0, KS).  Returns (uniformly
 // over the workgroup) whether any height changed; *cycle is set when a value
 // reached N.  Every thread of the workgroup calls it.
@@ -473,6 +533,15 @@ __device__ int small_linearize(const int32_t *children, int N, int K, int32_t *s
     for (int j = 0; j < PER; ++j)
 #pragma unroll
       for (int s = 0; s < 4; ++s) ext[j][s] = -1;
+    // dataflow order first (hgt = -1: not computed), then sweeps confirm
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      if (tid + j * THREADS < N) lds_store(&hgt[tid + j * THREADS], -1);
+    __syncthreads();
+    if (K <= 2)
+      height_dataflow<PER, THREADS, 2>(myc, ext, myh, hgt, N, 4 * N);
+    else
+      height_dataflow<PER, THREADS, 4>(myc, ext, myh, hgt, N, 4 * N);
     bool cyc;
     int sweeps = 0;
     relax_heights<PER, THREADS>(myc, ext, myh, hgt, N, K, N, &cyc, &sweeps);

@@ -120,12 +120,39 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   }
   bool ok = status0 == 0;
   if (bad) raise_status(a.status, CORTEX_ST_CHILD_RANGE);
-  for (int i = tid; i < n; i += kLinThreads) hs[i] = 0;
+  for (int i = tid; i < n; i += kLinThreads) hs[i] = in_regs ? -1 : 0;
   __syncthreads();
+  CORTEX_BIG_STAMP(9, wall_clock64());
+  if (in_regs && ok) {
+    // round 0: children outside the chunk count 0 (a lower bound); nodes
+    // whose in-chunk children are final are computed once, in dataflow order
+#pragma unroll
+    for (int j = 0; j < kLinPer; ++j)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) ext[j][s] = (cid[j][s] < 0 || lc[j][s] >= 0) ? -1 : 0;
+    if (K <= 2)
+      height_dataflow<kLinPer, kLinThreads, 2>(lc, ext, myh, hs, n, 4 * kTargetChunk);
+    else
+      height_dataflow<kLinPer, kLinThreads, 4>(lc, ext, myh, hs, n, 4 * kTargetChunk);
+  }
+  CORTEX_BIG_STAMP(10, wall_clock64());
+  // a chunk whose children all lie inside it reaches its exact heights in
+  // round 0; only when some chunk reads an outside child (counted 0 in round
+  // 0) does a second round have to check the fixed point across chunks
+  int has_ext = 0;
+  if (in_regs) {
+#pragma unroll
+    for (int j = 0; j < kLinPer; ++j)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) has_ext |= (cid[j][s] >= 0 && lc[j][s] < 0);
+  } else {
+    has_ext = 1;
+  }
+  has_ext = __syncthreads_or(has_ext);
   int round = 0;
   int L = 0;
   while (ok) {
-    int block_changed = (round == 0);
+    int block_changed = (round == 0) && has_ext;
     int local_max = 0;
     if (in_regs) {
       // children outside the chunk keep one height per round: 0 in round 0
@@ -140,7 +167,10 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
                           : (round == 0 ? 0 : __hip_atomic_load(&a.height[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
         }
       bool cyc;
-      if (relax_heights<kLinPer, kLinThreads>(lc, ext, myh, hs, n, K, N, &cyc, &sweeps0)) block_changed = 1;
+      // (round 0 reports has_ext alone: a chunk without outside children
+      // is exact whatever its sweeps changed)
+      if (relax_heights<kLinPer, kLinThreads>(lc, ext, myh, hs, n, K, N, &cyc, &sweeps0) && round > 0)
+        block_changed = 1;
       if (cyc && tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
     } else for (;;) {
       int changed = 0, cyc = 0;
@@ -183,6 +213,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       local_max = max(local_max, hv);
     }
     local_max = block_max(local_max, scan_tmp);
+    if (round == 0) CORTEX_BIG_STAMP(11, wall_clock64());
     if (G == 1) {
       L = local_max + 1;
       ok = grid_sync(sw, a.status, a.timeout);
@@ -194,6 +225,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       st_agent(sw.slot(1, round & 1, blockIdx.x), (unsigned)local_max);
     }
     ok = grid_sync(sw, a.status, a.timeout);
+    if (round == 0) CORTEX_BIG_STAMP(12, wall_clock64());
     if (!ok) break;
     int any = 0, mx = 0;
     for (int b = tid; b < G; b += kLinThreads) {

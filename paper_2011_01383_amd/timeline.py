@@ -174,6 +174,10 @@ def main():
         rep["linearize_big_phases_us"] = [float(x - t[0]) / TICKS_PER_US for x in t]
         rep["linearize_big_rounds"] = int(lin_big[7])
         rep["linearize_big_sweeps0"] = int(lin_big[8])
+        # heights, round 0 (trace stamps 9-12 where present): children in
+        # registers, dataflow pass done, local fixed point and heights written,
+        # first grid barrier passed
+        rep["linearize_big_round0_us"] = [float(x - t[0]) / TICKS_PER_US if x > 0 else None for x in lin_big[9:13]]
     if C.cortex_last_grid(0) == 1 and lin_stamps[0] > 0:
         # single-workgroup linearizer: entry, children loaded, heights done,
         # level counts, sort done, outputs written, offsets written
@@ -200,6 +204,10 @@ def main():
                "%d local sweeps in round 0), histograms %.2f, scan %.2f, sort %.2f, offsets and child rows %.2f us."
                % (C.cortex_last_grid(0), rep["linearize_big_phases_us"][1], rep["linearize_big_rounds"],
                   rep["linearize_big_sweeps0"], *rep["linearize_big_phases_us"][2:]))
+        r0 = rep["linearize_big_round0_us"]
+        if all(v is not None for v in r0):
+            md += (" Round 0 of the heights: children in registers %.2f, dataflow pass %.2f, local fixed point and "
+                   "heights written %.2f, first grid barrier %.2f us." % tuple(r0))
     print(md)
     sys.stdout.flush()
     if args.json:
