@@ -1433,20 +1433,25 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
                       u32x4 (&xn)[MT][NBX]) __attribute__((always_inline)) -> bool {
     const int l = st[0], lend = st[4];
     const bool two = st[3] >= 0;
-    // 1. child-state fragments of every row of the step
     Frag hv[MT][NBR];
     int cr[MT];
+    // 1. child-state fragments of every row of the step, requested halfway
+    //    through the input part rather than at the start: a level's children
+    //    are written at the end of the previous level, about when this step
+    //    begins, so pairs read at once would mostly still carry old tags
+    auto issue_h = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      const int base = st[2 + t];
-      cr[t] = (base >= 0 && base + i16 < lend) ? st[kDagStepHead + (t * kTileM + i16) * 3 + 1 + rslot] : -1;
-      const uint32_t ho = cr[t] >= 0 ? (uint32_t)(cr[t] * H + rcol + 4 * g4) * 8u : kNoSource;
+      for (int t = 0; t < MT; ++t) {
+        const int base = st[2 + t];
+        cr[t] = (base >= 0 && base + i16 < lend) ? st[kDagStepHead + (t * kTileM + i16) * 3 + 1 + rslot] : -1;
+        const uint32_t ho = cr[t] >= 0 ? (uint32_t)(cr[t] * H + rcol + 4 * g4) * 8u : kNoSource;
 #pragma unroll
-      for (int b = 0; b < NBR; ++b) {
-        hv[t][b].lo = hs.load2_at(ho + 128u * b);
-        hv[t][b].hi = hs.load2_at(ho + 128u * b + 16u);
+        for (int b = 0; b < NBR; ++b) {
+          hv[t][b].lo = hs.load2_at(ho + 128u * b);
+          hv[t][b].hi = hs.load2_at(ho + 128u * b + 16u);
+        }
       }
-    }
+    };
     // 2. input part; one weight fragment serves both tiles
     floatx4 acc[MT][NT];
 #pragma unroll
@@ -1461,6 +1466,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       for (int nt = 0; nt < NT; ++nt) wv[nt] = *(const float4 *)(bx + nt * 16 * LDX + 16 * b);
       mfma_k16_xn<NT>(as_float4(xc[0][b]), wv, acc[0]);
       if (two) mfma_k16_xn<NT>(as_float4(xc[1][b]), wv, acc[1]);
+      if (b == NBX / 2 - 1) issue_h();
     }
     // 3. the next step's input fragments, in flight through this step
     if (nst) issue_x(nst, xn);
