@@ -200,6 +200,13 @@ struct InBuf {
   }
 };
 
+// Makes the compiler complete the load that produced v here (an empty asm
+// that reads v).  The memory counter on gfx950 counts stores as well as
+// loads, so a wait for a load issued before some stores also waits for those
+// stores once they are outstanding; settling a prefetched operand before a
+// step's stores keeps its first use from waiting on them.
+__device__ __forceinline__ void settle(const u32x4 &v) { asm volatile("" ::"v"(v)); }
+
 __device__ __forceinline__ float4 as_float4(u32x4 v) {
   return make_float4(as_float(v.x), as_float(v.y), as_float(v.z), as_float(v.w));
 }
@@ -336,6 +343,18 @@ __device__ __forceinline__ void mfma_k16_xn(float4 a4, const float4 (&b4)[NT], f
   for (int nt = 0; nt < NT; ++nt) c[nt] = mfma16x16x4(a4.z, b4[nt].z, c[nt]);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) c[nt] = mfma16x16x4(a4.w, b4[nt].w, c[nt]);
+}
+
+// Step s (0..3) of mfma_k16_xn alone, so other instructions can be placed
+// between the steps; steps 0..3 in order add exactly what mfma_k16_xn adds.
+template <int NT>
+__device__ __forceinline__ void mfma_kstep_xn(int s, float4 a4, const float4 (&b4)[NT], floatx4 (&c)[NT]) {
+  const float a = s == 0 ? a4.x : s == 1 ? a4.y : s == 2 ? a4.z : a4.w;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const float b = s == 0 ? b4[nt].x : s == 1 ? b4[nt].y : s == 2 ? b4[nt].z : b4[nt].w;
+    c[nt] = mfma16x16x4(a, b, c[nt]);
+  }
 }
 
 // ---------------------------------------------------------------------------

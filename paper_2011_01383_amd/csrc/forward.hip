@@ -1213,15 +1213,16 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
 // level of up to 2Q tiles is one step per group).  The tiles of a step share
 // one wait, one cross-wave reduction and one epilogue, and every weight
 // fragment is read once for both tiles.  Per step, wave w
-//   1. requests the child-state fragments of its recurrent columns
+//   1. contracts input columns [32w, 32w+32) (requested one step earlier;
+//      they depend on no child), and between the MFMA steps of the second
+//      half requests the child-state fragments of its recurrent columns
 //      [64w, 64w+64) of [h(slot 0) | h(slot 1)] for every row of the step,
-//   2. contracts input columns [32w, 32w+32) (requested one step earlier;
-//      they depend on no child) while those loads are in flight,
-//   3. requests the next step's input fragments,
-//   4. waits until every fragment it read carries this launch's tag,
-//   5. contracts the recurrent columns;
+//   2. requests the next step's input fragments,
+//   3. waits until every fragment it read carries this launch's tag,
+//   4. contracts the recurrent columns;
 // the eight partial sums then meet in LDS and the workgroup applies tanh and
-// writes the step's rows.  At entry each workgroup lists its steps of every
+// writes the step's rows.  The next step's input fragments are complete
+// before the stores are issued, so no wait of the next step covers them.  At entry each workgroup lists its steps of every
 // level with their operand sources in LDS, so the level loop never goes back
 // to the linearization in memory; a group whose list does not fit walks the
 // levels instead, staging one step's sources at a time.
@@ -1415,11 +1416,13 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   int gave_up = 0;
 
   // input fragments of a step's rows (tile t, row i16): x[node][xcol + 16 b + 4 g4 .. +3]
-  auto issue_x = [&](const int *st, u32x4 (&xv)[MT][NBX]) __attribute__((always_inline)) {
+  // (live false: every load reads zeros, so a step without a successor still
+  // issues the same loads and the waits after them keep fixed counts)
+  auto issue_x = [&](const int *st, u32x4 (&xv)[MT][NBX], bool live) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       const int base = st[2 + t];
-      const int xc = (base >= 0 && base + i16 < st[4]) ? st[kDagStepHead + (t * kTileM + i16) * 3] : -1;
+      const int xc = (live && base >= 0 && base + i16 < st[4]) ? st[kDagStepHead + (t * kTileM + i16) * 3] : -1;
       const uint32_t xo = xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 4 * g4) * 4) : kNoSource;
 #pragma unroll
       for (int b = 0; b < NBX; ++b) xv[t][b] = xin.load4(xo + 64u * b);
@@ -1435,24 +1438,20 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     const bool two = st[3] >= 0;
     Frag hv[MT][NBR];
     int cr[MT];
-    // 1. child-state fragments of every row of the step, requested halfway
-    //    through the input part rather than at the start: a level's children
-    //    are written at the end of the previous level, about when this step
-    //    begins, so pairs read at once would mostly still carry old tags
-    auto issue_h = [&]() __attribute__((always_inline)) {
+    uint32_t ho[MT];
 #pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        const int base = st[2 + t];
-        cr[t] = (base >= 0 && base + i16 < lend) ? st[kDagStepHead + (t * kTileM + i16) * 3 + 1 + rslot] : -1;
-        const uint32_t ho = cr[t] >= 0 ? (uint32_t)(cr[t] * H + rcol + 4 * g4) * 8u : kNoSource;
-#pragma unroll
-        for (int b = 0; b < NBR; ++b) {
-          hv[t][b].lo = hs.load2_at(ho + 128u * b);
-          hv[t][b].hi = hs.load2_at(ho + 128u * b + 16u);
-        }
-      }
-    };
-    // 2. input part; one weight fragment serves both tiles
+    for (int t = 0; t < MT; ++t) {
+      const int base = st[2 + t];
+      cr[t] = (base >= 0 && base + i16 < lend) ? st[kDagStepHead + (t * kTileM + i16) * 3 + 1 + rslot] : -1;
+      ho[t] = cr[t] >= 0 ? (uint32_t)(cr[t] * H + rcol + 4 * g4) * 8u : kNoSource;
+    }
+    // 1. input part; one weight fragment serves both tiles.  The
+    // child-state fragments of every row of the step are requested during
+    // its second half, one block per MFMA step of each tile, rather than at
+    // the start (a level's children are written at the end of the previous
+    // level, about when this step begins, so pairs read at once would mostly
+    // still carry old tags) and rather than in one burst, which would hold
+    // the MFMAs behind it until the address unit has taken every load.
     floatx4 acc[MT][NT];
 #pragma unroll
     for (int t = 0; t < MT; ++t)
@@ -1464,18 +1463,30 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       float4 wv[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) wv[nt] = *(const float4 *)(bx + nt * 16 * LDX + 16 * b);
-      mfma_k16_xn<NT>(as_float4(xc[0][b]), wv, acc[0]);
-      if (two) mfma_k16_xn<NT>(as_float4(xc[1][b]), wv, acc[1]);
-      if (b == NBX / 2 - 1) issue_h();
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        mfma_kstep_xn<NT>(k, as_float4(xc[0][b]), wv, acc[0]);
+        if (two) mfma_kstep_xn<NT>(k, as_float4(xc[1][b]), wv, acc[1]);
+        if (b == NBX - 1) {
+          static_assert(NBR == 4, "one child block per MFMA step");
+          hv[0][k].lo = hs.load2_at(ho[0] + 128u * k);
+          hv[0][k].hi = hs.load2_at(ho[0] + 128u * k + 16u);
+          if (two) {
+            hv[1][k].lo = hs.load2_at(ho[1] + 128u * k);
+            hv[1][k].hi = hs.load2_at(ho[1] + 128u * k + 16u);
+          }
+        }
+      }
     }
-    // 3. the next step's input fragments, in flight through this step
-    if (nst) issue_x(nst, xn);
+    // 2. the next step's input fragments, in flight through this step
+    issue_x(nst ? nst : st, xn, nst != nullptr);
     CORTEX_TRACE_POINT(l, 1);
-    // 4. wait for the children
+    // 3. wait for the children
     auto ready = [&]() __attribute__((always_inline)) -> bool {
       bool r = true;
 #pragma unroll
       for (int t = 0; t < MT; ++t) {
+        if (t > 0 && !two) break;
         bool rt = true;
 #pragma unroll
         for (int b = 0; b < NBR; ++b) rt = rt && hv[t][b].ready(tag);
@@ -1491,7 +1502,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
         for (int t = 0; t < MT; ++t)
 #pragma unroll
           for (int b = 0; b < NBR; ++b) {
-            if (cr[t] >= 0 && !hv[t][b].ready(tag)) {
+            if ((t == 0 || two) && cr[t] >= 0 && !hv[t][b].ready(tag)) {
               const uint32_t so = (uint32_t)(cr[t] * H + rcol + 16 * b + 4 * g4) * 8u;
               hv[t][b].lo = hs.load2_at(so);
               hv[t][b].hi = hs.load2_at(so + 16u);
@@ -1511,13 +1522,19 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       }
     }
     CORTEX_TRACE_POINT(l, 2);
-    // 5. recurrent part
+    // 4. recurrent part
 #pragma unroll
     for (int b = 0; b < NBR; ++b) {
       mfma_k16_xn<NT>(hv[0][b].value(true), wr[b], acc[0]);
       if (two) mfma_k16_xn<NT>(hv[1][b].value(true), wr[b], acc[1]);
     }
     CORTEX_TRACE_WAVE(l);
+    // the next step's input fragments are complete before this step's stores
+    // are issued, so its first contraction does not wait for the stores
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int b = 0; b < NBX; ++b) settle(xn[t][b]);
 #pragma unroll
     for (int t = 0; t < MT; ++t)
       if (t == 0 || two)
@@ -1561,7 +1578,13 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     auto step = [&](int e) __attribute__((always_inline)) -> const int * { return &list[e * SI]; };
     // two steps per iteration, written out, so each step's input fragments
     // stay in fixed registers (xa, xb) rather than being selected at run time
-    if (total > 0) issue_x(step(0), xa);
+    if (total > 0) {
+      issue_x(step(0), xa, true);
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int b = 0; b < NBX; ++b) settle(xa[t][b]);
+    }
     for (int e = 0; e < total; e += 2) {
       CORTEX_TRACE_POINT(step(e)[0], 0);
       if (run_step(step(e), xa, e + 1 < total ? step(e + 1) : nullptr, xb)) return;
@@ -1598,7 +1621,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
           raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
           return;
         }
-        issue_x(st, xa);
+        issue_x(st, xa, true);
         if (run_step(st, xa, nullptr, xb)) return;
       }
       CORTEX_TRACE_POINT(l, 5);
