@@ -1214,12 +1214,12 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
 // one wait, one cross-wave reduction and one epilogue, and every weight
 // fragment is read once for both tiles.  Per step, wave w
 //   1. contracts input columns [32w, 32w+32) (requested one step earlier;
-//      they depend on no child), and between the MFMA steps of the second
-//      half requests the child-state fragments of its recurrent columns
+//      they depend on no child); between the MFMA steps of the first half it
+//      requests the next step's input fragments, and between those of the
+//      second half the child-state fragments of its recurrent columns
 //      [64w, 64w+64) of [h(slot 0) | h(slot 1)] for every row of the step,
-//   2. requests the next step's input fragments,
-//   3. waits until every fragment it read carries this launch's tag,
-//   4. contracts the recurrent columns;
+//   2. waits until every fragment it read carries this launch's tag,
+//   3. contracts the recurrent columns;
 // the eight partial sums then meet in LDS and the workgroup applies tanh and
 // writes the step's rows.  The next step's input fragments are complete
 // before the stores are issued, so no wait of the next step covers them.  At entry each workgroup lists its steps of every
@@ -1308,7 +1308,9 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   constexpr int KX = H / kFwdWaves, NBX = KX / 16;          // input columns per wave, 16-blocks
   constexpr int KR = 2 * H / kFwdWaves, NBR = KR / 16;      // recurrent columns per wave, 16-blocks
   constexpr int LDX = H + 4;                                // W row stride in LDS
-  constexpr int LDC = J + 4;                                // partial-sum row stride
+  // partial sums: C_s[wave][tile][column][16 rows], the four 16-byte row
+  // quarters of column c stored in the order q ^ ((c >> 2) & 3), so the
+  // 16-byte accesses of 16 consecutive columns meet 64 distinct banks
   constexpr int MT = kDagStepTiles;
   constexpr int SI = kDagStepInts;
   constexpr int EPI = MT * kTileM * J / kFwdThreads;        // outputs per thread per full step
@@ -1316,7 +1318,8 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   static_assert(KR == 64 && H % KR == 0, "a wave's recurrent columns lie in one child slot");
 
   __shared__ __attribute__((aligned(16))) float Wx_s[J * LDX];
-  __shared__ __attribute__((aligned(16))) float C_s[kFwdWaves * MT * kTileM * LDC];
+  __shared__ __attribute__((aligned(16))) float C_s[kFwdWaves * MT * J * kTileM];
+  __shared__ int stop_s;
   __shared__ float bias_s[J];
   __shared__ int wsum[kFwdWaves + 1];
   extern __shared__ int list[];               // [kDagStepCap][kDagStepInts]
@@ -1358,6 +1361,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       v[k] = *(const float4 *)(a.W + (size_t)(hbase + idx / (H / 4)) * H + 4 * (idx % (H / 4)));
     }
     if (tid < J) bias_s[tid] = a.b[hbase + tid];
+    if (tid == 0) stop_s = 0;
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int idx = tid + k * kFwdThreads;
@@ -1418,15 +1422,21 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   // input fragments of a step's rows (tile t, row i16): x[node][xcol + 16 b + 4 g4 .. +3]
   // (live false: every load reads zeros, so a step without a successor still
   // issues the same loads and the waits after them keep fixed counts)
-  auto issue_x = [&](const int *st, u32x4 (&xv)[MT][NBX], bool live) __attribute__((always_inline)) {
+  auto x_offsets = [&](const int *st, bool live, uint32_t (&xo)[MT]) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       const int base = st[2 + t];
       const int xc = (live && base >= 0 && base + i16 < st[4]) ? st[kDagStepHead + (t * kTileM + i16) * 3] : -1;
-      const uint32_t xo = xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 4 * g4) * 4) : kNoSource;
-#pragma unroll
-      for (int b = 0; b < NBX; ++b) xv[t][b] = xin.load4(xo + 64u * b);
+      xo[t] = xc <= -2 ? (uint32_t)(((-2 - xc) * H + xcol + 4 * g4) * 4) : kNoSource;
     }
+  };
+  auto issue_x = [&](const int *st, u32x4 (&xv)[MT][NBX], bool live) __attribute__((always_inline)) {
+    uint32_t xo[MT];
+    x_offsets(st, live, xo);
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int b = 0; b < NBX; ++b) xv[t][b] = xin.load4(xo[t] + 64u * b);
   };
 
   // One step.  xc: its input fragments (requested earlier); nst: the next
@@ -1445,13 +1455,16 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       cr[t] = (base >= 0 && base + i16 < lend) ? st[kDagStepHead + (t * kTileM + i16) * 3 + 1 + rslot] : -1;
       ho[t] = cr[t] >= 0 ? (uint32_t)(cr[t] * H + rcol + 4 * g4) * 8u : kNoSource;
     }
-    // 1. input part; one weight fragment serves both tiles.  The
-    // child-state fragments of every row of the step are requested during
-    // its second half, one block per MFMA step of each tile, rather than at
-    // the start (a level's children are written at the end of the previous
-    // level, about when this step begins, so pairs read at once would mostly
-    // still carry old tags) and rather than in one burst, which would hold
-    // the MFMAs behind it until the address unit has taken every load.
+    uint32_t xo_next[MT];
+    x_offsets(nst ? nst : st, nst != nullptr, xo_next);
+    // 1. input part; one weight fragment serves both tiles.  The next step's
+    // input fragments are requested during its first half and the
+    // child-state fragments of every row of this step during its second
+    // half, one load or one block per MFMA step, rather than in bursts, which
+    // would hold the MFMAs behind them until the address unit has taken every
+    // load.  The child fragments are not requested at the start: a level's
+    // children are written at the end of the previous level, about when this
+    // step begins, so pairs read at once would mostly still carry old tags.
     floatx4 acc[MT][NT];
 #pragma unroll
     for (int t = 0; t < MT; ++t)
@@ -1467,6 +1480,10 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       for (int k = 0; k < 4; ++k) {
         mfma_kstep_xn<NT>(k, as_float4(xc[0][b]), wv, acc[0]);
         if (two) mfma_kstep_xn<NT>(k, as_float4(xc[1][b]), wv, acc[1]);
+        if (b == 0) {
+          static_assert(MT * NBX == 4, "one next-step input load per MFMA step");
+          xn[k / NBX][k % NBX] = xin.load4(xo_next[k / NBX] + 64u * (k % NBX));
+        }
         if (b == NBX - 1) {
           static_assert(NBR == 4, "one child block per MFMA step");
           hv[0][k].lo = hs.load2_at(ho[0] + 128u * k);
@@ -1478,10 +1495,8 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
         }
       }
     }
-    // 2. the next step's input fragments, in flight through this step
-    issue_x(nst ? nst : st, xn, nst != nullptr);
     CORTEX_TRACE_POINT(l, 1);
-    // 3. wait for the children
+    // 2. wait for the children
     auto ready = [&]() __attribute__((always_inline)) -> bool {
       bool r = true;
 #pragma unroll
@@ -1520,9 +1535,10 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
           break;
         }
       }
+      if (gave_up) stop_s = 1;             // read by every wave after the next barrier
     }
     CORTEX_TRACE_POINT(l, 2);
-    // 4. recurrent part
+    // 3. recurrent part
 #pragma unroll
     for (int b = 0; b < NBR; ++b) {
       mfma_k16_xn<NT>(hv[0][b].value(true), wr[b], acc[0]);
@@ -1539,37 +1555,47 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     for (int t = 0; t < MT; ++t)
       if (t == 0 || two)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int v = 0; v < 4; ++v)
-            C_s[((wave * MT + t) * kTileM + 4 * g4 + v) * LDC + nt * 16 + i16] = acc[t][nt][v];
+        for (int nt = 0; nt < NT; ++nt) {
+          const int c = nt * 16 + i16;
+          *(floatx4 *)&C_s[((wave * MT + t) * J + c) * kTileM + 4 * (g4 ^ ((c >> 2) & 3))] = acc[t][nt];
+        }
     __syncthreads();
     CORTEX_TRACE_POINT(l, 3);
-    // every output of the thread first, then the stores: a store's data
-    // registers are not reused while earlier stores are in flight
-    const int outs = (two ? MT : 1) * kTileM * J;
+    if (stop_s) return true;               // a wave gave up its wait: every wave stops here
+    // epilogue: thread (unit j, row quarter q of tile t) sums the eight
+    // partial sums of four rows, bias first, and writes them; every output of
+    // the thread first, then the stores (a store's data registers are not
+    // reused while earlier stores are in flight)
+    static_assert(EPI == 4 && kFwdThreads == J * MT * 4, "one row quarter of one tile per thread");
+    const int j = tid & (J - 1), t = tid / (J * 4), q = (tid / J) & 3;
+    const bool live_t = t == 0 || two;
+    floatx4 sum = floatx4{bias_s[j], bias_s[j], bias_s[j], bias_s[j]};
+    if (live_t) {
+#pragma unroll
+      for (int w = 0; w < kFwdWaves; ++w) {
+        const floatx4 p = *(const floatx4 *)&C_s[((w * MT + t) * J + j) * kTileM + 4 * (q ^ ((j >> 2) & 3))];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sum[v] += p[v];
+      }
+    }
     float hv_out[EPI];
     uint32_t el[EPI];
 #pragma unroll
-    for (int e = 0; e < EPI; ++e) {
-      const int p = tid + e * kFwdThreads;
-      const int t = p / (kTileM * J), i = (p / J) % kTileM, j = p % J;
-      const int row = st[2 + t] + i;
-      float sum = bias_s[j];
-#pragma unroll
-      for (int w = 0; w < kFwdWaves; ++w) sum += C_s[((w * MT + t) * kTileM + i) * LDC + j];
-      hv_out[e] = tanh_f(sum);
-      el[e] = (p < outs && row < lend) ? (uint32_t)(row * H + hbase + j) : 0xFFFFFFFFu;
+    for (int v = 0; v < EPI; ++v) {
+      const int row = st[2 + (t & 1)] + 4 * q + v;
+      hv_out[v] = tanh_f(sum[v]);
+      el[v] = (live_t && row < lend) ? (uint32_t)(row * H + hbase + j) : 0xFFFFFFFFu;
     }
 #pragma unroll
-    for (int e = 0; e < EPI; ++e) {
-      if (el[e] != 0xFFFFFFFFu) {
-        hs.store1(el[e], hv_out[e], tag);
-        a.h[el[e]] = hv_out[e];
+    for (int v = 0; v < EPI; ++v) {
+      if (el[v] != 0xFFFFFFFFu) {
+        hs.store1(el[v], hv_out[v], tag);
+        a.h[el[v]] = hv_out[v];
       }
     }
     CORTEX_TRACE_POINT(l, 4);
-    return __syncthreads_or(gave_up) != 0;
+    __syncthreads();                       // C_s is written again by the next step
+    return false;
   };
 
   u32x4 xa[MT][NBX], xb[MT][NBX];
