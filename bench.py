@@ -309,10 +309,12 @@ def ablation(args):
     after every level, or one launch per level that reloads weights and
     structure each time; for the TreeGRU cells also a barrier after each of
     the level's two exchanges (the schedule without recursive refactoring,
-    Secs. 3.1 and 7.4).  Then, on the N-ary TreeLSTM and TreeFC batches, the
-    optimizations of Sec. 7.3 switched off (CORTEX_KNOB_ABLATE): model
-    persistence, leaf specialization, both, and both with one launch per
-    level.  One JSON line per (workload, mode): the forward kernel time (for
+    Secs. 3.1 and 7.4); for the 64-grid DAG-RNN also the input products
+    hoisted into one matrix product before the level loop (ABLATE bit 2)
+    instead of fused into each tile.  Then, on the N-ary TreeLSTM and TreeFC
+    batches, the optimizations of Sec. 7.3 switched off (CORTEX_KNOB_ABLATE):
+    model persistence, leaf specialization, both, and both with one launch
+    per level.  One JSON line per (workload, mode): the forward kernel time (for
     mode 2, the whole per-level launch sequence, which also synchronizes once
     to read L), the median of five rounds in which every schedule of a
     workload is timed once."""
@@ -332,13 +334,18 @@ def ablation(args):
     for wl, units in cases:
         for mode in ((0, 1, 3, 2) if wl.cell in (I.CELL_CHILDSUM_TREEGRU, I.CELL_SIMPLE_TREEGRU) else (0, 1, 2)):
             runs.append((wl, units, mode, 0))
+        if wl.cell == I.CELL_DAGRNN:
+            # the input products hoisted into one matrix product ahead of the
+            # level loop (Sec. 7.1), against the fused input part
+            runs.append((wl, units, 0, 4))
     # optimizations switched off one at a time, then all with one launch per
     # level (Sec. 7.3): model persistence (bit 0), leaf specialization (bit 1)
     for wl in (I.make_workload(1), I.treefc_workload(I.BASE_SEED + 61, batch=10, H=256)):
         for mode, bits in ((0, 0), (0, 1), (0, 2), (0, 3), (2, 3)):
             runs.append((wl, 0, mode, bits))
     abl_names = {0: "", 1: "; weights read from memory at every tile", 2: "; leaf states staged and waited for",
-                 3: "; weights from memory and leaf states staged"}
+                 3: "; weights from memory and leaf states staged",
+                 4: "; input products hoisted into one matrix product before the level loop"}
     def knobs(units, mode, bits):
         C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, units)
         C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, mode)

@@ -339,10 +339,18 @@ int cortex_dag_infer(int32_t H, const int32_t *d_children, const cortex_lin_t *l
  *                                   wait for them instead of reading the
  *                                   inputs directly.  Slice kernels only
  *                                   (TreeRNN at H = 256 / 512, N-ary TreeLSTM;
- *                                   bit 0 also DAG-RNN with 16-unit slices);
- *                                   other forwards return CORTEX_E_INVAL.
+ *                                   bit 0 also DAG-RNN with 16-unit slices).
+ *                                   Bit 2 = input products hoisted (Sec. 7.1):
+ *                                   W x + b of every node is computed by one
+ *                                   matrix-product launch before the level
+ *                                   loop (into d_h, which the loop then
+ *                                   overwrites) instead of inside each tile;
+ *                                   DAG-RNN with 64-unit slices only, results
+ *                                   equal to rounding.  Other forwards return
+ *                                   CORTEX_E_INVAL.
  * cortex_set_knob returns CORTEX_E_INVAL for an unknown knob or a negative value
- * (or a LEVEL_SYNC or ABLATE value above 3, a TREE_UNROLL value above 2).
+ * (or a LEVEL_SYNC value above 3, an ABLATE value above 7, a TREE_UNROLL
+ * value above 2).
  */
 #define CORTEX_KNOB_LIN_BLOCKS 0
 #define CORTEX_KNOB_FWD_NODE_GROUPS 1

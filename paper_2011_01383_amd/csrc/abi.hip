@@ -73,7 +73,7 @@ extern "C" int cortex_set_knob(int32_t which, int64_t value) {
   if (which < 0 || which >= cortex::kKnobs || value < 0) return CORTEX_E_INVAL;
   if (which == CORTEX_KNOB_LEVEL_SYNC && value > 3) return CORTEX_E_INVAL;
   if (which == CORTEX_KNOB_TREE_UNROLL && value > 2) return CORTEX_E_INVAL;
-  if (which == CORTEX_KNOB_ABLATE && value > 3) return CORTEX_E_INVAL;
+  if (which == CORTEX_KNOB_ABLATE && value > 7) return CORTEX_E_INVAL;
   cortex::g_knobs[which].store(value);
   return CORTEX_OK;
 }

@@ -99,6 +99,7 @@ struct FwdArgs {
   int32_t ablate;               // slice kernel, for ablation studies: bit 0 (its own instance) reads the weight slice from
                                 // memory at every tile instead of LDS; bit 1 stages the leaf states and
                                 // has parents wait for them instead of reading their inputs directly
+  float *pre;                   // DAG-RNN with hoisted input products: W x + b of every row, [N][H] in row order
 };
 
 // ---------------------------------------------------------------------------
@@ -1303,6 +1304,73 @@ __device__ __forceinline__ bool dag_fill_codes(const FwdArgs &a, int *st, int sl
   return ok;
 }
 
+// Hoisted input products of the DAG-RNN at H = 256 (the ablation of the
+// fused input part; Sec. 7.1 computes them with one matrix product before the
+// recursion): pre[r][u] = sum_k x[node(r)][k] W[u][k] + b[u] for every row r,
+// in row order.  Workgroup (row block m, slice s) computes rows
+// [128m, 128m + 128) x units [64s, 64s + 64): each wave 16 rows, its input
+// fragments in registers, the slice of W in LDS, fp32 MFMA.  With a grid that
+// is a multiple of 32, the four slices of a row block are workgroups
+// 32m' + r + 8s (m = 8m' + r), which round-robin dispatch places on one XCD.
+__global__ void __launch_bounds__(kFwdThreads) dag_input_gemm_kernel(FwdArgs a) {
+  constexpr int H = kDagH, J = kDagJ, NT = J / 16, NB = H / 16, LDX = H + 4;
+  __shared__ __attribute__((aligned(16))) float W_s[J * LDX];
+  __shared__ float bias_s[J];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int bid = blockIdx.x;
+  const bool xcd_map = (gridDim.x & 31) == 0;
+  const int slice = xcd_map ? ((bid >> 3) & 3) : bid % kDagS;
+  const int block = xcd_map ? ((bid & 7) + 8 * (bid >> 5)) : bid / kDagS;
+  const int N = a.N, hbase = slice * J;
+  const int r0 = block * (kFwdWaves * kTileM);
+  if (r0 >= N || load_status(a.status) != 0) return;
+  // input fragments of row r0 + 16 wave + i16: x[node][16 b + 4 g4 .. +3]
+  const int r = r0 + kTileM * wave + i16;
+  const int v = r < N ? a.level_nodes[r] : -1;
+  const InBuf xin(a.x, (uint32_t)N * H * 4);
+  const uint32_t xo = (v >= 0 && v < N) ? (uint32_t)(v * H + 4 * g4) * 4u : kNoSource;
+  u32x4 xf[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) xf[b] = xin.load4(xo + 64u * b);
+  {
+    constexpr int PER = J * H / 4 / kFwdThreads;
+    float4 w[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      w[k] = *(const float4 *)(a.W + (size_t)(hbase + idx / (H / 4)) * H + 4 * (idx % (H / 4)));
+    }
+    if (tid < J) bias_s[tid] = a.b[hbase + tid];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      *(float4 *)&W_s[(idx / (H / 4)) * LDX + 4 * (idx % (H / 4))] = w[k];
+    }
+  }
+  __syncthreads();
+  floatx4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const float *bx = &W_s[i16 * LDX + 4 * g4];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    float4 wv[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) wv[nt] = *(const float4 *)(bx + nt * 16 * LDX + 16 * b);
+    mfma_k16_xn<NT>(as_float4(xf[b]), wv, acc);
+  }
+  // lane (i16, g4) holds rows 4 g4 .. 4 g4 + 3 of the wave's 16, column 16 nt + i16
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = r0 + kTileM * wave + 4 * g4 + e;
+      if (row < N) a.pre[(size_t)row * H + hbase + 16 * nt + i16] = acc[nt][e] + bias_s[16 * nt + i16];
+    }
+}
+
+template <bool kHoisted>
 __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   constexpr int H = kDagH, J = kDagJ, NT = J / 16;
   constexpr int KX = H / kFwdWaves, NBX = KX / 16;          // input columns per wave, 16-blocks
@@ -1317,7 +1385,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   static_assert(NBX * 16 == KX && NBR * 16 == KR && EPI * kFwdThreads == MT * kTileM * J, "tiling");
   static_assert(KR == 64 && H % KR == 0, "a wave's recurrent columns lie in one child slot");
 
-  __shared__ __attribute__((aligned(16))) float Wx_s[J * LDX];
+  __shared__ __attribute__((aligned(16))) float Wx_s[kHoisted ? 4 : J * LDX];
   __shared__ __attribute__((aligned(16))) float C_s[kFwdWaves * MT * J * kTileM];
   __shared__ int stop_s;
   __shared__ float bias_s[J];
@@ -1335,7 +1403,8 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   const int N = a.N;
   const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
   const TagBuf hs(a.hs, (uint32_t)N * H * 8);
-  const InBuf xin(a.x, (uint32_t)N * H * 4);
+  const InBuf xin(a.x, kHoisted ? 0u : (uint32_t)N * H * 4);
+  const InBuf pin(a.pre, kHoisted ? (uint32_t)N * H * 4 : 0u);
   const int rslot = wave >> 2;                 // child slot of this wave's recurrent columns
   const int rcol = KR * (wave & 3);            // their first column within that child's h
   const int xcol = KX * wave;                  // this wave's first input column
@@ -1352,7 +1421,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
       wr[b][nt] = *(const float4 *)(a.U + ((size_t)rslot * H + hbase + 16 * nt + i16) * H + rcol + 16 * b + 4 * g4);
-  {
+  if constexpr (!kHoisted) {
     constexpr int ITEMS = J * H / 4, PER = ITEMS / kFwdThreads;
     float4 v[PER];
 #pragma unroll
@@ -1361,13 +1430,13 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       v[k] = *(const float4 *)(a.W + (size_t)(hbase + idx / (H / 4)) * H + 4 * (idx % (H / 4)));
     }
     if (tid < J) bias_s[tid] = a.b[hbase + tid];
-    if (tid == 0) stop_s = 0;
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int idx = tid + k * kFwdThreads;
       *(float4 *)&Wx_s[(idx / (H / 4)) * LDX + 4 * (idx % (H / 4))] = v[k];
     }
   }
+  if (tid == 0) stop_s = 0;
   if (status0 != 0) return;
   if (L < 1 || L > N) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
@@ -1455,42 +1524,67 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       cr[t] = (base >= 0 && base + i16 < lend) ? st[kDagStepHead + (t * kTileM + i16) * 3 + 1 + rslot] : -1;
       ho[t] = cr[t] >= 0 ? (uint32_t)(cr[t] * H + rcol + 4 * g4) * 8u : kNoSource;
     }
-    uint32_t xo_next[MT];
-    x_offsets(nst ? nst : st, nst != nullptr, xo_next);
-    // 1. input part; one weight fragment serves both tiles.  The next step's
-    // input fragments are requested during its first half and the
-    // child-state fragments of every row of this step during its second
-    // half, one load or one block per MFMA step, rather than in bursts, which
-    // would hold the MFMAs behind them until the address unit has taken every
-    // load.  The child fragments are not requested at the start: a level's
-    // children are written at the end of the previous level, about when this
-    // step begins, so pairs read at once would mostly still carry old tags.
     floatx4 acc[MT][NT];
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[t][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const float *bx = &Wx_s[i16 * LDX + xcol + 4 * g4];
+    float pv[4];                             // hoisted: W x + b of the thread's four outputs
+    if constexpr (kHoisted) {
+      // 1. (hoisted) the step's input products, computed before the level
+      // loop, for the epilogue's four outputs of this thread, then every
+      // child-state fragment of the step at once: there is no input part to
+      // place them in
+      const int j = tid & (J - 1), t = tid / (J * 4), q = (tid / J) & 3;
+      const bool live_t = t == 0 || two;
 #pragma unroll
-    for (int b = 0; b < NBX; ++b) {
-      float4 wv[NT];
+      for (int v = 0; v < 4; ++v) {
+        const int row = st[2 + (t & 1)] + 4 * q + v;
+        pv[v] = as_float(pin.load1((live_t && row < lend) ? (uint32_t)(row * H + hbase + j) * 4u : kNoSource));
+      }
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) wv[nt] = *(const float4 *)(bx + nt * 16 * LDX + 16 * b);
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        mfma_kstep_xn<NT>(k, as_float4(xc[0][b]), wv, acc[0]);
-        if (two) mfma_kstep_xn<NT>(k, as_float4(xc[1][b]), wv, acc[1]);
-        if (b == 0) {
-          static_assert(MT * NBX == 4, "one next-step input load per MFMA step");
-          xn[k / NBX][k % NBX] = xin.load4(xo_next[k / NBX] + 64u * (k % NBX));
+      for (int k = 0; k < NBR; ++k) {
+        hv[0][k].lo = hs.load2_at(ho[0] + 128u * k);
+        hv[0][k].hi = hs.load2_at(ho[0] + 128u * k + 16u);
+        if (two) {
+          hv[1][k].lo = hs.load2_at(ho[1] + 128u * k);
+          hv[1][k].hi = hs.load2_at(ho[1] + 128u * k + 16u);
         }
-        if (b == NBX - 1) {
-          static_assert(NBR == 4, "one child block per MFMA step");
-          hv[0][k].lo = hs.load2_at(ho[0] + 128u * k);
-          hv[0][k].hi = hs.load2_at(ho[0] + 128u * k + 16u);
-          if (two) {
-            hv[1][k].lo = hs.load2_at(ho[1] + 128u * k);
-            hv[1][k].hi = hs.load2_at(ho[1] + 128u * k + 16u);
+      }
+    } else {
+      uint32_t xo_next[MT];
+      x_offsets(nst ? nst : st, nst != nullptr, xo_next);
+      // 1. input part; one weight fragment serves both tiles.  The next
+      // step's input fragments are requested during its first half and the
+      // child-state fragments of every row of this step during its second
+      // half, one load or one block per MFMA step, rather than in bursts,
+      // which would hold the MFMAs behind them until the address unit has
+      // taken every load.  The child fragments are not requested at the
+      // start: a level's children are written at the end of the previous
+      // level, about when this step begins, so pairs read at once would
+      // mostly still carry old tags.
+      const float *bx = &Wx_s[i16 * LDX + xcol + 4 * g4];
+#pragma unroll
+      for (int b = 0; b < NBX; ++b) {
+        float4 wv[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) wv[nt] = *(const float4 *)(bx + nt * 16 * LDX + 16 * b);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          mfma_kstep_xn<NT>(k, as_float4(xc[0][b]), wv, acc[0]);
+          if (two) mfma_kstep_xn<NT>(k, as_float4(xc[1][b]), wv, acc[1]);
+          if (b == 0) {
+            static_assert(MT * NBX == 4, "one next-step input load per MFMA step");
+            xn[k / NBX][k % NBX] = xin.load4(xo_next[k / NBX] + 64u * (k % NBX));
+          }
+          if (b == NBX - 1) {
+            static_assert(NBR == 4, "one child block per MFMA step");
+            hv[0][k].lo = hs.load2_at(ho[0] + 128u * k);
+            hv[0][k].hi = hs.load2_at(ho[0] + 128u * k + 16u);
+            if (two) {
+              hv[1][k].lo = hs.load2_at(ho[1] + 128u * k);
+              hv[1][k].hi = hs.load2_at(ho[1] + 128u * k + 16u);
+            }
           }
         }
       }
@@ -1547,10 +1641,11 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     CORTEX_TRACE_WAVE(l);
     // the next step's input fragments are complete before this step's stores
     // are issued, so its first contraction does not wait for the stores
+    if constexpr (!kHoisted)
 #pragma unroll
-    for (int t = 0; t < MT; ++t)
+      for (int t = 0; t < MT; ++t)
 #pragma unroll
-      for (int b = 0; b < NBX; ++b) settle(xn[t][b]);
+        for (int b = 0; b < NBX; ++b) settle(xn[t][b]);
 #pragma unroll
     for (int t = 0; t < MT; ++t)
       if (t == 0 || two)
@@ -1569,7 +1664,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     static_assert(EPI == 4 && kFwdThreads == J * MT * 4, "one row quarter of one tile per thread");
     const int j = tid & (J - 1), t = tid / (J * 4), q = (tid / J) & 3;
     const bool live_t = t == 0 || two;
-    floatx4 sum = floatx4{bias_s[j], bias_s[j], bias_s[j], bias_s[j]};
+    floatx4 sum = kHoisted ? floatx4{pv[0], pv[1], pv[2], pv[3]} : floatx4{bias_s[j], bias_s[j], bias_s[j], bias_s[j]};
     if (live_t) {
 #pragma unroll
       for (int w = 0; w < kFwdWaves; ++w) {
@@ -1604,7 +1699,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     auto step = [&](int e) __attribute__((always_inline)) -> const int * { return &list[e * SI]; };
     // two steps per iteration, written out, so each step's input fragments
     // stay in fixed registers (xa, xb) rather than being selected at run time
-    if (total > 0) {
+    if (!kHoisted && total > 0) {
       issue_x(step(0), xa, true);
 #pragma unroll
       for (int t = 0; t < MT; ++t)
@@ -1647,7 +1742,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
           raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
           return;
         }
-        issue_x(st, xa, true);
+        if constexpr (!kHoisted) issue_x(st, xa, true);
         if (run_step(st, xa, nullptr, xb)) return;
       }
       CORTEX_TRACE_POINT(l, 5);
@@ -3106,7 +3201,9 @@ static bool pick(int cell, int H, int32_t N, bool cached, Instance &out) {
   // tile's contraction is 4x shorter, and small levels are latency-bound);
   // the knob forces either (16 or 64)
   if (cell == CELL_DAG && H == kDagH && (units == 64 || (units != 16 && N >= kDagWideMinRows))) {
-    out.fn = dag_slice64_kernel;
+    // ablation bit 2: the input products hoisted into dag_input_gemm_kernel
+    out.fn = (knob(CORTEX_KNOB_ABLATE) & 4) ? dag_slice64_kernel<true> : dag_slice64_kernel<false>;
+    out.ablate_bits = 4;
     out.J = kDagJ;
     out.threads = kFwdThreads;
     out.lds = kDagListBytes;
@@ -3355,6 +3452,18 @@ static int launch_forward(int cell, int H, const cortex_lin_t *lin, FwdArgs &a, 
   }
   a.ablate = (int32_t)ablate;
   set_last_grid(1, (int32_t)G);
+  if (ablate & 4) {
+    // hoisted input products: W x + b of every row goes to the output rows
+    // first; the level loop reads each element there just before it writes
+    // the element's state (the same thread, so no other ordering is needed)
+    a.pre = a.h;
+    const int blocks = (int)(((int64_t)lin->num_nodes + kFwdWaves * kTileM - 1) / (kFwdWaves * kTileM));
+    const int grid = (blocks * kDagS + 31) / 32 * 32;
+    void *kargs[] = {(void *)&a};
+    if (grid > 0 && hipLaunchKernel((const void *)dag_input_gemm_kernel, dim3(grid), dim3(kFwdThreads), kargs, 0,
+                                    (hipStream_t)stream) != hipSuccess)
+      return CORTEX_E_HIP;
+  }
   if (sync_mode == 1) a.level_barrier = 1;
   if (sync_mode == 3) a.level_barrier = 2;
   if (fused_children) {

@@ -89,8 +89,8 @@ def test_level_sync_knob_range(lib):
 
 def test_ablate_knob_range(lib):
     assert C.cortex_get_knob(C.CORTEX_KNOB_ABLATE) == 0
-    assert C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 4) == C.CORTEX_E_INVAL
-    for v in (3, 2, 1, 0):
+    assert C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 8) == C.CORTEX_E_INVAL
+    for v in (7, 6, 5, 4, 3, 2, 1, 0):
         assert C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, v) == C.CORTEX_OK
         assert C.cortex_get_knob(C.CORTEX_KNOB_ABLATE) == v
 

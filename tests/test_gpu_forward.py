@@ -353,16 +353,19 @@ ABLATE_CASES = {
     "tree_rnn_h256": (lambda: I.tree_rnn_workload(41, n_leaves=37, H=256), 0, 3),
     "tree_rnn_h512": (lambda: I.tree_rnn_workload(49, n_leaves=23, H=512), 0, 3),
     "dag_h256_units16": (lambda: I.dagrnn_workload(42, n_grids=3, rows=9, cols=7, H=256), 16, 1),
+    "dag_h256_units64": (lambda: I.dagrnn_workload(43, n_grids=3, rows=9, cols=7, H=256), 64, 4),
 }
 
 
 @pytest.mark.parametrize("name", sorted(ABLATE_CASES))
-@pytest.mark.parametrize("bits", [1, 2, 3])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
 def test_ablations_change_only_the_schedule(name, bits):
     """Weights read from memory at every tile (bit 0) and leaf states staged
     and waited for (bit 1) feed the same values to the same contraction
-    order, so the states are bitwise identical; a kernel without the
-    ablation rejects it on the host."""
+    order, so the states are bitwise identical; the hoisted input products
+    (bit 2, DAG-RNN with 64-unit slices) add the same terms in another order,
+    so they meet the oracle only.  A kernel without the ablation rejects it
+    on the host."""
     make, units, supported = ABLATE_CASES[name]
     wl = make()
     announce("ablate %d %s N=%d" % (bits, name, wl.N))
@@ -382,8 +385,21 @@ def test_ablations_change_only_the_schedule(name, bits):
         C.cortex_set_knob(C.CORTEX_KNOB_LEVEL_SYNC, sync)
         got = run(wl).states_by_node()
         compare_states(got, oracle, "%s ablate %d level sync %d" % (name, bits, sync))
+        if bits & 4:
+            continue
         for key in ref:
             assert np.array_equal(ref[key], got[key]), (key, sync)
+
+
+def test_hoisted_input_products_full_grid():
+    """The 64-grid DAG-RNN batch with its input products hoisted into one
+    matrix product before the level loop (CORTEX_KNOB_ABLATE bit 2) against
+    the oracle, element by element."""
+    wl = I.make_workload(4)
+    announce("hoisted input products, %s N=%d" % (wl.name, wl.N))
+    C.cortex_set_knob(C.CORTEX_KNOB_ABLATE, 4)
+    got = run(wl).states_by_node()
+    compare_states(got, _oracle_of("w4", wl), "%s hoisted" % wl.name)
 
 
 @pytest.mark.parametrize("k", [0, 2, 3])
