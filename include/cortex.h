@@ -52,6 +52,27 @@
  * - Results are deterministic: the same inputs give bitwise identical outputs
  *   on the same GPU.
  *
+ * Interface choices beyond the three calls cortex_linearize,
+ * cortex_tree_forward and cortex_dag_forward (with their workspace sizes):
+ * - cortex_tree_infer / cortex_dag_infer run the whole path of a batch in one
+ *   call (one kernel launch where a fused instance fits), and
+ *   cortex_tree_infer_noalloc does the same in a library-owned workspace.
+ * - Device status 4 reports an inconsistent linearization handed to a
+ *   forward.  The arity K is a host check (CORTEX_E_INVAL outside 1..4): the
+ *   child format cannot give a node more than K children.  Status 5 reports
+ *   an input index outside the input table, status 6 a workspace whose
+ *   launch-tag epoch is used up.
+ * - cortex_tree_forward takes x_rows, the row count of d_x_table, so input
+ *   indices are range-checked on the device, and takes the weights by
+ *   pointer (NULL is a host error; a pointer crosses any FFI unchanged).
+ * - Cells are int32_t ids (the width of a C enum is up to the compiler),
+ *   including the two TreeGRU cells of the refactoring study (Sec. 7.4).
+ * - N == 0 is an empty batch, not an error.
+ * - stream is a void * holding a hipStream_t, so this header needs no HIP
+ *   header.
+ * - Launch knobs (cortex_set_knob) select schedules for the ablation
+ *   studies; probes measure the MFMA peak and the level-loop floor.
+ *
  * Structure format (Sec. 3: a batch of trees or DAGs whose maximum number of
  * children K is declared up front):
  *   d_children[v*K + s] is the node id in child slot s of node v, or -1 when
