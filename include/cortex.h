@@ -284,7 +284,7 @@ int cortex_dag_forward(int32_t H, const cortex_lin_t *lin, const float *d_x, con
  * cortex_dag_forward, with the arguments and results of those two calls.  One
  * kernel launch where the batch fits the fused instance of the kernel with
  * 16-unit slices (H = 64 or 512, or 256 below the 64-unit kernel's range of
- * 12288 nodes; N <= 2048, default schedule knobs, the linearization fitting
+ * 6144 nodes; N <= 2048, default schedule knobs, the linearization fitting
  * one compute unit's LDS beside the weight slice): every workgroup linearizes
  * the batch in LDS and workgroup 0 writes *lin out.  Otherwise the two calls.
  *   d_ws   cortex_dag_infer_workspace_bytes(N, K, H) bytes, zeroed before first use
@@ -319,7 +319,7 @@ int cortex_dag_infer(int32_t H, const int32_t *d_children, const cortex_lin_t *l
  *                                   has a kernel for them: 2 for the N-ary
  *                                   TreeLSTM at H = 256; 16 or 64 for the
  *                                   DAG-RNN at H = 256, whose default is 64
- *                                   for batches of at least 12288 nodes and
+ *                                   for batches of at least 6144 nodes and
  *                                   16 below)
  *   CORTEX_KNOB_LEVEL_SYNC          how the forward orders its levels, for
  *                                   ablation studies (the results are the same):

@@ -1229,7 +1229,7 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
 // levels instead, staging one step's sources at a time.
 // ---------------------------------------------------------------------------
 constexpr int kDagH = 256, kDagJ = 64, kDagS = kDagH / kDagJ;
-constexpr int kDagWideMinRows = 12288;             // default choice of this kernel (measured crossover)
+constexpr int kDagWideMinRows = 6144;              // default choice of this kernel (measured crossover)
 constexpr int kDagStepTiles = 2;                   // tiles per step
 constexpr int kDagStepRows = kDagStepTiles * kTileM;
 // level, level start, first row of tile 0, first row of tile 1 (-1: none),
