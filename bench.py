@@ -231,7 +231,7 @@ def cpu_baseline(wl, runs):
 # Cortex's own latencies on the paper's V100 GPU, in ms (the GPU rows of the
 # latency table comparing Cortex with DyNet, Sec. 7), keyed by (model,
 # hidden size h_s / h_l, batch).  Context for the grid below, never a target:
-# other hardware, and SST trees where this build uses SST-sized random ones.
+# other hardware, and SST trees where the grid here uses SST-sized random ones.
 PAPER_V100_CORTEX_MS = {
     ("treefc", "s", 1): 0.08, ("treefc", "s", 10): 0.17, ("treefc", "l", 1): 0.12, ("treefc", "l", 10): 0.37,
     ("dagrnn", "s", 1): 0.22, ("dagrnn", "s", 10): 0.39, ("dagrnn", "l", 1): 0.26, ("dagrnn", "l", 10): 0.54,
@@ -482,7 +482,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the path shards by whole trees/grids with no "
-              "exchange, and runs on more than one GPU are not part of this build", file=sys.stderr)
+              "exchange, and this implementation has no multi-GPU run", file=sys.stderr)
         sys.exit(2)
 
     import torch
