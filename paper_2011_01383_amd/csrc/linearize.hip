@@ -22,6 +22,10 @@
 namespace cortex {
 
 constexpr int kLinThreads = 256;
+// The digit phases of the sort give thread t digit t: the per-tile
+// histograms, the digit bases and their scan index 256-entry arrays (and the
+// global tile histograms) by thread id.
+static_assert(kLinThreads == 256, "one thread per 8-bit digit");
 constexpr int kLinWaves = kLinThreads / 64;
 constexpr int kTile = 1024;                  // radix tile
 constexpr int kSubs = kTile / 64;            // 64-item sub-chunks per tile
