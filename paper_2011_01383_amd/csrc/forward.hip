@@ -1673,6 +1673,9 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
         for (int v = 0; v < 4; ++v) sum[v] += p[v];
       }
     }
+    // C_s is written again by the next step: every wave has read it once all
+    // pass here, before the tanh and the stores, so the stores hold nobody up
+    __syncthreads();
     float hv_out[EPI];
     uint32_t el[EPI];
 #pragma unroll
@@ -1681,15 +1684,14 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       hv_out[v] = tanh_f(sum[v]);
       el[v] = (live_t && row < lend) ? (uint32_t)(row * H + hbase + j) : 0xFFFFFFFFu;
     }
+    // the tagged pairs (what the next level waits for) first, then the outputs
 #pragma unroll
-    for (int v = 0; v < EPI; ++v) {
-      if (el[v] != 0xFFFFFFFFu) {
-        hs.store1(el[v], hv_out[v], tag);
-        a.h[el[v]] = hv_out[v];
-      }
-    }
+    for (int v = 0; v < EPI; ++v)
+      if (el[v] != 0xFFFFFFFFu) hs.store1(el[v], hv_out[v], tag);
+#pragma unroll
+    for (int v = 0; v < EPI; ++v)
+      if (el[v] != 0xFFFFFFFFu) a.h[el[v]] = hv_out[v];
     CORTEX_TRACE_POINT(l, 4);
-    __syncthreads();                       // C_s is written again by the next step
     return false;
   };
 
