@@ -114,34 +114,48 @@ template <int PER, int THREADS, int KS>
 __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
                                 int max_tries) {
   const int wave_first = (int)(threadIdx.x & ~63u);
+  // per node: the LDS slots of its in-block children (absent ones read slot
+  // 0, masked out below) and the bound from the children outside the block
+  int slot[PER][KS], ebound[PER];
+  unsigned inmask[PER];
   bool pending[PER];
 #pragma unroll
-  for (int j = 0; j < PER; ++j) pending[j] = (int)threadIdx.x + j * THREADS < n;
+  for (int j = 0; j < PER; ++j) {
+    pending[j] = (int)threadIdx.x + j * THREADS < n;
+    inmask[j] = 0u;
+    ebound[j] = -1;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      slot[j][s] = lc[j][s] >= 0 ? lc[j][s] : 0;
+      inmask[j] |= lc[j][s] >= 0 ? 1u << s : 0u;
+      ebound[j] = max(ebound[j], ext[j][s]);
+    }
+  }
   for (int tries = 0; tries < max_tries; ++tries) {
     bool left = false;
     int hvs[PER][KS];
 #pragma unroll
     for (int j = 0; j < PER; ++j)
 #pragma unroll
-      for (int s = 0; s < KS; ++s) hvs[j][s] = lds_load(&hs[lc[j][s] >= 0 ? lc[j][s] : 0]);
+      for (int s = 0; s < KS; ++s) hvs[j][s] = lds_load(&hs[slot[j][s]]);
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
       if (wave_first + j * THREADS >= n) break;
-      bool ready = true;
-      int m = -1;
+      // an in-block child that is not final yet (-1) keeps the node pending
+      int m = ebound[j];
+      unsigned wait = 0u;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        if (lc[j][s] >= 0) {
-          ready = ready && hvs[j][s] >= 0;
-          m = max(m, hvs[j][s]);
-        }
-        m = max(m, ext[j][s]);
+        const bool in = (inmask[j] >> s) & 1u;
+        m = max(m, in ? hvs[j][s] : -1);
+        wait |= (in && hvs[j][s] < 0) ? 1u : 0u;
       }
-      if (pending[j] && ready) {
+      const bool fire = pending[j] && wait == 0u;
+      if (fire) {
         myh[j] = m + 1;
         lds_store(&hs[(int)threadIdx.x + j * THREADS], m + 1);
-        pending[j] = false;
       }
+      pending[j] = pending[j] && !fire;
       left = left || pending[j];
     }
     if (!__any(left)) break;
