@@ -1,8 +1,9 @@
 // Persistent level-synchronous forward kernels (Sec. 4.1 loop nest; kernel
 // fusion and model persistence as evaluated in Sec. 7.2-7.3).
 //
-// One launch runs every level.  Workgroup b owns hidden slice s = b % S
-// (J hidden units, all gates of those units) and node group q = b / S.  Its
+// One launch runs every level.  Workgroup b owns hidden slice s = b / Q
+// (J hidden units, all gates of those units) and node group q = b % Q (the
+// TreeGRU kernel: s = b % S, q = b / S).  Its
 // slice of the cell weights is loaded into LDS once and stays there for the
 // whole pass (persistence).  The rows of level l are cut into 16-row tiles
 // starting at the level's first row; group q takes the tiles u with
@@ -788,7 +789,10 @@ __global__ void __launch_bounds__(kFwdThreads) slice_forward_kernel(FwdArgs a) {
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
-  const int slice = blockIdx.x % a.S, group = blockIdx.x / a.S, Q = a.Q;
+  // node group q's slices are workgroups q, q + Q, q + 2Q, ..., which
+  // round-robin dispatch puts on the XCDs congruent to q modulo gcd(Q, 8)
+  // (two XCDs for Q = 4) instead of spreading a group over all eight
+  const int slice = blockIdx.x / a.Q, group = blockIdx.x % a.Q, Q = a.Q;
   const int hbase = slice * J;
   const int N = a.N;
   const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
@@ -1786,7 +1790,10 @@ __global__ void __launch_bounds__(kFwdThreads) childsum_forward_kernel(FwdArgs a
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
-  const int slice = blockIdx.x % a.S, group = blockIdx.x / a.S, Q = a.Q;
+  // node group q's slices are workgroups q, q + Q, q + 2Q, ..., which
+  // round-robin dispatch puts on the XCDs congruent to q modulo gcd(Q, 8)
+  // (two XCDs for Q = 4) instead of spreading a group over all eight
+  const int slice = blockIdx.x / a.Q, group = blockIdx.x % a.Q, Q = a.Q;
   const int hbase = slice * J;
   const int N = a.N, K = a.K;
   const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
@@ -2407,6 +2414,9 @@ __global__ void __launch_bounds__(kFwdThreads) treegru_forward_kernel(FwdArgs a)
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
+  // (consecutive slices here: the group-interleaved order of the slice and
+  // child-sum kernels made this kernel slower, 77.5 against 74.4 us per step
+  // on a 10-tree batch)
   const int slice = blockIdx.x % a.S, group = blockIdx.x / a.S, Q = a.Q;
   const int hbase = slice * J;
   const int N = a.N, K = a.K;
@@ -2801,10 +2811,11 @@ __device__ __forceinline__ bool level_bounds(const FwdArgs &a, int l, int &r0, i
 
 // ---------------------------------------------------------------------------
 // MV-RNN (d = 64 or 128): p = tanh(W [B a; A b]), P = W_M [A; B].
-// Node-parallel: with RB = d / 16 row blocks, workgroup b owns output rows
-// [16*(b%RB), 16*(b%RB)+16) of every node it processes (its 16 rows of W_M in
-// LDS, its share of the same rows of W in registers), and node group b/RB
-// takes nodes q, q + G/RB, ... of each level.  P = W_M[A;B] runs on MFMA with
+// Node-parallel: with RB = d / 16 row blocks and G/RB node groups, workgroup
+// b owns output rows [16 r, 16 r + 16), r = b / (G/RB), of every node it
+// processes (its 16 rows of W_M in LDS, its share of the same rows of W in
+// registers), and node group q = b % (G/RB) takes nodes q, q + G/RB, ... of
+// each level.  P = W_M[A;B] runs on MFMA with
 // [A;B] staged in LDS (wave w computes output columns 16w .. 16w+15, so a
 // workgroup has d/16 waves); the matrix-vector products use VALU.  Levels are
 // ordered per datum, as in the slice kernels: every element of p and P is
@@ -2855,7 +2866,9 @@ __global__ void __launch_bounds__(MvDims<D>::kThreads) mvrnn_forward_kernel(FwdA
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i16 = lane & 15, g4 = lane >> 4;
-  const int rblk = blockIdx.x % RB, ngroup = blockIdx.x / RB, ngroups = gridDim.x / RB;
+  // node group g's RB workgroups are g, g + G/RB, ...: round-robin dispatch
+  // puts them on one XCD
+  const int ngroups = gridDim.x / RB, rblk = blockIdx.x / ngroups, ngroup = blockIdx.x % ngroups;
   const int N = a.N;
   const bool cached = kFused || N <= M::kCacheRows;
   const uint32_t tag = launch_tag(a.sync);     // read with the status: one round trip
