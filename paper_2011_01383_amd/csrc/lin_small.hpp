@@ -57,7 +57,8 @@ __device__ int block_exclusive_scan(int *data, int n, int *wsum) {
 
 // ---------------------------------------------------------------------------
 // Height relaxation over a block of nodes whose heights live in LDS (hs).  A
-// thread owns the nodes i = tid + j*THREADS (j < PER) and holds their child
+// thread owns the nodes i = tid + j*THREADS (j < PER; see owned_node for the
+// blocked order) and holds their child
 // slots in registers: lc = the child's index inside the block (-1 when the
 // slot is empty or the child lies outside), ext = a fixed lower bound on the
 // height of a child outside the block (-1 otherwise).  A sweep raises h(i) to
@@ -70,21 +71,34 @@ __device__ int block_exclusive_scan(int *data, int n, int *wsum) {
 // ---------------------------------------------------------------------------
 constexpr int kSweepBatch = 4;
 
-template <int PER, int THREADS, int KS>
+// Node j (< PER) of the calling thread: i = tid + j*THREADS, or, with BLK,
+// i = tid*PER + j (a thread owns PER consecutive nodes).  wave_has: whether
+// some lane of the calling wave owns a node j below n (uniform over the
+// wave, and false for every larger j once false).
+template <int PER, int THREADS, bool BLK>
+__device__ __forceinline__ int owned_node(int j) {
+  return BLK ? (int)threadIdx.x * PER + j : (int)threadIdx.x + j * THREADS;
+}
+template <int PER, int THREADS, bool BLK>
+__device__ __forceinline__ bool wave_has(int j, int n) {
+  const int wave_first = (int)(threadIdx.x & ~63u);
+  return BLK ? wave_first * PER + j < n : wave_first + j * THREADS < n;
+}
+
+template <int PER, int THREADS, int KS, bool BLK = false>
 __device__ __forceinline__ bool height_sweep(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER],
                                              int *hs, int n, int N, bool &cyc) {
   bool changed = false;
   // A wave reads the child heights of its live nodes back to back, with one
   // wait: whether round j holds live nodes is uniform over the wave, and an
   // empty slot reads entry 0 of the block and is masked.  KS = slots read.
-  const int wave_first = (int)(threadIdx.x & ~63u);
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    if (wave_first + j * THREADS >= n) break;
+    if (!wave_has<PER, THREADS, BLK>(j, n)) break;
     int hv[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) hv[s] = lds_load(&hs[lc[j][s] >= 0 ? lc[j][s] : 0]);
-    const int i = (int)threadIdx.x + j * THREADS;
+    const int i = owned_node<PER, THREADS, BLK>(j);
     int m = -1;
 #pragma unroll
     for (int s = 0; s < KS; ++s) m = max(m, max(lc[j][s] >= 0 ? hv[s] : -1, ext[j][s]));
@@ -109,11 +123,13 @@ __device__ __forceinline__ bool height_sweep(const int (&lc)[PER][4], const int 
 // the pass gives up and leaves them at 0.  Every computed value is the height
 // given ext, which is at most the true height, so the sweeps that follow
 // start from valid lower bounds and confirm (or finish) the fixed point.
+// With BLK (a thread owns consecutive nodes) a height computed in a retry is
+// also handed, in registers, to the thread's later nodes that have it as a
+// child, so a chain through consecutive ids advances PER nodes per retry.
 // Returns after a workgroup barrier.
-template <int PER, int THREADS, int KS>
+template <int PER, int THREADS, int KS, bool BLK = false>
 __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
                                 int max_tries) {
-  const int wave_first = (int)(threadIdx.x & ~63u);
   // per node: the LDS slots of its in-block children (absent ones read slot
   // 0, masked out below) and the bound from the children outside the block
   int slot[PER][KS], ebound[PER];
@@ -121,7 +137,7 @@ __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4
   bool pending[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    pending[j] = (int)threadIdx.x + j * THREADS < n;
+    pending[j] = owned_node<PER, THREADS, BLK>(j) < n;
     inmask[j] = 0u;
     ebound[j] = -1;
 #pragma unroll
@@ -140,7 +156,7 @@ __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4
       for (int s = 0; s < KS; ++s) hvs[j][s] = lds_load(&hs[slot[j][s]]);
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-      if (wave_first + j * THREADS >= n) break;
+      if (!wave_has<PER, THREADS, BLK>(j, n)) break;
       // an in-block child that is not final yet (-1) keeps the node pending
       int m = ebound[j];
       unsigned wait = 0u;
@@ -152,8 +168,16 @@ __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4
       }
       const bool fire = pending[j] && wait == 0u;
       if (fire) {
+        const int i = owned_node<PER, THREADS, BLK>(j);
         myh[j] = m + 1;
-        lds_store(&hs[(int)threadIdx.x + j * THREADS], m + 1);
+        lds_store(&hs[i], m + 1);
+        if constexpr (BLK) {
+#pragma unroll
+          for (int j2 = j + 1; j2 < PER; ++j2)
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+              if (((inmask[j2] >> s) & 1u) && slot[j2][s] == i) hvs[j2][s] = m + 1;
+        }
       }
       pending[j] = pending[j] && !fire;
       left = left || pending[j];
@@ -163,7 +187,7 @@ __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    const int i = (int)threadIdx.x + j * THREADS;
+    const int i = owned_node<PER, THREADS, BLK>(j);
     if (i < n && pending[j]) {
       myh[j] = 0;
       lds_store(&hs[i], 0);
@@ -175,7 +199,7 @@ __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4
 // Sweeps to the fixed point over child slots [0, KS).  Returns (uniformly
 // over the workgroup) whether any height changed; *cycle is set when a value
 // reached N.  Every thread of the workgroup calls it.
-template <int PER, int THREADS, int KS>
+template <int PER, int THREADS, int KS, bool BLK = false>
 __device__ bool relax_heights_k(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
                                 int N, bool *cycle, int *sweeps) {
   bool any = false;
@@ -183,9 +207,9 @@ __device__ bool relax_heights_k(const int (&lc)[PER][4], const int (&ext)[PER][4
   for (;;) {
     bool cyc = false;
 #pragma unroll 1
-    for (int r = 0; r < kSweepBatch; ++r) any |= height_sweep<PER, THREADS, KS>(lc, ext, myh, hs, n, N, cyc);
+    for (int r = 0; r < kSweepBatch; ++r) any |= height_sweep<PER, THREADS, KS, BLK>(lc, ext, myh, hs, n, N, cyc);
     __syncthreads();
-    const bool ch = height_sweep<PER, THREADS, KS>(lc, ext, myh, hs, n, N, cyc);
+    const bool ch = height_sweep<PER, THREADS, KS, BLK>(lc, ext, myh, hs, n, N, cyc);
     any |= ch;
     *sweeps += kSweepBatch + 1;
     if (__syncthreads_or(cyc)) {
@@ -197,11 +221,11 @@ __device__ bool relax_heights_k(const int (&lc)[PER][4], const int (&ext)[PER][4
   return __syncthreads_or(any) != 0;
 }
 
-template <int PER, int THREADS>
+template <int PER, int THREADS, bool BLK = false>
 __device__ bool relax_heights(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
                               int K, int N, bool *cycle, int *sweeps) {
-  if (K <= 2) return relax_heights_k<PER, THREADS, 2>(lc, ext, myh, hs, n, N, cycle, sweeps);
-  return relax_heights_k<PER, THREADS, 4>(lc, ext, myh, hs, n, N, cycle, sweeps);
+  if (K <= 2) return relax_heights_k<PER, THREADS, 2, BLK>(lc, ext, myh, hs, n, N, cycle, sweeps);
+  return relax_heights_k<PER, THREADS, 4, BLK>(lc, ext, myh, hs, n, N, cycle, sweeps);
 }
 
 // ---------------------------------------------------------------------------

@@ -94,7 +94,8 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
 
   // ---------------- 1. heights ----------------
   // The children of a chunk of at most kLinPer nodes per thread (the default
-  // chunk) go to registers once; a larger chunk reads them on every sweep.
+  // chunk) go to registers once, thread t holding nodes kLinPer*t ..
+  // kLinPer*t + kLinPer - 1; a larger chunk reads them on every sweep.
   const bool in_regs = n <= kLinPer * kLinThreads;
   int cid[kLinPer][4], lc[kLinPer][4], ext[kLinPer][4], myh[kLinPer];
   int bad = 0;
@@ -103,12 +104,12 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   for (int j = 0; j < kLinPer; ++j)
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const int i = tid + j * kLinThreads;
+      const int i = owned_node<kLinPer, kLinThreads, true>(j);
       cid[j][s] = a.children[(in_regs && i < n && s < K) ? (size_t)(lo + i) * K + s : 0];
     }
 #pragma unroll
   for (int j = 0; j < kLinPer; ++j) {
-    const int i = tid + j * kLinThreads;
+    const int i = owned_node<kLinPer, kLinThreads, true>(j);
     myh[j] = 0;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -135,9 +136,9 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
 #pragma unroll
       for (int s = 0; s < 4; ++s) ext[j][s] = (cid[j][s] < 0 || lc[j][s] >= 0) ? -1 : 0;
     if (K <= 2)
-      height_dataflow<kLinPer, kLinThreads, 2>(lc, ext, myh, hs, n, 4 * kTargetChunk);
+      height_dataflow<kLinPer, kLinThreads, 2, true>(lc, ext, myh, hs, n, 4 * kTargetChunk);
     else
-      height_dataflow<kLinPer, kLinThreads, 4>(lc, ext, myh, hs, n, 4 * kTargetChunk);
+      height_dataflow<kLinPer, kLinThreads, 4, true>(lc, ext, myh, hs, n, 4 * kTargetChunk);
   }
   CORTEX_BIG_STAMP(10, wall_clock64());
   // a chunk whose children all lie inside it reaches its exact heights in
@@ -173,7 +174,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       bool cyc;
       // (round 0 reports has_ext alone: a chunk without outside children
       // is exact whatever its sweeps changed)
-      if (relax_heights<kLinPer, kLinThreads>(lc, ext, myh, hs, n, K, N, &cyc, &sweeps0) && round > 0)
+      if (relax_heights<kLinPer, kLinThreads, true>(lc, ext, myh, hs, n, K, N, &cyc, &sweeps0) && round > 0)
         block_changed = 1;
       if (cyc && tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
     } else for (;;) {
