@@ -154,6 +154,11 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     has_ext = 1;
   }
   has_ext = __syncthreads_or(has_ext);
+  const int T = a.tiles;
+  // every workgroup's chunk is its radix tile: the sort then reads heights
+  // from LDS, gets its first histograms from the height rounds, and the
+  // child rows are written per node
+  const bool own_tile = a.chunk == kTile && G == T && in_regs;
   int round = 0;
   int L = 0;
   while (ok) {
@@ -218,6 +223,16 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       local_max = max(local_max, hv);
     }
     local_max = block_max(local_max, scan_tmp);
+    if (own_tile) {
+      // the first sort pass's digit histogram of this tile, from this
+      // round's heights; after the last round they are final, and the grid
+      // barrier below publishes the histogram with them
+      hist[tid] = 0;
+      __syncthreads();
+      for (int i = tid; i < n; i += kLinThreads) atomicAdd(&hist[hs[i] & 255], 1);
+      __syncthreads();
+      a.tile_hist[(size_t)tid * T + blockIdx.x] = hist[tid];
+    }
     if (round == 0) CORTEX_BIG_STAMP(11, wall_clock64());
     if (G == 1) {
       L = local_max + 1;
@@ -252,7 +267,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   // ---------------- 2. stable counting sort on height ----------------
   int passes = 1;
   for (int v = (L - 1) >> 8; v > 0; v >>= 8) ++passes;
-  const int T = a.tiles;
+  const bool rows_per_node = own_tile && passes == 1;
   const int wave = tid >> 6, lane = tid & 63;
   const unsigned long long lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
 
@@ -262,8 +277,9 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     const bool last = (p == passes - 1);
     int32_t *out = last ? a.level_nodes : ((p & 1) ? a.perm_b : a.perm_a);
 
-    // (a) per-tile digit histograms, stored digit-major
-    for (int t = blockIdx.x; t < T; t += G) {
+    // (a) per-tile digit histograms, stored digit-major (those of the first
+    //     pass already came with the heights when every chunk is a tile)
+    for (int t = blockIdx.x; t < T && !(own_tile && p == 0); t += G) {
       hist[tid] = 0;
       __syncthreads();
       for (int i = tid; i < kTile; i += kLinThreads) {
@@ -277,7 +293,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       a.tile_hist[(size_t)tid * T + t] = hist[tid];
       __syncthreads();
     }
-    ok = grid_sync(sw, a.status, a.timeout);
+    if (!(own_tile && p == 0)) ok = grid_sync(sw, a.status, a.timeout);
     if (!ok) break;
     if (p == 0) CORTEX_BIG_STAMP(3, wall_clock64());
 
@@ -288,7 +304,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       // smaller digits, plus the rows of the same digit in earlier tiles
       {
         int tot = 0, before = 0;
-#pragma unroll 8
+#pragma unroll 32
         for (int t2 = 0; t2 < T; ++t2) {
           const int x = a.tile_hist[(size_t)tid * T + t2];
           tot += x;
@@ -298,6 +314,8 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
         __syncthreads();
         block_exclusive_scan<kLinThreads>(hist, 256, scan_tmp);
         base_s[tid] = hist[tid] + before;
+        // one pass: digit = height, so a digit's first row is its level's
+        if (rows_per_node && blockIdx.x == 0 && tid < L) a.level_offsets[tid] = hist[tid];
       }
       if (p == 0 && t == (int)blockIdx.x) CORTEX_BIG_STAMP(4, wall_clock64());
       for (int i = tid; i < kSubs * 256; i += kLinThreads) (&cnt[0][0])[i] = 0;
@@ -310,7 +328,8 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
         const int idx = t * kTile + q * 64 + lane;
         valid[qq] = idx < N;
         item[qq] = valid[qq] ? (in ? in[idx] : idx) : 0;
-        dig[qq] = valid[qq] ? ((a.height[item[qq]] >> shift) & 255) : 0;
+        const int hq = !valid[qq] ? 0 : (own_tile && p == 0) ? hs[idx - lo] : a.height[item[qq]];
+        dig[qq] = (hq >> shift) & 255;
         unsigned long long peers = __ballot(valid[qq]);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
@@ -338,6 +357,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
         }
         out[pos] = item[qq];
         if (last) a.node_row[item[qq]] = pos;
+        if (rows_per_node) hs[kTile + q * 64 + lane] = pos;     // this chunk's node q*64 + lane
       }
       __syncthreads();
     }
@@ -346,7 +366,33 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   CORTEX_BIG_STAMP(5, wall_clock64());
 
   // ---------------- 3. level offsets and child rows ----------------
-  if (ok) {
+  if (ok && rows_per_node) {
+    // per node of this chunk: its row (kept in LDS by the scatter) and its
+    // child slots (in registers) give its child rows; the children's rows
+    // were written by their chunks before the barrier above.  (The level
+    // offsets came from the digit starts.)
+    int pos[kLinPer], cr[kLinPer][4];
+#pragma unroll
+    for (int j = 0; j < kLinPer; ++j) {
+      const int i = owned_node<kLinPer, kLinThreads, true>(j);
+      pos[j] = i < n ? hs[kTile + i] : -1;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int c = (i < n && s < K) ? cid[j][s] : -1;
+        cr[j][s] = c < 0 ? -1 : a.node_row[c];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kLinPer; ++j)
+      if (pos[j] >= 0 && pos[j] < N)
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          if (s < K) a.child_rows[(size_t)pos[j] * K + s] = cr[j][s];
+    if (blockIdx.x == 0 && tid == 0) {
+      a.level_offsets[L] = N;
+      *a.num_levels = L;
+    }
+  } else if (ok) {
     const int gtid = blockIdx.x * kLinThreads + tid;
     const int gstride = G * kLinThreads;
     for (int r = gtid; r < N; r += gstride) {
@@ -485,7 +531,8 @@ int linearize_impl(const int32_t *d_children, int32_t N, int32_t K, const cortex
   a.perm_a = (int32_t *)ws;
   ws += align_up((size_t)N * sizeof(int32_t), 256);
   a.perm_b = (int32_t *)ws;
-  a.chunk = (int32_t)((N + g - 1) / g);
+  // one chunk per radix tile when the grid has one workgroup per tile
+  a.chunk = g == (int64_t)a.tiles ? kTile : (int32_t)((N + g - 1) / g);
   a.timeout = barrier_timeout_ticks();
   set_last_grid(0, (int32_t)g);
   return launch_persistent(linearize_kernel, (int)g, kLinThreads, 0, a, stream);

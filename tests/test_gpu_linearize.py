@@ -116,6 +116,21 @@ def test_random_dags_fuzz():
         compare_lin(got, O.linearize(ch, K), K)
 
 
+@pytest.mark.parametrize("N,K,blocks", [(20480, 2, 0), (20000, 3, 0), (20000, 4, 20), (20000, 2, 7)])
+def test_large_random_dags_across_chunks(N, K, blocks):
+    """Batches beyond one workgroup whose children lie anywhere below them, so
+    heights take several global rounds.  With one workgroup per 1024-node
+    tile (the default grid, or 20 workgroups for 20,000 nodes) the sort takes
+    its first histograms from the height rounds and the child rows are written
+    per node; 7 workgroups take the general path."""
+    rng = np.random.default_rng(N + 10 * K + blocks)
+    ch = I.random_dag(rng, N, K, p_absent=0.3)
+    announce("large random dag N=%d K=%d blocks=%d" % (N, K, blocks))
+    st, got, _ = gpu_linearize(ch, K, blocks)
+    assert st == 0
+    compare_lin(got, O.linearize(ch, K), K)
+
+
 def test_relabeled_workloads():
     rng = np.random.default_rng(7)
     for k in range(4):
