@@ -126,9 +126,11 @@ __device__ __forceinline__ bool height_sweep(const int (&lc)[PER][4], const int 
 // With BLK (a thread owns consecutive nodes) a height computed in a retry is
 // also handed, in registers, to the thread's later nodes that have it as a
 // child, so a chain through consecutive ids advances PER nodes per retry.
-// Returns after a workgroup barrier.
+// Returns (uniformly, after a workgroup barrier) whether every node was
+// computed: then the heights are exact for the bounds ext and no sweep can
+// change them.
 template <int PER, int THREADS, int KS, bool BLK = false>
-__device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
+__device__ bool height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4], int (&myh)[PER], int *hs, int n,
                                 int max_tries) {
   // per node: the LDS slots of its in-block children (absent ones read slot
   // 0, masked out below) and the bound from the children outside the block
@@ -184,7 +186,10 @@ __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4
     }
     if (!__any(left)) break;
   }
-  __syncthreads();
+  bool any_left = false;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) any_left = any_left || (owned_node<PER, THREADS, BLK>(j) < n && pending[j]);
+  const bool complete = !__syncthreads_or(any_left);
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int i = owned_node<PER, THREADS, BLK>(j);
@@ -194,6 +199,7 @@ __device__ void height_dataflow(const int (&lc)[PER][4], const int (&ext)[PER][4
     }
   }
   __syncthreads();
+  return complete;
 }
 
 // Sweeps to the fixed point over child slots [0, KS).  Returns (uniformly

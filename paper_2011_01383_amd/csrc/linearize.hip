@@ -128,6 +128,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   for (int i = tid; i < n; i += kLinThreads) hs[i] = in_regs ? -1 : 0;
   __syncthreads();
   CORTEX_BIG_STAMP(9, wall_clock64());
+  bool complete0 = false;
   if (in_regs && ok) {
     // round 0: children outside the chunk count 0 (a lower bound); nodes
     // whose in-chunk children are final are computed once, in dataflow order
@@ -136,9 +137,9 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
 #pragma unroll
       for (int s = 0; s < 4; ++s) ext[j][s] = (cid[j][s] < 0 || lc[j][s] >= 0) ? -1 : 0;
     if (K <= 2)
-      height_dataflow<kLinPer, kLinThreads, 2, true>(lc, ext, myh, hs, n, 4 * kTargetChunk);
+      complete0 = height_dataflow<kLinPer, kLinThreads, 2, true>(lc, ext, myh, hs, n, 4 * kTargetChunk);
     else
-      height_dataflow<kLinPer, kLinThreads, 4, true>(lc, ext, myh, hs, n, 4 * kTargetChunk);
+      complete0 = height_dataflow<kLinPer, kLinThreads, 4, true>(lc, ext, myh, hs, n, 4 * kTargetChunk);
   }
   CORTEX_BIG_STAMP(10, wall_clock64());
   // a chunk whose children all lie inside it reaches its exact heights in
@@ -176,10 +177,12 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
                           ? -1
                           : (round == 0 ? 0 : __hip_atomic_load(&a.height[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
         }
-      bool cyc;
+      bool cyc = false;
       // (round 0 reports has_ext alone: a chunk without outside children
-      // is exact whatever its sweeps changed)
-      if (relax_heights<kLinPer, kLinThreads, true>(lc, ext, myh, hs, n, K, N, &cyc, &sweeps0) && round > 0)
+      // is exact whatever its sweeps changed.  When the dataflow pass
+      // computed every node, round 0 needs no sweep at all.)
+      if (!(round == 0 && complete0) &&
+          relax_heights<kLinPer, kLinThreads, true>(lc, ext, myh, hs, n, K, N, &cyc, &sweeps0) && round > 0)
         block_changed = 1;
       if (cyc && tid == 0) raise_status(a.status, CORTEX_ST_CYCLE);
     } else for (;;) {
@@ -304,11 +307,23 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       // smaller digits, plus the rows of the same digit in earlier tiles
       {
         int tot = 0, before = 0;
+        if ((T & 3) == 0 && ((uintptr_t)a.tile_hist & 15) == 0) {
+          // this digit's row of T counts, 16 bytes per load, all in flight
+          const int4 *row = (const int4 *)(a.tile_hist + (size_t)tid * T);
+#pragma unroll 16
+          for (int t4 = 0; t4 < T / 4; ++t4) {
+            const int4 x = row[t4];
+            const int b = 4 * t4;
+            tot += x.x + x.y + x.z + x.w;
+            before += (b < t ? x.x : 0) + (b + 1 < t ? x.y : 0) + (b + 2 < t ? x.z : 0) + (b + 3 < t ? x.w : 0);
+          }
+        } else {
 #pragma unroll 32
-        for (int t2 = 0; t2 < T; ++t2) {
-          const int x = a.tile_hist[(size_t)tid * T + t2];
-          tot += x;
-          before += t2 < t ? x : 0;
+          for (int t2 = 0; t2 < T; ++t2) {
+            const int x = a.tile_hist[(size_t)tid * T + t2];
+            tot += x;
+            before += t2 < t ? x : 0;
+          }
         }
         hist[tid] = tot;
         __syncthreads();
