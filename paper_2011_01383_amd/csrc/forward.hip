@@ -1281,19 +1281,20 @@ __device__ __forceinline__ int dag_group_tiles(int group, int l, int Q, int ntil
 // Operand sources of row slot (t, i) of a step record; validates them as the
 // forward requires (a child lies below its row's level).  Returns false when
 // the linearization is inconsistent.
-__device__ __forceinline__ bool dag_fill_codes(const FwdArgs &a, int *st, int slot) {
-  const int t = slot / kTileM, i = slot % kTileM;
-  const int base = st[2 + t], lstart = st[1], lend = st[4];
-  const int row = base + i;
+// The row of slot (t, i) of a step record, or -1 when the slot is empty.
+__device__ __forceinline__ int dag_slot_row(const int *st, int slot) {
+  const int base = st[2 + slot / kTileM], row = base + slot % kTileM;
+  return (base >= 0 && row < st[4]) ? row : -1;
+}
+
+// Stores the operand sources of a slot from its row's node id v and child
+// rows c0, c1 (read when live, i.e. the slot holds a row); returns false when
+// they are inconsistent.
+__device__ __forceinline__ bool dag_store_codes(const FwdArgs &a, int *st, int slot, bool live, int v, int c0, int c1) {
+  const int lstart = st[1];
   int *cd = &st[kDagStepHead + slot * 3];
-  bool ok = true;
-  int v = -1, c0 = -1, c1 = -1;
-  if (base >= 0 && row < lend) {
-    v = a.level_nodes[row];
-    c0 = a.child_rows[(size_t)row * 2];
-    c1 = a.child_rows[(size_t)row * 2 + 1];
-    if (v < 0 || v >= a.N) ok = false;
-  }
+  if (!live) v = c0 = c1 = -1;
+  bool ok = !live || (v >= 0 && v < a.N);
   cd[0] = (v >= 0 && v < a.N) ? -2 - v : -1;
   if (c0 < -1 || c0 >= lstart) {
     ok = false;
@@ -1306,6 +1307,17 @@ __device__ __forceinline__ bool dag_fill_codes(const FwdArgs &a, int *st, int sl
   cd[1] = c0;
   cd[2] = c1;
   return ok;
+}
+
+__device__ __forceinline__ bool dag_fill_codes(const FwdArgs &a, int *st, int slot) {
+  const int row = dag_slot_row(st, slot);
+  int v = -1, c0 = -1, c1 = -1;
+  if (row >= 0) {
+    v = a.level_nodes[row];
+    c0 = a.child_rows[(size_t)row * 2];
+    c1 = a.child_rows[(size_t)row * 2 + 1];
+  }
+  return dag_store_codes(a, st, slot, row >= 0, v, c0, c1);
 }
 
 // Hoisted input products of the DAG-RNN at H = 256 (the ablation of the
@@ -1414,39 +1426,19 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   const int xcol = KX * wave;                  // this wave's first input column
 
   CORTEX_TRACE_KERNEL(0);
-  // the status, the level count and the weights are requested together: one
-  // memory round trip for all of them
+  // The structure is read first and the weights (192 KB per workgroup, the
+  // longest transfer of the entry) are requested once the step list is
+  // known, after the operand sources' loads: vector loads complete in order,
+  // so weights requested first would hold back every structure read behind
+  // them.
   const int status0 = load_status(a.status);
   const int L = *a.num_levels;
-  // recurrent weights: wr[b][nt] = U_rslot[hbase + 16 nt + i16][rcol + 16 b + 4 g4 .. +3]
-  float4 wr[NBR][NT];
-#pragma unroll
-  for (int b = 0; b < NBR; ++b)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      wr[b][nt] = *(const float4 *)(a.U + ((size_t)rslot * H + hbase + 16 * nt + i16) * H + rcol + 16 * b + 4 * g4);
-  if constexpr (!kHoisted) {
-    constexpr int ITEMS = J * H / 4, PER = ITEMS / kFwdThreads;
-    float4 v[PER];
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int idx = tid + k * kFwdThreads;
-      v[k] = *(const float4 *)(a.W + (size_t)(hbase + idx / (H / 4)) * H + 4 * (idx % (H / 4)));
-    }
-    if (tid < J) bias_s[tid] = a.b[hbase + tid];
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int idx = tid + k * kFwdThreads;
-      *(float4 *)&Wx_s[(idx / (H / 4)) * LDX + 4 * (idx % (H / 4))] = v[k];
-    }
-  }
   if (tid == 0) stop_s = 0;
   if (status0 != 0) return;
   if (L < 1 || L > N) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
     return;
   }
-  CORTEX_TRACE_KERNEL(1);
 
   // ---- this group's steps of every level, one level per thread per round ----
   int total = 0, bad = 0;
@@ -1480,14 +1472,59 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     return;
   }
   const bool listed = total <= kDagStepCap;
-  if (listed) {
-    for (int idx = tid; idx < total * kDagStepRows; idx += kFwdThreads)
-      if (!dag_fill_codes(a, &list[(idx / kDagStepRows) * SI], idx % kDagStepRows)) bad = 1;
-    if (__syncthreads_or(bad)) {
-      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
-      return;
+  // operand sources of every listed slot: requested now, stored below
+  constexpr int kFillPer = (kDagStepCap * kDagStepRows + kFwdThreads - 1) / kFwdThreads;
+  int frow[kFillPer], fv[kFillPer], f0[kFillPer], f1[kFillPer];
+#pragma unroll
+  for (int k = 0; k < kFillPer; ++k) {
+    const int idx = tid + k * kFwdThreads;
+    frow[k] = (listed && idx < total * kDagStepRows) ? dag_slot_row(&list[(idx / kDagStepRows) * SI], idx % kDagStepRows)
+                                                     : -1;
+    fv[k] = f0[k] = f1[k] = -1;
+    if (frow[k] >= 0) {
+      fv[k] = a.level_nodes[frow[k]];
+      f0[k] = a.child_rows[(size_t)frow[k] * 2];
+      f1[k] = a.child_rows[(size_t)frow[k] * 2 + 1];
     }
   }
+  // recurrent weights: wr[b][nt] = U_rslot[hbase + 16 nt + i16][rcol + 16 b + 4 g4 .. +3]
+  float4 wr[NBR][NT];
+#pragma unroll
+  for (int b = 0; b < NBR; ++b)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      wr[b][nt] = *(const float4 *)(a.U + ((size_t)rslot * H + hbase + 16 * nt + i16) * H + rcol + 16 * b + 4 * g4);
+  constexpr int ITEMS = J * H / 4, PER = kHoisted ? 1 : ITEMS / kFwdThreads;
+  float4 v[PER];
+  if constexpr (!kHoisted) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      v[k] = *(const float4 *)(a.W + (size_t)(hbase + idx / (H / 4)) * H + 4 * (idx % (H / 4)));
+    }
+    if (tid < J) bias_s[tid] = a.b[hbase + tid];
+  }
+  if (listed) {
+#pragma unroll
+    for (int k = 0; k < kFillPer; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      if (idx < total * kDagStepRows &&
+          !dag_store_codes(a, &list[(idx / kDagStepRows) * SI], idx % kDagStepRows, frow[k] >= 0, fv[k], f0[k], f1[k]))
+        bad = 1;
+    }
+  }
+  if constexpr (!kHoisted) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      *(float4 *)&Wx_s[(idx / (H / 4)) * LDX + 4 * (idx % (H / 4))] = v[k];
+    }
+  }
+  if (__syncthreads_or(bad)) {
+    raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+    return;
+  }
+  CORTEX_TRACE_KERNEL(1);
   CORTEX_TRACE_KERNEL(2);
   if (!mark_entered(a.sync, tag, a.status)) return;
   int gave_up = 0;
