@@ -21,11 +21,13 @@
 
 namespace cortex {
 
-constexpr int kLinThreads = 256;
-// The digit phases of the sort give thread t digit t: the per-tile
+constexpr int kLinThreads = 1024;
+// The digit phases of the sort give thread t < 256 digit t: the per-tile
 // histograms, the digit bases and their scan index 256-entry arrays (and the
-// global tile histograms) by thread id.
-static_assert(kLinThreads == 256, "one thread per 8-bit digit");
+// global tile histograms) by thread id, so every such access sits behind
+// `digit_thread`; threads 256 and up only join the barriers there.
+constexpr int kDigits = 256;
+static_assert(kLinThreads >= kDigits && kLinThreads % 64 == 0, "a thread per 8-bit digit");
 constexpr int kLinWaves = kLinThreads / 64;
 constexpr int kTile = 1024;                  // radix tile
 constexpr int kSubs = kTile / 64;            // 64-item sub-chunks per tile
@@ -83,6 +85,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
 
   const SyncWords sw{a.sync};
   const int tid = threadIdx.x;
+  const bool digit_thread = tid < kDigits;
   const int G = gridDim.x;
   const int N = a.N, K = a.K;
   const int lo = blockIdx.x * a.chunk;
@@ -230,11 +233,11 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       // the first sort pass's digit histogram of this tile, from this
       // round's heights; after the last round they are final, and the grid
       // barrier below publishes the histogram with them
-      hist[tid] = 0;
+      if (digit_thread) hist[tid] = 0;
       __syncthreads();
       for (int i = tid; i < n; i += kLinThreads) atomicAdd(&hist[hs[i] & 255], 1);
       __syncthreads();
-      a.tile_hist[(size_t)tid * T + blockIdx.x] = hist[tid];
+      if (digit_thread) a.tile_hist[(size_t)tid * T + blockIdx.x] = hist[tid];
     }
     if (round == 0) CORTEX_BIG_STAMP(11, wall_clock64());
     if (G == 1) {
@@ -283,7 +286,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     // (a) per-tile digit histograms, stored digit-major (those of the first
     //     pass already came with the heights when every chunk is a tile)
     for (int t = blockIdx.x; t < T && !(own_tile && p == 0); t += G) {
-      hist[tid] = 0;
+      if (digit_thread) hist[tid] = 0;
       __syncthreads();
       for (int i = tid; i < kTile; i += kLinThreads) {
         const int idx = t * kTile + i;
@@ -293,7 +296,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
         }
       }
       __syncthreads();
-      a.tile_hist[(size_t)tid * T + t] = hist[tid];
+      if (digit_thread) a.tile_hist[(size_t)tid * T + t] = hist[tid];
       __syncthreads();
     }
     if (!(own_tile && p == 0)) ok = grid_sync(sw, a.status, a.timeout);
@@ -301,13 +304,16 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
     if (p == 0) CORTEX_BIG_STAMP(3, wall_clock64());
 
     // (c) stable scatter: rank = (digit base of this tile) + (equal digits
-    //     earlier in the tile).  Sub-chunk q of 64 items goes to wave q/4.
+    //     earlier in the tile).  Sub-chunk q of 64 items goes to wave
+    //     q / kSubsPerWave.
     for (int t = blockIdx.x; t < T; t += G) {
       // digit bases of tile t, from every tile's histogram: the rows of all
       // smaller digits, plus the rows of the same digit in earlier tiles
       {
         int tot = 0, before = 0;
-        if ((T & 3) == 0 && ((uintptr_t)a.tile_hist & 15) == 0) {
+        if (!digit_thread) {
+          // no digit: only the scan's barriers
+        } else if ((T & 3) == 0 && ((uintptr_t)a.tile_hist & 15) == 0) {
           // this digit's row of T counts, 16 bytes per load, all in flight
           const int4 *row = (const int4 *)(a.tile_hist + (size_t)tid * T);
 #pragma unroll 16
@@ -325,12 +331,12 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
             before += t2 < t ? x : 0;
           }
         }
-        hist[tid] = tot;
+        if (digit_thread) hist[tid] = tot;
         __syncthreads();
-        block_exclusive_scan<kLinThreads>(hist, 256, scan_tmp);
-        base_s[tid] = hist[tid] + before;
+        block_exclusive_scan<kLinThreads>(hist, kDigits, scan_tmp);
+        if (digit_thread) base_s[tid] = hist[tid] + before;
         // one pass: digit = height, so a digit's first row is its level's
-        if (rows_per_node && blockIdx.x == 0 && tid < L) a.level_offsets[tid] = hist[tid];
+        if (rows_per_node && blockIdx.x == 0 && digit_thread && tid < L) a.level_offsets[tid] = hist[tid];
       }
       if (p == 0 && t == (int)blockIdx.x) CORTEX_BIG_STAMP(4, wall_clock64());
       for (int i = tid; i < kSubs * 256; i += kLinThreads) (&cnt[0][0])[i] = 0;
@@ -356,7 +362,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
         if (valid[qq] && rank[qq] == 0) cnt[q][dig[qq]] = __popcll(peers);
       }
       __syncthreads();
-      {   // exclusive scan over sub-chunks, one digit per thread
+      if (digit_thread) {   // exclusive scan over sub-chunks, one digit per thread
         int run = 0;
         for (int q = 0; q < kSubs; ++q) { int x = cnt[q][tid]; cnt[q][tid] = run; run += x; }
       }
