@@ -167,6 +167,10 @@ size_t cortex_linearize_workspace_bytes(int32_t N, int32_t K);
  * Kernel-detected errors: CORTEX_ST_CHILD_RANGE, CORTEX_ST_CYCLE,
  * CORTEX_ST_BARRIER_TIMEOUT (outputs are then undefined).
  * N == 0 is an empty batch: it writes num_levels = 0.
+ * A batch beyond one workgroup's LDS (above 4,096 nodes; fewer at arity 3
+ * and 4) runs on co-resident workgroups of 1,024 threads, each holding at
+ * most 8,192 nodes: CORTEX_E_TOO_LARGE when the GPU cannot hold enough of
+ * them (two per compute unit: 4,194,304 nodes on 256 CUs).
  */
 int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin,
                      int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream);
