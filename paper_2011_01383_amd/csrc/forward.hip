@@ -1619,51 +1619,44 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
             xn[k / NBX][k % NBX] = xin.load4(xo_next[k / NBX] + 64u * (k % NBX));
           }
           if (b == NBX - 1) {
+            // (tile 1's blocks follow during tile 0's recurrent part)
             static_assert(NBR == 4, "one child block per MFMA step");
             hv[0][k].lo = hs.load2_at(ho[0] + 128u * k);
             hv[0][k].hi = hs.load2_at(ho[0] + 128u * k + 16u);
-            if (two) {
-              hv[1][k].lo = hs.load2_at(ho[1] + 128u * k);
-              hv[1][k].hi = hs.load2_at(ho[1] + 128u * k + 16u);
-            }
           }
         }
       }
     }
     CORTEX_TRACE_POINT(l, 1);
-    // 2. wait for the children
-    auto ready = [&]() __attribute__((always_inline)) -> bool {
-      bool r = true;
-#pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        if (t > 0 && !two) break;
+    // 2. per tile: wait until its child fragments carry the launch tag, then
+    // contract them.  With the fused input part, tile 1's fragments are
+    // requested between the MFMA blocks of tile 0's contraction, so the
+    // address unit takes half the fragments during the input part and half
+    // in the shadow of tile 0's recurrent MFMAs.
+    auto wait_tile = [&](int t) __attribute__((always_inline)) {
+      auto ready_t = [&]() __attribute__((always_inline)) -> bool {
         bool rt = true;
 #pragma unroll
         for (int b = 0; b < NBR; ++b) rt = rt && hv[t][b].ready(tag);
-        r = r && (cr[t] < 0 || rt);
-      }
-      return r;
-    };
-    if (!gave_up && !ready()) {
+        return cr[t] < 0 || rt;
+      };
+      if (gave_up || ready_t()) return;
       const uint64_t t0 = wall_clock64();
       for (;;) {
         __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-        for (int t = 0; t < MT; ++t)
-#pragma unroll
-          for (int b = 0; b < NBR; ++b) {
-            if ((t == 0 || two) && cr[t] >= 0 && !hv[t][b].ready(tag)) {
-              const uint32_t so = (uint32_t)(cr[t] * H + rcol + 16 * b + 4 * g4) * 8u;
-              hv[t][b].lo = hs.load2_at(so);
-              hv[t][b].hi = hs.load2_at(so + 16u);
-            }
+        for (int b = 0; b < NBR; ++b)
+          if (cr[t] >= 0 && !hv[t][b].ready(tag)) {
+            hv[t][b].lo = hs.load2_at(ho[t] + 128u * b);
+            hv[t][b].hi = hs.load2_at(ho[t] + 128u * b + 16u);
           }
-        const int stv = load_status(a.status);
-        if (ready()) break;
-        if (stv != 0) {
+        // the status first: a load still in flight at the exit would hold
+        // back the MFMAs that follow until it returns
+        if (load_status(a.status) != 0) {
           gave_up = 1;
           break;
         }
+        if (ready_t()) break;
         if (wall_clock64() - t0 > a.timeout) {
           raise_status(a.status, CORTEX_ST_BARRIER_TIMEOUT);
           gave_up = 1;
@@ -1671,13 +1664,22 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
         }
       }
       if (gave_up) stop_s = 1;             // read by every wave after the next barrier
-    }
+    };
+    wait_tile(0);
     CORTEX_TRACE_POINT(l, 2);
     // 3. recurrent part
 #pragma unroll
     for (int b = 0; b < NBR; ++b) {
       mfma_k16_xn<NT>(hv[0][b].value(true), wr[b], acc[0]);
-      if (two) mfma_k16_xn<NT>(hv[1][b].value(true), wr[b], acc[1]);
+      if (!kHoisted && two) {
+        hv[1][b].lo = hs.load2_at(ho[1] + 128u * b);
+        hv[1][b].hi = hs.load2_at(ho[1] + 128u * b + 16u);
+      }
+    }
+    if (two) {
+      wait_tile(1);
+#pragma unroll
+      for (int b = 0; b < NBR; ++b) mfma_k16_xn<NT>(hv[1][b].value(true), wr[b], acc[1]);
     }
     CORTEX_TRACE_WAVE(l);
     // the next step's input fragments are complete before this step's stores
