@@ -266,6 +266,20 @@ def test_dag_slice_widths(units, groups):
     compare_states(dw.states_by_node(), O.forward_workload(wl), "dag units %d" % units)
 
 
+@pytest.mark.parametrize("groups", [2, 3])
+def test_dag_two_tile_steps_ragged(groups):
+    """64-unit DAG-RNN slices with few node groups, so most steps carry two
+    tiles (tile 1's child fragments are requested during tile 0's recurrent
+    part and waited for on their own) and levels end in ragged tiles; ten
+    20x15 grids, against the oracle."""
+    wl = I.dagrnn_workload(79 + groups, n_grids=10, rows=20, cols=15, H=256)
+    announce("dag two-tile steps groups %d N=%d" % (groups, wl.N))
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 64)
+    dw = run(wl, groups)
+    assert C.cortex_last_grid(1) == 4 * groups
+    compare_states(dw.states_by_node(), O.forward_workload(wl), "dag two-tile groups %d" % groups)
+
+
 def test_dag_tile_list_overflow():
     """One node group over 6 grids of 32x32: the group's tiles exceed the
     per-workgroup tile list, so the kernel walks the levels and stages each
