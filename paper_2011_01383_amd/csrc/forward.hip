@@ -1278,9 +1278,6 @@ __device__ __forceinline__ int dag_group_tiles(int group, int l, int Q, int ntil
   return uf < ntile ? (ntile - 1 - uf) / Q + 1 : 0;
 }
 
-// Operand sources of row slot (t, i) of a step record; validates them as the
-// forward requires (a child lies below its row's level).  Returns false when
-// the linearization is inconsistent.
 // The row of slot (t, i) of a step record, or -1 when the slot is empty.
 __device__ __forceinline__ int dag_slot_row(const int *st, int slot) {
   const int base = st[2 + slot / kTileM], row = base + slot % kTileM;
@@ -1288,8 +1285,9 @@ __device__ __forceinline__ int dag_slot_row(const int *st, int slot) {
 }
 
 // Stores the operand sources of a slot from its row's node id v and child
-// rows c0, c1 (read when live, i.e. the slot holds a row); returns false when
-// they are inconsistent.
+// rows c0, c1 (read when live, i.e. the slot holds a row), validated as the
+// forward requires (a child lies below its row's level); returns false when
+// the linearization is inconsistent.
 __device__ __forceinline__ bool dag_store_codes(const FwdArgs &a, int *st, int slot, bool live, int v, int c0, int c1) {
   const int lstart = st[1];
   int *cd = &st[kDagStepHead + slot * 3];
@@ -1309,6 +1307,7 @@ __device__ __forceinline__ bool dag_store_codes(const FwdArgs &a, int *st, int s
   return ok;
 }
 
+// Reads and stores the operand sources of a slot.
 __device__ __forceinline__ bool dag_fill_codes(const FwdArgs &a, int *st, int slot) {
   const int row = dag_slot_row(st, slot);
   int v = -1, c0 = -1, c1 = -1;
@@ -1597,8 +1596,8 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       x_offsets(nst ? nst : st, nst != nullptr, xo_next);
       // 1. input part; one weight fragment serves both tiles.  The next
       // step's input fragments are requested during its first half and the
-      // child-state fragments of every row of this step during its second
-      // half, one load or one block per MFMA step, rather than in bursts,
+      // child-state fragments of tile 0's rows during its second half, one
+      // load or one block per MFMA step, rather than in bursts,
       // which would hold the MFMAs behind them until the address unit has
       // taken every load.  The child fragments are not requested at the
       // start: a level's children are written at the end of the previous
