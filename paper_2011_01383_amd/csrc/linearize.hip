@@ -274,6 +274,11 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
   int passes = 1;
   for (int v = (L - 1) >> 8; v > 0; v >>= 8) ++passes;
   const bool rows_per_node = own_tile && passes == 1;
+  // every child lies in its parent's chunk (round 0 found no chunk reading
+  // outside itself, so the height loop stopped after it, or there is one
+  // chunk): a chunk's child rows then come from its own rows in LDS, and no
+  // barrier across workgroups is needed after the scatter
+  const bool rows_local = rows_per_node && (G == 1 || round == 1);
   const int wave = tid >> 6, lane = tid & 63;
   const unsigned long long lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
 
@@ -382,16 +387,17 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
       }
       __syncthreads();
     }
-    ok = grid_sync(sw, a.status, a.timeout);
+    if (!(last && rows_local)) ok = grid_sync(sw, a.status, a.timeout);
   }
   CORTEX_BIG_STAMP(5, wall_clock64());
 
   // ---------------- 3. level offsets and child rows ----------------
   if (ok && rows_per_node) {
     // per node of this chunk: its row (kept in LDS by the scatter) and its
-    // child slots (in registers) give its child rows; the children's rows
-    // were written by their chunks before the barrier above.  (The level
-    // offsets came from the digit starts.)
+    // child slots (in registers) give its child rows; a child's row is in
+    // LDS too when it lies in the chunk and every child does (rows_local),
+    // else its chunk wrote it before the barrier above.  (The level offsets
+    // came from the digit starts.)
     int pos[kLinPer], cr[kLinPer][4];
 #pragma unroll
     for (int j = 0; j < kLinPer; ++j) {
@@ -400,7 +406,7 @@ __global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         const int c = (i < n && s < K) ? cid[j][s] : -1;
-        cr[j][s] = c < 0 ? -1 : a.node_row[c];
+        cr[j][s] = c < 0 ? -1 : (rows_local && lc[j][s] >= 0) ? hs[kTile + lc[j][s]] : a.node_row[c];
       }
     }
 #pragma unroll
