@@ -24,6 +24,7 @@
 // table directly, so nothing ever waits on the leaf level.
 #include <algorithm>
 #include <atomic>
+#include <type_traits>
 
 #include "cortex_device.hpp"
 #include "cortex_host.hpp"
@@ -1227,18 +1228,23 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
 //   3. contracts the recurrent columns;
 // the eight partial sums then meet in LDS and the workgroup applies tanh and
 // writes the step's rows.  The next step's input fragments are complete
-// before the stores are issued, so no wait of the next step covers them.  At entry each workgroup lists its steps of every
-// level with their operand sources in LDS, so the level loop never goes back
-// to the linearization in memory; a group whose list does not fit walks the
-// levels instead, staging one step's sources at a time.
+// before the stores are issued, so no wait of the next step covers them.
+// A level of at most Q/2 tiles is split finer: each of its tiles is a half
+// step of two groups, one per half of the slice's units, so the narrow first
+// and last levels of a batch, whose chain of waits sets the pace, take half
+// the contraction time per group.  At entry each workgroup lists its steps of
+// every level with their operand sources in LDS, so the level loop never
+// goes back to the linearization in memory; a group whose list does not fit
+// walks the levels instead, staging one step's sources at a time.
 // ---------------------------------------------------------------------------
 constexpr int kDagH = 256, kDagJ = 64, kDagS = kDagH / kDagJ;
 constexpr int kDagWideMinRows = 6144;              // default choice of this kernel (measured crossover)
 constexpr int kDagStepTiles = 2;                   // tiles per step
 constexpr int kDagStepRows = kDagStepTiles * kTileM;
 // level, level start, first row of tile 0, first row of tile 1 (-1: none),
-// level end, then codes[32][3]: -2 - node id (input row) or -1, child rows
-constexpr int kDagStepHead = 5;
+// level end, units (0: the slice's 64, 1: its first 32, 2: its last 32),
+// then codes[32][3]: -2 - node id (input row) or -1, child rows
+constexpr int kDagStepHead = 6;
 constexpr int kDagStepInts = kDagStepHead + kDagStepRows * 3;
 constexpr int kDagStepCap = 60;                    // steps per workgroup list (dynamic LDS)
 constexpr size_t kDagListBytes = (size_t)kDagStepCap * kDagStepInts * sizeof(int);
@@ -1271,11 +1277,31 @@ __device__ __forceinline__ int block_excl_scan(int v, int *wsum, int *total) {
   return ex;
 }
 
-// Tiles of group `group` at a level of ntile tiles: u = uf, uf + Q, ...;
-// returns their count.
-__device__ __forceinline__ int dag_group_tiles(int group, int l, int Q, int ntile, int &uf) {
-  uf = ((group - l) % Q + Q) % Q;
-  return uf < ntile ? (ntile - 1 - uf) / Q + 1 : 0;
+// Tiles of group `group` at a level of ntile tiles; returns their count.
+// Normally the tiles u = uf, uf + Q, ... with uf = (group - l) mod Q, whole
+// (half = 0).  A level of at most Q/2 tiles (Q even) gives each tile to two
+// groups, each computing half of its slice's units, so the tile's
+// contraction is split over twice the compute units: group q takes tile
+// (q - l) mod Q as half 1 (the first 32 units) or tile (q - l + Q/2) mod Q
+// as half 2 (the last 32); at most one of the two exists.
+__device__ __forceinline__ int dag_group_tiles(int group, int l, int Q, int ntile, int &uf, int &half) {
+  const int u1 = ((group - l) % Q + Q) % Q;
+  half = 0;
+  uf = u1;
+  if (Q % 2 == 0 && 2 * ntile <= Q) {
+    const int u2 = (u1 + Q / 2) % Q;
+    if (u1 < ntile) {
+      half = 1;
+      return 1;
+    }
+    if (u2 < ntile) {
+      uf = u2;
+      half = 2;
+      return 1;
+    }
+    return 0;
+  }
+  return u1 < ntile ? (ntile - 1 - u1) / Q + 1 : 0;
 }
 
 // The row of slot (t, i) of a step record, or -1 when the slot is empty.
@@ -1443,14 +1469,14 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
   int total = 0, bad = 0;
   for (int lb = 0; lb < L; lb += kFwdThreads) {
     const int l = lb + tid;
-    int nst = 0, r0 = 0, r1 = 0, uf = 0, cnt = 0;
+    int nst = 0, r0 = 0, r1 = 0, uf = 0, cnt = 0, half = 0;
     if (l < L) {
       r0 = a.level_offsets[l];
       r1 = a.level_offsets[l + 1];
       const bool ok = r0 >= 0 && r1 >= r0 && r1 <= N && (l != 0 || r0 == 0) && (l != L - 1 || r1 == N);
       if (!ok) bad = 1;
       const int ntile = (ok && l >= a.level_lo && l < a.level_hi) ? (r1 - r0 + kTileM - 1) / kTileM : 0;
-      cnt = dag_group_tiles(group, l, Q, ntile, uf);
+      cnt = dag_group_tiles(group, l, Q, ntile, uf, half);
       nst = (cnt + MT - 1) / MT;
     }
     int round_total;
@@ -1462,6 +1488,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       st[2] = r0 + kTileM * (uf + (MT * j) * Q);
       st[3] = MT * j + 1 < cnt ? r0 + kTileM * (uf + (MT * j + 1) * Q) : -1;
       st[4] = r1;
+      st[5] = half;
     }
     total += round_total;
   }
@@ -1548,13 +1575,24 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       for (int b = 0; b < NBX; ++b) xv[t][b] = xin.load4(xo[t] + 64u * b);
   };
 
-  // One step.  xc: its input fragments (requested earlier); nst: the next
-  // step (nullptr: none), whose input fragments go to xn.  Returns true when
-  // the kernel must stop.
-  auto run_step = [&](const int *st, const u32x4 (&xc)[MT][NBX], const int *nst,
+  // One step.  half_c: the step's units as a compile-time constant (0: the
+  // slice's 64, 1: its first 32, 2: its last 32; a half step has one tile);
+  // xc: its input fragments (requested earlier); nst: the next step
+  // (nullptr: none), whose input fragments go to xn.  Returns true when the
+  // kernel must stop.
+  auto run_step = [&](auto half_c, const int *st, const u32x4 (&xc)[MT][NBX], const int *nst,
                       u32x4 (&xn)[MT][NBX]) __attribute__((always_inline)) -> bool {
+    constexpr int kHalf = decltype(half_c)::value;
+    constexpr int NT0 = kHalf == 2 ? NT / 2 : 0;         // first n-tile of the step's units
+    constexpr int NTS = kHalf == 0 ? NT : NT / 2;        // n-tiles of the step's units
     const int l = st[0], lend = st[4];
-    const bool two = st[3] >= 0;
+    const bool two = kHalf == 0 && st[3] >= 0;
+    // epilogue thread: unit ej (within the slice) of row quarter eq of tile
+    // et; a whole step uses every thread, a half step the first 128
+    const int ej = kHalf == 0 ? (tid & (J - 1)) : J / 2 * (kHalf - 1) + (tid & (J / 2 - 1));
+    const int et = kHalf == 0 ? tid / (J * 4) : 0;
+    const int eq = kHalf == 0 ? (tid / J) & 3 : (tid / (J / 2)) & 3;
+    const bool elive = kHalf == 0 ? (et == 0 || two) : tid < J / 2 * 4;
     Frag hv[MT][NBR];
     int cr[MT];
     uint32_t ho[MT];
@@ -1569,18 +1607,23 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     for (int t = 0; t < MT; ++t)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[t][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // the accumulators and recurrent weights of the step's units
+    auto step_acc = [&](int t) __attribute__((always_inline)) -> floatx4 (&)[NTS] {
+      return *reinterpret_cast<floatx4 (*)[NTS]>(&acc[t][NT0]);
+    };
+    auto step_wr = [&](int b) __attribute__((always_inline)) -> const float4 (&)[NTS] {
+      return *reinterpret_cast<const float4 (*)[NTS]>(&wr[b][NT0]);
+    };
     float pv[4];                             // hoisted: W x + b of the thread's four outputs
     if constexpr (kHoisted) {
       // 1. (hoisted) the step's input products, computed before the level
       // loop, for the epilogue's four outputs of this thread, then every
       // child-state fragment of the step at once: there is no input part to
       // place them in
-      const int j = tid & (J - 1), t = tid / (J * 4), q = (tid / J) & 3;
-      const bool live_t = t == 0 || two;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int row = st[2 + (t & 1)] + 4 * q + v;
-        pv[v] = as_float(pin.load1((live_t && row < lend) ? (uint32_t)(row * H + hbase + j) * 4u : kNoSource));
+        const int row = st[2 + et] + 4 * eq + v;
+        pv[v] = as_float(pin.load1((elive && row < lend) ? (uint32_t)(row * H + hbase + ej) * 4u : kNoSource));
       }
 #pragma unroll
       for (int k = 0; k < NBR; ++k) {
@@ -1606,13 +1649,13 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       const float *bx = &Wx_s[i16 * LDX + xcol + 4 * g4];
 #pragma unroll
       for (int b = 0; b < NBX; ++b) {
-        float4 wv[NT];
+        float4 wv[NTS];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) wv[nt] = *(const float4 *)(bx + nt * 16 * LDX + 16 * b);
+        for (int nt = 0; nt < NTS; ++nt) wv[nt] = *(const float4 *)(bx + (NT0 + nt) * 16 * LDX + 16 * b);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          mfma_kstep_xn<NT>(k, as_float4(xc[0][b]), wv, acc[0]);
-          if (two) mfma_kstep_xn<NT>(k, as_float4(xc[1][b]), wv, acc[1]);
+          mfma_kstep_xn<NTS>(k, as_float4(xc[0][b]), wv, step_acc(0));
+          if (two) mfma_kstep_xn<NTS>(k, as_float4(xc[1][b]), wv, step_acc(1));
           if (b == 0) {
             static_assert(MT * NBX == 4, "one next-step input load per MFMA step");
             xn[k / NBX][k % NBX] = xin.load4(xo_next[k / NBX] + 64u * (k % NBX));
@@ -1669,7 +1712,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     // 3. recurrent part
 #pragma unroll
     for (int b = 0; b < NBR; ++b) {
-      mfma_k16_xn<NT>(hv[0][b].value(true), wr[b], acc[0]);
+      mfma_k16_xn<NTS>(hv[0][b].value(true), step_wr(b), step_acc(0));
       if (!kHoisted && two) {
         hv[1][b].lo = hs.load2_at(ho[1] + 128u * b);
         hv[1][b].hi = hs.load2_at(ho[1] + 128u * b + 16u);
@@ -1678,7 +1721,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     if (two) {
       wait_tile(1);
 #pragma unroll
-      for (int b = 0; b < NBR; ++b) mfma_k16_xn<NT>(hv[1][b].value(true), wr[b], acc[1]);
+      for (int b = 0; b < NBR; ++b) mfma_k16_xn<NTS>(hv[1][b].value(true), step_wr(b), step_acc(1));
     }
     CORTEX_TRACE_WAVE(l);
     // the next step's input fragments are complete before this step's stores
@@ -1692,25 +1735,23 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     for (int t = 0; t < MT; ++t)
       if (t == 0 || two)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int nt = NT0; nt < NT0 + NTS; ++nt) {
           const int c = nt * 16 + i16;
           *(floatx4 *)&C_s[((wave * MT + t) * J + c) * kTileM + 4 * (g4 ^ ((c >> 2) & 3))] = acc[t][nt];
         }
     __syncthreads();
     CORTEX_TRACE_POINT(l, 3);
     if (stop_s) return true;               // a wave gave up its wait: every wave stops here
-    // epilogue: thread (unit j, row quarter q of tile t) sums the eight
+    // epilogue: thread (unit ej, row quarter eq of tile et) sums the eight
     // partial sums of four rows, bias first, and writes them; every output of
     // the thread first, then the stores (a store's data registers are not
     // reused while earlier stores are in flight)
     static_assert(EPI == 4 && kFwdThreads == J * MT * 4, "one row quarter of one tile per thread");
-    const int j = tid & (J - 1), t = tid / (J * 4), q = (tid / J) & 3;
-    const bool live_t = t == 0 || two;
-    floatx4 sum = kHoisted ? floatx4{pv[0], pv[1], pv[2], pv[3]} : floatx4{bias_s[j], bias_s[j], bias_s[j], bias_s[j]};
-    if (live_t) {
+    floatx4 sum = kHoisted ? floatx4{pv[0], pv[1], pv[2], pv[3]} : floatx4{bias_s[ej], bias_s[ej], bias_s[ej], bias_s[ej]};
+    if (elive) {
 #pragma unroll
       for (int w = 0; w < kFwdWaves; ++w) {
-        const floatx4 p = *(const floatx4 *)&C_s[((w * MT + t) * J + j) * kTileM + 4 * (q ^ ((j >> 2) & 3))];
+        const floatx4 p = *(const floatx4 *)&C_s[((w * MT + et) * J + ej) * kTileM + 4 * (eq ^ ((ej >> 2) & 3))];
 #pragma unroll
         for (int v = 0; v < 4; ++v) sum[v] += p[v];
       }
@@ -1722,9 +1763,9 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     uint32_t el[EPI];
 #pragma unroll
     for (int v = 0; v < EPI; ++v) {
-      const int row = st[2 + (t & 1)] + 4 * q + v;
+      const int row = st[2 + et] + 4 * eq + v;
       hv_out[v] = tanh_f(sum[v]);
-      el[v] = (live_t && row < lend) ? (uint32_t)(row * H + hbase + j) : 0xFFFFFFFFu;
+      el[v] = (elive && row < lend) ? (uint32_t)(row * H + hbase + ej) : 0xFFFFFFFFu;
     }
     // the tagged pairs (what the next level waits for) first, then the outputs
 #pragma unroll
@@ -1735,6 +1776,16 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       if (el[v] != 0xFFFFFFFFu) a.h[el[v]] = hv_out[v];
     CORTEX_TRACE_POINT(l, 4);
     return false;
+  };
+
+  // a step of its recorded units
+  auto step_of = [&](const int *st, const u32x4 (&xc)[MT][NBX], const int *nst,
+                     u32x4 (&xn)[MT][NBX]) __attribute__((always_inline)) -> bool {
+    switch (st[5]) {
+      case 1: return run_step(std::integral_constant<int, 1>{}, st, xc, nst, xn);
+      case 2: return run_step(std::integral_constant<int, 2>{}, st, xc, nst, xn);
+      default: return run_step(std::integral_constant<int, 0>{}, st, xc, nst, xn);
+    }
   };
 
   u32x4 xa[MT][NBX], xb[MT][NBX];
@@ -1750,14 +1801,39 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
 #pragma unroll
         for (int b = 0; b < NBX; ++b) settle(xa[t][b]);
     }
-    for (int e = 0; e < total; e += 2) {
-      CORTEX_TRACE_POINT(step(e)[0], 0);
-      if (run_step(step(e), xa, e + 1 < total ? step(e + 1) : nullptr, xb)) return;
-      CORTEX_TRACE_POINT(step(e)[0], 5);
-      if (e + 1 >= total) break;
-      CORTEX_TRACE_POINT(step(e + 1)[0], 0);
-      if (run_step(step(e + 1), xb, e + 2 < total ? step(e + 2) : nullptr, xa)) return;
-      CORTEX_TRACE_POINT(step(e + 1)[0], 5);
+    // Steps of one kind (whole or half) run in a loop of their own, entered
+    // with no load in flight: a loop entered with another kind's loads
+    // pending would wait for them on every iteration, since the compiler's
+    // wait counts merge every path into the loop.
+    int e = 0;
+    auto run_kind = [&](auto half_c) __attribute__((always_inline)) -> bool {
+      constexpr int kKind = decltype(half_c)::value;
+      for (;;) {
+        CORTEX_TRACE_POINT(step(e)[0], 0);
+        if (run_step(half_c, step(e), xa, e + 1 < total ? step(e + 1) : nullptr, xb)) return true;
+        CORTEX_TRACE_POINT(step(e)[0], 5);
+        if (++e >= total) return false;
+        if (step(e)[5] != kKind) {
+          // the next step's input fragments are in xb; the next run reads xa
+#pragma unroll
+          for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int b = 0; b < NBX; ++b) xa[t][b] = xb[t][b];
+          return false;
+        }
+        CORTEX_TRACE_POINT(step(e)[0], 0);
+        if (run_step(half_c, step(e), xb, e + 1 < total ? step(e + 1) : nullptr, xa)) return true;
+        CORTEX_TRACE_POINT(step(e)[0], 5);
+        if (++e >= total || step(e)[5] != kKind) return false;
+      }
+    };
+    while (e < total) {
+      __builtin_amdgcn_s_waitcnt(kWaitVmcntZero);
+      const int kind = step(e)[5];
+      const bool stop = kind == 1   ? run_kind(std::integral_constant<int, 1>{})
+                        : kind == 2 ? run_kind(std::integral_constant<int, 2>{})
+                                    : run_kind(std::integral_constant<int, 0>{});
+      if (stop) return;
     }
   } else {
     // the list does not fit: walk the levels, staging one step's sources at
@@ -1767,8 +1843,8 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     for (int l = a.level_lo; l < L && l < a.level_hi; ++l) {
       CORTEX_TRACE_POINT(l, 0);
       const int r0 = off[l], r1 = off[l + 1];
-      int uf;
-      const int cnt = dag_group_tiles(group, l, Q, (r1 - r0 + kTileM - 1) / kTileM, uf);
+      int uf, half;
+      const int cnt = dag_group_tiles(group, l, Q, (r1 - r0 + kTileM - 1) / kTileM, uf, half);
       for (int k = 0; k < cnt; k += MT) {
         __syncthreads();                // the previous step's sources are no longer read
         if (tid == 0) {
@@ -1777,6 +1853,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
           st[2] = r0 + kTileM * (uf + k * Q);
           st[3] = k + 1 < cnt ? r0 + kTileM * (uf + (k + 1) * Q) : -1;
           st[4] = r1;
+          st[5] = half;
         }
         __syncthreads();
         int bad_codes = 0;
@@ -1787,7 +1864,7 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
           return;
         }
         if constexpr (!kHoisted) issue_x(st, xa, true);
-        if (run_step(st, xa, nullptr, xb)) return;
+        if (step_of(st, xa, nullptr, xb)) return;
       }
       CORTEX_TRACE_POINT(l, 5);
     }

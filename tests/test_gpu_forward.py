@@ -280,6 +280,24 @@ def test_dag_two_tile_steps_ragged(groups):
     compare_states(dw.states_by_node(), O.forward_workload(wl), "dag two-tile groups %d" % groups)
 
 
+@pytest.mark.parametrize("groups,n_grids,side", [(16, 8, 24), (64, 3, 20), (2, 6, 32), (5, 4, 12)])
+def test_dag_half_steps(groups, n_grids, side):
+    """Levels of at most groups/2 tiles run as half steps (two groups per
+    tile, 32 units each): 8 grids of 24x24 over 16 groups mix half levels
+    (up to 128 rows) with whole ones, so groups change kind of step at
+    either parity of their step lists; 3 grids of 20x20 over 64 groups are
+    half steps throughout; 2 groups over 6 grids of 32x32 overflow the step
+    list, so the level walk takes the half steps of the one-tile levels;
+    an odd group count (5) never splits.  Ragged tiles throughout; against
+    the oracle."""
+    wl = I.dagrnn_workload(90 + groups, n_grids=n_grids, rows=side, cols=side, H=256)
+    announce("dag half steps groups %d N=%d" % (groups, wl.N))
+    C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 64)
+    dw = run(wl, groups)
+    assert C.cortex_last_grid(1) == 4 * groups
+    compare_states(dw.states_by_node(), O.forward_workload(wl), "dag half steps groups %d" % groups)
+
+
 def test_dag_tile_list_overflow():
     """One node group over 6 grids of 32x32: the group's tiles exceed the
     per-workgroup tile list, so the kernel walks the levels and stages each
