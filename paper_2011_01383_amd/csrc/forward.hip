@@ -1234,8 +1234,9 @@ __global__ void __launch_bounds__(kFwdThreads) tree_rnn_lds_kernel(FwdArgs a) {
 // and last levels of a batch, whose chain of waits sets the pace, take half
 // the contraction time per group.  At entry each workgroup lists its steps of
 // every level with their operand sources in LDS, so the level loop never
-// goes back to the linearization in memory; a group whose list does not fit
-// walks the levels instead, staging one step's sources at a time.
+// goes back to the linearization in memory; a group with more steps than the
+// list holds (60) lists them a chunk at a time, the next chunk once it has
+// run the previous one.
 // ---------------------------------------------------------------------------
 constexpr int kDagH = 256, kDagJ = 64, kDagS = kDagH / kDagJ;
 constexpr int kDagWideMinRows = 6144;              // default choice of this kernel (measured crossover)
@@ -1331,18 +1332,6 @@ __device__ __forceinline__ bool dag_store_codes(const FwdArgs &a, int *st, int s
   cd[1] = c0;
   cd[2] = c1;
   return ok;
-}
-
-// Reads and stores the operand sources of a slot.
-__device__ __forceinline__ bool dag_fill_codes(const FwdArgs &a, int *st, int slot) {
-  const int row = dag_slot_row(st, slot);
-  int v = -1, c0 = -1, c1 = -1;
-  if (row >= 0) {
-    v = a.level_nodes[row];
-    c0 = a.child_rows[(size_t)row * 2];
-    c1 = a.child_rows[(size_t)row * 2 + 1];
-  }
-  return dag_store_codes(a, st, slot, row >= 0, v, c0, c1);
 }
 
 // Hoisted input products of the DAG-RNN at H = 256 (the ablation of the
@@ -1465,47 +1454,54 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     return;
   }
 
-  // ---- this group's steps of every level, one level per thread per round ----
-  int total = 0, bad = 0;
-  for (int lb = 0; lb < L; lb += kFwdThreads) {
-    const int l = lb + tid;
-    int nst = 0, r0 = 0, r1 = 0, uf = 0, cnt = 0, half = 0;
-    if (l < L) {
-      r0 = a.level_offsets[l];
-      r1 = a.level_offsets[l + 1];
-      const bool ok = r0 >= 0 && r1 >= r0 && r1 <= N && (l != 0 || r0 == 0) && (l != L - 1 || r1 == N);
-      if (!ok) bad = 1;
-      const int ntile = (ok && l >= a.level_lo && l < a.level_hi) ? (r1 - r0 + kTileM - 1) / kTileM : 0;
-      cnt = dag_group_tiles(group, l, Q, ntile, uf, half);
-      nst = (cnt + MT - 1) / MT;
+  // ---- this group's steps of every level, one level per thread per round:
+  // the list holds steps [first, first + kDagStepCap) of them; returns the
+  // group's step count.  A group with more steps runs them in chunks,
+  // listing the next chunk once it has run the previous one.
+  auto list_steps = [&](int first, int &bad) __attribute__((always_inline)) -> int {
+    int total = 0;
+    for (int lb = 0; lb < L; lb += kFwdThreads) {
+      const int l = lb + tid;
+      int nst = 0, r0 = 0, r1 = 0, uf = 0, cnt = 0, half = 0;
+      if (l < L) {
+        r0 = a.level_offsets[l];
+        r1 = a.level_offsets[l + 1];
+        const bool ok = r0 >= 0 && r1 >= r0 && r1 <= N && (l != 0 || r0 == 0) && (l != L - 1 || r1 == N);
+        if (!ok) bad = 1;
+        const int ntile = (ok && l >= a.level_lo && l < a.level_hi) ? (r1 - r0 + kTileM - 1) / kTileM : 0;
+        cnt = dag_group_tiles(group, l, Q, ntile, uf, half);
+        nst = (cnt + MT - 1) / MT;
+      }
+      int round_total;
+      const int pos = total + block_excl_scan(nst, wsum, &round_total) - first;
+      for (int j = max(0, -pos); j < nst && pos + j < kDagStepCap; ++j) {
+        int *st = &list[(pos + j) * SI];
+        st[0] = l;
+        st[1] = r0;
+        st[2] = r0 + kTileM * (uf + (MT * j) * Q);
+        st[3] = MT * j + 1 < cnt ? r0 + kTileM * (uf + (MT * j + 1) * Q) : -1;
+        st[4] = r1;
+        st[5] = half;
+      }
+      total += round_total;
     }
-    int round_total;
-    const int pos = total + block_excl_scan(nst, wsum, &round_total);
-    for (int j = 0; j < nst && pos + j < kDagStepCap; ++j) {
-      int *st = &list[(pos + j) * SI];
-      st[0] = l;
-      st[1] = r0;
-      st[2] = r0 + kTileM * (uf + (MT * j) * Q);
-      st[3] = MT * j + 1 < cnt ? r0 + kTileM * (uf + (MT * j + 1) * Q) : -1;
-      st[4] = r1;
-      st[5] = half;
-    }
-    total += round_total;
-  }
+    return total;
+  };
+  int bad = 0;
+  const int total = list_steps(0, bad);
   // (each level's end is the next level's start, so the levels tile [0, N))
   if (__syncthreads_or(bad)) {
     raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
     return;
   }
-  const bool listed = total <= kDagStepCap;
+  int listed = min(total, kDagStepCap);        // steps in the list
   // operand sources of every listed slot: requested now, stored below
   constexpr int kFillPer = (kDagStepCap * kDagStepRows + kFwdThreads - 1) / kFwdThreads;
   int frow[kFillPer], fv[kFillPer], f0[kFillPer], f1[kFillPer];
 #pragma unroll
   for (int k = 0; k < kFillPer; ++k) {
     const int idx = tid + k * kFwdThreads;
-    frow[k] = (listed && idx < total * kDagStepRows) ? dag_slot_row(&list[(idx / kDagStepRows) * SI], idx % kDagStepRows)
-                                                     : -1;
+    frow[k] = idx < listed * kDagStepRows ? dag_slot_row(&list[(idx / kDagStepRows) * SI], idx % kDagStepRows) : -1;
     fv[k] = f0[k] = f1[k] = -1;
     if (frow[k] >= 0) {
       fv[k] = a.level_nodes[frow[k]];
@@ -1530,14 +1526,12 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     }
     if (tid < J) bias_s[tid] = a.b[hbase + tid];
   }
-  if (listed) {
 #pragma unroll
-    for (int k = 0; k < kFillPer; ++k) {
-      const int idx = tid + k * kFwdThreads;
-      if (idx < total * kDagStepRows &&
-          !dag_store_codes(a, &list[(idx / kDagStepRows) * SI], idx % kDagStepRows, frow[k] >= 0, fv[k], f0[k], f1[k]))
-        bad = 1;
-    }
+  for (int k = 0; k < kFillPer; ++k) {
+    const int idx = tid + k * kFwdThreads;
+    if (idx < listed * kDagStepRows &&
+        !dag_store_codes(a, &list[(idx / kDagStepRows) * SI], idx % kDagStepRows, frow[k] >= 0, fv[k], f0[k], f1[k]))
+      bad = 1;
   }
   if constexpr (!kHoisted) {
 #pragma unroll
@@ -1778,23 +1772,14 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
     return false;
   };
 
-  // a step of its recorded units
-  auto step_of = [&](const int *st, const u32x4 (&xc)[MT][NBX], const int *nst,
-                     u32x4 (&xn)[MT][NBX]) __attribute__((always_inline)) -> bool {
-    switch (st[5]) {
-      case 1: return run_step(std::integral_constant<int, 1>{}, st, xc, nst, xn);
-      case 2: return run_step(std::integral_constant<int, 2>{}, st, xc, nst, xn);
-      default: return run_step(std::integral_constant<int, 0>{}, st, xc, nst, xn);
-    }
-  };
-
   u32x4 xa[MT][NBX], xb[MT][NBX];
-  if (listed) {
-    // one flat pass over this group's steps, level after level
-    auto step = [&](int e) __attribute__((always_inline)) -> const int * { return &list[e * SI]; };
+  // one flat pass over this group's steps, level after level, a listed chunk
+  // at a time
+  auto step = [&](int e) __attribute__((always_inline)) -> const int * { return &list[e * SI]; };
+  for (int first = 0;;) {
     // two steps per iteration, written out, so each step's input fragments
     // stay in fixed registers (xa, xb) rather than being selected at run time
-    if (!kHoisted && total > 0) {
+    if (!kHoisted && listed > 0) {
       issue_x(step(0), xa, true);
 #pragma unroll
       for (int t = 0; t < MT; ++t)
@@ -1810,9 +1795,9 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
       constexpr int kKind = decltype(half_c)::value;
       for (;;) {
         CORTEX_TRACE_POINT(step(e)[0], 0);
-        if (run_step(half_c, step(e), xa, e + 1 < total ? step(e + 1) : nullptr, xb)) return true;
+        if (run_step(half_c, step(e), xa, e + 1 < listed ? step(e + 1) : nullptr, xb)) return true;
         CORTEX_TRACE_POINT(step(e)[0], 5);
-        if (++e >= total) return false;
+        if (++e >= listed) return false;
         if (step(e)[5] != kKind) {
           // the next step's input fragments are in xb; the next run reads xa
 #pragma unroll
@@ -1822,12 +1807,12 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
           return false;
         }
         CORTEX_TRACE_POINT(step(e)[0], 0);
-        if (run_step(half_c, step(e), xb, e + 1 < total ? step(e + 1) : nullptr, xa)) return true;
+        if (run_step(half_c, step(e), xb, e + 1 < listed ? step(e + 1) : nullptr, xa)) return true;
         CORTEX_TRACE_POINT(step(e)[0], 5);
-        if (++e >= total || step(e)[5] != kKind) return false;
+        if (++e >= listed || step(e)[5] != kKind) return false;
       }
     };
-    while (e < total) {
+    while (e < listed) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcntZero);
       const int kind = step(e)[5];
       const bool stop = kind == 1   ? run_kind(std::integral_constant<int, 1>{})
@@ -1835,38 +1820,36 @@ __global__ void __launch_bounds__(kFwdThreads) dag_slice64_kernel(FwdArgs a) {
                                     : run_kind(std::integral_constant<int, 0>{});
       if (stop) return;
     }
-  } else {
-    // the list does not fit: walk the levels, staging one step's sources at
-    // a time in the first list entry
-    int *st = list;
-    const int *off = a.level_offsets;
-    for (int l = a.level_lo; l < L && l < a.level_hi; ++l) {
-      CORTEX_TRACE_POINT(l, 0);
-      const int r0 = off[l], r1 = off[l + 1];
-      int uf, half;
-      const int cnt = dag_group_tiles(group, l, Q, (r1 - r0 + kTileM - 1) / kTileM, uf, half);
-      for (int k = 0; k < cnt; k += MT) {
-        __syncthreads();                // the previous step's sources are no longer read
-        if (tid == 0) {
-          st[0] = l;
-          st[1] = r0;
-          st[2] = r0 + kTileM * (uf + k * Q);
-          st[3] = k + 1 < cnt ? r0 + kTileM * (uf + (k + 1) * Q) : -1;
-          st[4] = r1;
-          st[5] = half;
-        }
-        __syncthreads();
-        int bad_codes = 0;
-        for (int s = tid; s < kDagStepRows; s += kFwdThreads)
-          if (!dag_fill_codes(a, st, s)) bad_codes = 1;
-        if (__syncthreads_or(bad_codes)) {
-          raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
-          return;
-        }
-        if constexpr (!kHoisted) issue_x(st, xa, true);
-        if (step_of(st, xa, nullptr, xb)) return;
+    first += kDagStepCap;
+    if (first >= total) break;
+    // the next chunk: every wave is done with this one's records
+    __syncthreads();
+    int bad_chunk = 0;
+    list_steps(first, bad_chunk);
+    listed = min(total - first, kDagStepCap);
+    __syncthreads();                           // the step records are written
+    int crow[kFillPer], cv[kFillPer], c0[kFillPer], c1[kFillPer];
+#pragma unroll
+    for (int k = 0; k < kFillPer; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      crow[k] = idx < listed * kDagStepRows ? dag_slot_row(&list[(idx / kDagStepRows) * SI], idx % kDagStepRows) : -1;
+      cv[k] = c0[k] = c1[k] = -1;
+      if (crow[k] >= 0) {
+        cv[k] = a.level_nodes[crow[k]];
+        c0[k] = a.child_rows[(size_t)crow[k] * 2];
+        c1[k] = a.child_rows[(size_t)crow[k] * 2 + 1];
       }
-      CORTEX_TRACE_POINT(l, 5);
+    }
+#pragma unroll
+    for (int k = 0; k < kFillPer; ++k) {
+      const int idx = tid + k * kFwdThreads;
+      if (idx < listed * kDagStepRows &&
+          !dag_store_codes(a, &list[(idx / kDagStepRows) * SI], idx % kDagStepRows, crow[k] >= 0, cv[k], c0[k], c1[k]))
+        bad_chunk = 1;
+    }
+    if (__syncthreads_or(bad_chunk)) {
+      raise_status(a.status, CORTEX_ST_BAD_LINEARIZATION);
+      return;
     }
   }
   CORTEX_TRACE_KERNEL(3);

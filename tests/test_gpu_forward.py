@@ -287,7 +287,8 @@ def test_dag_half_steps(groups, n_grids, side):
     (up to 128 rows) with whole ones, so groups change kind of step at
     either parity of their step lists; 3 grids of 20x20 over 64 groups are
     half steps throughout; 2 groups over 6 grids of 32x32 overflow the step
-    list, so the level walk takes the half steps of the one-tile levels;
+    list, so the half steps of the one-tile levels fall in its first and
+    last chunks;
     an odd group count (5) never splits.  Ragged tiles throughout; against
     the oracle."""
     wl = I.dagrnn_workload(90 + groups, n_grids=n_grids, rows=side, cols=side, H=256)
@@ -299,9 +300,9 @@ def test_dag_half_steps(groups, n_grids, side):
 
 
 def test_dag_tile_list_overflow():
-    """One node group over 6 grids of 32x32: the group's tiles exceed the
-    per-workgroup tile list, so the kernel walks the levels and stages each
-    chunk's sources instead; against the oracle."""
+    """One node group over 6 grids of 32x32: the group's steps (several per
+    level) exceed the per-workgroup step list many times over, so the kernel
+    lists and runs them a chunk at a time; against the oracle."""
     wl = I.dagrnn_workload(78, n_grids=6, rows=32, cols=32, H=256)
     announce("dag tile-list overflow N=%d" % wl.N)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, 64)
