@@ -456,6 +456,56 @@ def unroll_study(args):
         C.cortex_set_knob(C.CORTEX_KNOB_TREE_UNROLL, 0)
 
 
+def dag_batches(args):
+    """DAG-RNN at H = 256 over growing batches of 32 x 32 grids (the paper's
+    DAG-RNN cell, Sec. 7.1; 16 to 512 grids, 16,384 to 524,288 nodes, all 63
+    levels): the forward kernel and the step (cortex_dag_infer: linearizer,
+    then forward), each averaged over back-to-back launches between two
+    events (the median of three rounds), and the forward's algorithmic rate
+    against the fp32 peak.  One JSON line per batch.  Larger batches give each node group more steps
+    per level, so the per-level exchange is spread over more work."""
+    import torch
+    from paper_2011_01383_amd import inputs as I
+    from paper_2011_01383_amd.runner import DeviceWorkload
+    stream = torch.cuda.current_stream()
+    n = max(5, min(args.steps, 50))
+
+    def timed(fn):
+        # the median of three rounds of n launches each
+        for _ in range(max(args.warmup, 5)):
+            fn()
+        torch.cuda.synchronize()
+        rounds = []
+        for _ in range(3):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(n):
+                fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            rounds.append(a.elapsed_time(b) / n)
+        return sorted(rounds)[1]
+
+    for grids in (16, 32, 64, 128, 256, 512):
+        wl = I.dagrnn_workload(I.BASE_SEED + 2000 + grids, n_grids=grids)
+        dw = DeviceWorkload(wl)
+        dw.step()
+        torch.cuda.synchronize()
+        assert dw.status_code() == 0
+        fwd = timed(dw.forward)
+        step = timed(dw.step)
+        assert dw.status_code() == 0
+        flops, _ = algorithmic_work(wl)
+        print(json.dumps({"workload": wl.name, "grids": grids, "nodes": wl.N, "levels": int(dw.lin_host()["num_levels"]),
+                          "forward_ms": fwd, "step_ms": step, "nodes_per_s": wl.N / (step * 1e-3),
+                          "forward_tflops": flops / (fwd * 1e-3) * 1e-12,
+                          "forward_frac": flops / (fwd * 1e-3) * 1e-12 / PEAK_FP32_TFLOPS}))
+        sys.stdout.flush()
+        del dw
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -478,6 +528,8 @@ def main():
                     help="forward time under each level-ordering mode; one JSON line per (workload, mode)")
     ap.add_argument("--unroll", action="store_true",
                     help="TreeRNN H = 64 batches under each unrolling schedule; one JSON line per (batch, schedule)")
+    ap.add_argument("--dag-batches", action="store_true",
+                    help="DAG-RNN H = 256 over 16 to 512 grids of 32x32; one JSON line per batch")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -512,6 +564,9 @@ def main():
         return
     if args.unroll:
         unroll_study(args)
+        return
+    if args.dag_batches:
+        dag_batches(args)
         return
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_NODE_GROUPS, args.node_groups)
     C.cortex_set_knob(C.CORTEX_KNOB_FWD_SLICE_UNITS, args.slice_units)
