@@ -245,3 +245,46 @@ def test_single_wave_errors():
     big = np.full(128 * 4, -1, dtype=np.int32)
     big[127 * 4 + 3] = 128                                               # last slot of the last node
     assert gpu_linearize(big, 4, 0)[0] == C.CORTEX_ST_CHILD_RANGE
+
+
+def test_multi_workgroup_node_limit():
+    """Batches beyond one workgroup run on co-resident 1,024-thread
+    workgroups, one per compute unit at the kernel's register use, each
+    holding at most 8,192 nodes.  A batch at that limit (grids of 32x32)
+    linearizes, checked node by node against the grid's closed forms:
+    height(i, j) = i + j, 63 levels, rows in (height, id) order and the
+    children's rows; one node more returns CORTEX_E_TOO_LARGE with nothing
+    enqueued (the status word stays 0)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    limit = cus * 8192
+    one = I.grid_children(1, 32, 32).reshape(1024, 2)
+    grids = limit // 1024
+    off = (np.arange(grids, dtype=np.int64) * 1024)[:, None, None]
+    ch = np.where(one[None] >= 0, one[None] + off, -1).astype(np.int32).reshape(-1)
+    announce("linearize at the node limit N=%d" % limit)
+    st, got, _ = gpu_linearize(ch, 2)
+    assert st == 0
+    assert C.cortex_last_grid(0) == cus
+    ids = np.arange(limit)
+    h = (ids % 1024) // 32 + ids % 32
+    np.testing.assert_array_equal(got["height"], h)
+    assert int(got["num_levels"]) == 63
+    per_level = np.bincount(h, minlength=63)
+    np.testing.assert_array_equal(got["level_offsets"], np.concatenate([[0], np.cumsum(per_level)]))
+    order = np.argsort(h, kind="stable")
+    np.testing.assert_array_equal(got["level_nodes"], order)
+    row = np.empty(limit, np.int64)
+    row[order] = np.arange(limit)
+    np.testing.assert_array_equal(got["node_row"], row)
+    kids = ch.reshape(limit, 2)[order]
+    want = np.where(kids >= 0, row[np.maximum(kids, 0)], -1)
+    np.testing.assert_array_equal(got["child_rows"].reshape(limit, 2), want)
+
+    N = limit + 1
+    children = torch.from_numpy(np.concatenate([ch, [-1, -1]]).astype(np.int32)).cuda()
+    lin = C.Linearization.alloc(N, 2)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = C.workspace(C.cortex_linearize_workspace_bytes(N, 2))
+    assert C.cortex_linearize(children, N, 2, lin, status, ws) == C.CORTEX_E_TOO_LARGE
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
