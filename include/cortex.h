@@ -171,10 +171,11 @@ size_t cortex_linearize_workspace_bytes(int32_t N, int32_t K);
  * and 4) runs on co-resident workgroups of 1,024 threads, each holding at
  * most 8,192 nodes: CORTEX_E_TOO_LARGE when the GPU cannot hold enough of
  * them (one per compute unit at the kernel's register use: 2,097,152 nodes
- * on 256 CUs).  Up to one radix tile of 1,024 nodes per workgroup (262,144
- * nodes on 256 CUs) each workgroup keeps its nodes' children in registers;
- * larger batches take several height rounds and cost about 2.5 times as
- * much per node (524,288 nodes: 216 us against 41 us for 262,144).
+ * on 256 CUs).  While each workgroup can own one radix tile of 1,024 nodes
+ * (up to 524,288 nodes on 256 CUs, two workgroups per unit beyond 262,144)
+ * it keeps its nodes' children in registers; larger batches take several
+ * height rounds and cost about three times as much per node (655,360
+ * nodes: 315 us, against 95 us for 524,288).
  */
 int cortex_linearize(const int32_t *d_children, int32_t N, int32_t K, const cortex_lin_t *lin,
                      int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream);

@@ -76,7 +76,11 @@ __device__ __forceinline__ int block_max(int v, int *tmp) {
   } while (0)
 #endif
 
-__global__ void __launch_bounds__(kLinThreads) linearize_kernel(LinArgs a) {
+// kDual: compiled for two workgroups per compute unit (8 waves per SIMD, 64
+// VGPRs, a few spilled), the instance for batches of more radix tiles than
+// one workgroup per compute unit can hold one tile each.
+template <bool kDual>
+__global__ void __launch_bounds__(kLinThreads, kDual ? 8 : 1) linearize_kernel(LinArgs a) {
   __shared__ int hs[kMaxChunk];
   __shared__ int cnt[kSubs][256];
   __shared__ int hist[256];
@@ -525,10 +529,23 @@ int linearize_impl(const int32_t *d_children, int32_t N, int32_t K, const cortex
     set_last_grid(0, 1);
     return launch_persistent(linearize_small_kernel, 1, kSmallThreads, small_lds, s, stream);
   }
-  int cap = max_coresident(linearize_kernel, kLinThreads);
+  int cap = max_coresident(linearize_kernel<false>, kLinThreads);
   if (cap <= 0) return CORTEX_E_HIP;
   int64_t g = knob(CORTEX_KNOB_LIN_BLOCKS);
-  if (g <= 0) g = (N + kTargetChunk - 1) / kTargetChunk;
+  // one radix tile per workgroup keeps every node's children in registers:
+  // where one workgroup per compute unit cannot give each tile its own, the
+  // two-per-unit instance can (up to twice as many tiles)
+  bool dual = false;
+  if (g <= 0) {
+    g = (N + kTargetChunk - 1) / kTargetChunk;
+    if (g > cap && g <= kMaxGrid) {
+      const int cap2 = max_coresident(linearize_kernel<true>, kLinThreads);
+      if (g <= cap2) {
+        dual = true;
+        cap = cap2;
+      }
+    }
+  }
   const int64_t g_min = (N + kMaxChunk - 1) / kMaxChunk;
   if (g < g_min) g = g_min;
   if (g > N) g = N;
@@ -562,7 +579,8 @@ int linearize_impl(const int32_t *d_children, int32_t N, int32_t K, const cortex
   a.chunk = g == (int64_t)a.tiles ? kTile : (int32_t)((N + g - 1) / g);
   a.timeout = barrier_timeout_ticks();
   set_last_grid(0, (int32_t)g);
-  return launch_persistent(linearize_kernel, (int)g, kLinThreads, 0, a, stream);
+  return dual ? launch_persistent(linearize_kernel<true>, (int)g, kLinThreads, 0, a, stream)
+              : launch_persistent(linearize_kernel<false>, (int)g, kLinThreads, 0, a, stream);
 }
 
 }  // namespace cortex

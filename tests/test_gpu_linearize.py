@@ -247,25 +247,19 @@ def test_single_wave_errors():
     assert gpu_linearize(big, 4, 0)[0] == C.CORTEX_ST_CHILD_RANGE
 
 
-def test_multi_workgroup_node_limit():
-    """Batches beyond one workgroup run on co-resident 1,024-thread
-    workgroups, one per compute unit at the kernel's register use, each
-    holding at most 8,192 nodes.  A batch at that limit (grids of 32x32)
-    linearizes, checked node by node against the grid's closed forms:
-    height(i, j) = i + j, 63 levels, rows in (height, id) order and the
-    children's rows; one node more returns CORTEX_E_TOO_LARGE with nothing
-    enqueued (the status word stays 0)."""
-    cus = torch.cuda.get_device_properties(0).multi_processor_count
-    limit = cus * 8192
+def grid_batch(grids):
+    """Children of `grids` 32x32 grid DAGs (ids g*1024 + 32i + j)."""
     one = I.grid_children(1, 32, 32).reshape(1024, 2)
-    grids = limit // 1024
     off = (np.arange(grids, dtype=np.int64) * 1024)[:, None, None]
-    ch = np.where(one[None] >= 0, one[None] + off, -1).astype(np.int32).reshape(-1)
-    announce("linearize at the node limit N=%d" % limit)
-    st, got, _ = gpu_linearize(ch, 2)
-    assert st == 0
-    assert C.cortex_last_grid(0) == cus
-    ids = np.arange(limit)
+    return np.where(one[None] >= 0, one[None] + off, -1).astype(np.int32).reshape(-1)
+
+
+def check_grid_lin(got, ch):
+    """A linearization of grid DAGs against their closed forms, node by node:
+    height(i, j) = i + j, 63 levels, rows in (height, id) order and the
+    children's rows."""
+    N = ch.size // 2
+    ids = np.arange(N)
     h = (ids % 1024) // 32 + ids % 32
     np.testing.assert_array_equal(got["height"], h)
     assert int(got["num_levels"]) == 63
@@ -273,12 +267,53 @@ def test_multi_workgroup_node_limit():
     np.testing.assert_array_equal(got["level_offsets"], np.concatenate([[0], np.cumsum(per_level)]))
     order = np.argsort(h, kind="stable")
     np.testing.assert_array_equal(got["level_nodes"], order)
-    row = np.empty(limit, np.int64)
-    row[order] = np.arange(limit)
+    row = np.empty(N, np.int64)
+    row[order] = np.arange(N)
     np.testing.assert_array_equal(got["node_row"], row)
-    kids = ch.reshape(limit, 2)[order]
+    kids = ch.reshape(N, 2)[order]
     want = np.where(kids >= 0, row[np.maximum(kids, 0)], -1)
-    np.testing.assert_array_equal(got["child_rows"].reshape(limit, 2), want)
+    np.testing.assert_array_equal(got["child_rows"].reshape(N, 2), want)
+
+
+@pytest.mark.parametrize("kind", ["grids", "random"])
+def test_two_workgroups_per_cu_instance(kind):
+    """More radix tiles than compute units (and at most twice as many): the
+    linearizer's instance compiled for two workgroups per compute unit gives
+    each 1,024-node tile a workgroup of its own.  384 grids of 32x32 against
+    their closed forms, and a 300,000-node random DAG (children anywhere
+    below) bit-exact against the oracle."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if kind == "grids":
+        ch = grid_batch(384)
+    else:
+        ch = I.random_dag(np.random.default_rng(300), 300000, 2, p_absent=0.3)
+    N = ch.size // 2
+    tiles = (N + 1023) // 1024
+    assert cus < tiles <= 2 * cus
+    announce("linearize two per CU %s N=%d" % (kind, N))
+    st, got, _ = gpu_linearize(ch, 2)
+    assert st == 0
+    assert C.cortex_last_grid(0) == tiles
+    if kind == "grids":
+        check_grid_lin(got, ch)
+    else:
+        compare_lin(got, O.linearize(ch, 2), 2)
+
+
+def test_multi_workgroup_node_limit():
+    """Batches of more tiles than two per compute unit run on one co-resident
+    1,024-thread workgroup per compute unit, each holding at most 8,192
+    nodes.  A batch at that limit (grids of 32x32) linearizes, checked node
+    by node against the grids' closed forms; one node more returns
+    CORTEX_E_TOO_LARGE with nothing enqueued (the status word stays 0)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    limit = cus * 8192
+    ch = grid_batch(limit // 1024)
+    announce("linearize at the node limit N=%d" % limit)
+    st, got, _ = gpu_linearize(ch, 2)
+    assert st == 0
+    assert C.cortex_last_grid(0) == cus
+    check_grid_lin(got, ch)
 
     N = limit + 1
     children = torch.from_numpy(np.concatenate([ch, [-1, -1]]).astype(np.int32)).cuda()
