@@ -117,6 +117,23 @@ def test_dag_64_grids_two_launches():
     compare_states(dw.states_by_node(), cached_oracle(4, 0), wl.name)
 
 
+@pytest.mark.parametrize("grids", [128, 300])
+def test_dag_large_batches(grids):
+    """Batches beyond the headline's 64 grids of 32x32 through
+    cortex_dag_infer: at 128 grids (131,072 nodes) each node group has about
+    95 steps, more than its step list holds, so it runs them in listed
+    chunks; at 300 grids (307,200 nodes) the linearizer also takes its
+    instance with two workgroups per compute unit.  Every state against the
+    oracle."""
+    wl = I.dagrnn_workload(I.BASE_SEED + 3000 + grids, n_grids=grids)
+    announce("dag infer %d grids N=%d" % (grids, wl.N))
+    dw = DeviceWorkload(wl)
+    _states(dw)
+    dw.infer()
+    assert dw.status_code() == 0
+    compare_states(dw.states_by_node(), O.forward_workload(wl), wl.name)
+
+
 @pytest.mark.parametrize("groups", [1, 3])
 def test_fused_launch_node_groups(groups):
     wl = cached_workload(1, 2)
